@@ -1,0 +1,365 @@
+"""Pins for the fp64 oracle: checks against what the paper and the mathematics
+fix, independent of the oracle's own formulas.
+
+Each ``pin_*`` takes an oracle library handle and raises AssertionError on a
+mismatch, so the same battery runs against the real oracle (test_oracle.py)
+and against builds with a planted mistake (test_oracle_mutants.py), which it
+must reject.
+"""
+from __future__ import annotations
+
+import json
+import math
+import os
+
+import numpy as np
+
+import oracle
+from oracle import reach
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+EPS = json.load(open(os.path.join(GOLDEN, "defaults.json")))["eps"]
+
+
+# ---------------------------------------------------------------------------
+# independent references
+# ---------------------------------------------------------------------------
+def scan_membership(n: int, k: int, pi: int) -> np.ndarray:
+    """Brute-force membership scan: M[t, j] for every pair, straight from the
+    set definitions (eq. Nr causal, eq. Npi, eq. U); invalid positions dropped."""
+    M = np.zeros((n, n), dtype=bool)
+    for t in range(n):
+        for j in range(n):
+            in_window = max(0, t - k) <= j <= t
+            is_partner = j == t - pi
+            M[t, j] = in_window or is_partner
+    return M
+
+
+def rand_qkv(rng, B, H, N, D, dtype=np.float32):
+    return [rng.standard_normal((B, H, N, D)).astype(dtype) for _ in range(3)]
+
+
+def textbook_causal(q, k, v, scale):
+    """Dense causal scaled-dot-product attention (eqs. alpha and attn), fp64."""
+    q, k, v = (np.asarray(x, np.float64) for x in (q, k, v))
+    N = q.shape[-2]
+    S = (q @ np.swapaxes(k, -1, -2)) * scale
+    S = np.where(np.tril(np.ones((N, N), bool)), S, -np.inf)
+    S = S - S.max(-1, keepdims=True)
+    P = np.exp(S)
+    P /= P.sum(-1, keepdims=True)
+    return P @ v
+
+
+def logsumexp_masked(S, M):
+    S = np.where(M, S, -np.inf)
+    mx = S.max(-1, keepdims=True)
+    return (mx + np.log(np.exp(S - mx).sum(-1, keepdims=True)))[..., 0]
+
+
+def multiplicative_fusion(q, k, v, gate, kk, pi, scale):
+    """eq. (alphahat_adapt) in its multiplicative form: weights
+    omega_tj * exp(z_tj) normalised over U(t), omega = alpha~ on the window and
+    1 - alpha~ on the partner; mask from the brute-force scan.  fp64, dense."""
+    q, k, v = (np.asarray(x, np.float64) for x in (q, k, v))
+    B, H, N, D = q.shape
+    M = scan_membership(N, kk, pi)
+    window = np.zeros((N, N), bool)
+    for t in range(N):
+        window[t, max(0, t - kk):t + 1] = True
+    g = np.asarray(gate, np.float64)
+    g = np.broadcast_to(g[None, :, None] if g.shape == (H,) else g, (B, H, N))
+    a_t = EPS + (1 - 2 * EPS) / (1 + np.exp(-g))           # [B,H,N]
+    omega = np.where(window[None, None], a_t[..., None], (1 - a_t)[..., None])
+    Z = (q @ np.swapaxes(k, -1, -2)) * scale
+    W = np.where(M[None, None], omega * np.exp(Z), 0.0)
+    W /= W.sum(-1, keepdims=True)
+    return W @ v, W
+
+
+# ---------------------------------------------------------------------------
+# pins
+# ---------------------------------------------------------------------------
+IDX_CASES = [(1, 0, 0), (1, 3, 5), (7, 0, 1), (9, 2, 5), (16, 3, 3), (16, 3, 2), (16, 3, 4),
+             (20, 4, 16), (33, 5, 0), (40, 50, 7), (40, 6, 39), (40, 6, 40), (64, 8, 16)]
+
+
+def pin_index_set_scan(L):
+    """Working-set indices equal the brute-force membership scan, slot order
+    is window offsets -k..0 then the partner, and no index exceeds t."""
+    for n, k, pi in IDX_CASES:
+        idx = oracle.index_set(n, k, pi, L)
+        m = k + 1 + (1 if pi > k else 0)
+        assert idx.shape == (n, m), (n, k, pi, idx.shape)
+        M = scan_membership(n, k, pi)
+        for t in range(n):
+            got = idx[t][idx[t] >= 0]
+            assert len(set(got.tolist())) == len(got), "duplicate entry"
+            assert sorted(got.tolist()) == np.nonzero(M[t])[0].tolist(), (n, k, pi, t)
+            assert (got <= t).all()
+            for s in range(k + 1):
+                assert idx[t, s] == (t - k + s if t - k + s >= 0 else -1)
+            if m == k + 2:
+                assert idx[t, k + 1] == (t - pi if t >= pi else -1)
+
+
+def pin_working_set_sizes(L):
+    """|W_t| = min(t, k) + 1 + [pi > k and t >= pi] summed in closed form."""
+    for n, k, pi in [(256, 32, 64), (4096, 128, 256), (1000, 7, 3), (300, 299, 500)]:
+        idx = oracle.index_set(n, k, pi, L)
+        total = int((idx >= 0).sum())
+        if n > k:
+            closed = (k + 1) * (k + 2) // 2 + (n - k - 1) * (k + 1)
+        else:
+            closed = n * (n + 1) // 2
+        closed += max(0, n - pi) if pi > k else 0
+        assert total == closed, (n, k, pi, total, closed)
+
+
+def pin_dense_reduction(L):
+    """k >= N-1: every j <= t is in the window with one common prior, which
+    cancels in the softmax, so the result is dense causal attention (Sec. 3.1)
+    for any gate; lse = log alpha~ + logsumexp(z)."""
+    rng = np.random.default_rng(11)
+    B, H, N, D = 2, 3, 37, 16
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    gate = rng.uniform(-3, 3, H).astype(np.float32)
+    scale = 1 / math.sqrt(D)
+    ref = textbook_causal(q, k, v, scale)
+    for kk, pi in [(N - 1, 5), (N + 10, 0), (N - 1, N + 3)]:
+        out, lse = oracle.forward(q, k, v, gate, kk, pi, want_lse=True, L=L)
+        assert np.abs(out - ref).max() <= 1e-12, (kk, pi, np.abs(out - ref).max())
+        S = (q.astype(np.float64) @ np.swapaxes(k, -1, -2).astype(np.float64)) * scale
+        a_t = EPS + (1 - 2 * EPS) / (1 + np.exp(-gate.astype(np.float64)))
+        lse_ref = np.log(a_t)[None, :, None] + logsumexp_masked(S, np.tril(np.ones((N, N), bool)))
+        assert np.abs(lse - lse_ref).max() <= 1e-12
+
+
+def pin_local_reduction(L):
+    """pi <= k (partner already in the window), or t < pi: plain sliding-window
+    attention (eq. Nr), independent of the gate."""
+    rng = np.random.default_rng(12)
+    B, H, N, D = 1, 2, 40, 8
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    kk = 5
+    M = np.zeros((N, N), bool)
+    for t in range(N):
+        M[t, max(0, t - kk):t + 1] = True
+    S = (q.astype(np.float64) @ np.swapaxes(k, -1, -2).astype(np.float64)) / math.sqrt(D)
+    S = np.where(M, S, -np.inf)
+    P = np.exp(S - S.max(-1, keepdims=True))
+    P /= P.sum(-1, keepdims=True)
+    ref = P @ v.astype(np.float64)
+    for pi in (0, 1, 3, kk):
+        for g in (-4.0, 0.0, 2.5):
+            out = oracle.forward(q, k, v, np.full(H, g, np.float32), kk, pi, L=L)
+            assert np.abs(out - ref).max() <= 1e-12, (pi, g)
+    # pi > k, but rows t < pi have no partner
+    pi = 17
+    out = oracle.forward(q, k, v, np.array([1.5, -2.0], np.float32), kk, pi, L=L)
+    assert np.abs(out[:, :, :pi] - ref[:, :, :pi]).max() <= 1e-12
+    assert np.abs(out[:, :, pi:] - ref[:, :, pi:]).max() > 1e-6
+
+
+def pin_basic_union_g0(L):
+    """g = 0 gives alpha~ = 1/2 for both branches: the prior cancels and the
+    result is the basic union softmax (eqs. alpha_u, beta), which is also fixed
+    fusion with alpha = 0.5 (Variant 2)."""
+    rng = np.random.default_rng(13)
+    B, H, N, D = 1, 2, 48, 8
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    kk, pi = 4, 11
+    M = scan_membership(N, kk, pi)
+    S = (q.astype(np.float64) @ np.swapaxes(k, -1, -2).astype(np.float64)) / math.sqrt(D)
+    S = np.where(M, S, -np.inf)
+    P = np.exp(S - S.max(-1, keepdims=True))
+    P /= P.sum(-1, keepdims=True)
+    ref = P @ v.astype(np.float64)
+    out = oracle.forward(q, k, v, np.zeros(H, np.float32), kk, pi, L=L)
+    assert np.abs(out - ref).max() <= 1e-12
+
+
+def pin_multiplicative_form(L):
+    """General adaptive fusion equals eq. (alphahat_adapt) written
+    multiplicatively, per-head and per-query gates, weights included."""
+    rng = np.random.default_rng(14)
+    B, H, N, D = 2, 2, 45, 8
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    for kk, pi in [(3, 9), (6, 7), (2, 20)]:
+        for gate in (rng.uniform(-2, 2, H).astype(np.float32),
+                     rng.uniform(-4, 4, (B, H, N)).astype(np.float32)):
+            ref, W = multiplicative_fusion(q, k, v, gate, kk, pi, 1 / math.sqrt(D))
+            out, P = oracle.forward(q, k, v, gate, kk, pi, want_probs=True, L=L)
+            assert np.abs(out - ref).max() <= 1e-12, (kk, pi, np.abs(out - ref).max())
+            idx = oracle.index_set(N, kk, pi, L)
+            for t in (0, 1, kk, pi, N - 1):
+                for b in range(B):
+                    for h in range(H):
+                        for s in range(idx.shape[1]):
+                            j = idx[t, s]
+                            want = W[b, h, t, j] if j >= 0 else 0.0
+                            assert abs(P[b, h, t, s] - want) <= 1e-12
+
+
+def pin_gate_limits(L):
+    """alpha -> 1 (g -> +inf): partner weight relative to a window key is
+    eps/(1-eps) * exp(z_p - z_j); alpha -> 0: (1-eps)/eps * exp(z_p - z_j)
+    (Sec. 3.5: the clip keeps both priors inside [eps, 1-eps])."""
+    rng = np.random.default_rng(15)
+    B, H, N, D = 1, 2, 30, 8
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    kk, pi = 3, 10
+    gate = np.array([60.0, -60.0], np.float32)
+    _, P = oracle.forward(q, k, v, gate, kk, pi, want_probs=True, L=L)
+    q64, k64 = q.astype(np.float64), k.astype(np.float64)
+    for t in range(pi, N):
+        for h, ratio in ((0, EPS / (1 - EPS)), (1, (1 - EPS) / EPS)):
+            zp = q64[0, h, t] @ k64[0, h, t - pi] / math.sqrt(D)
+            zs = q64[0, h, t] @ k64[0, h, t] / math.sqrt(D)
+            got = P[0, h, t, kk + 1] / P[0, h, t, kk]
+            want = ratio * math.exp(zp - zs)
+            assert abs(got / want - 1) <= 1e-9, (t, h, got, want)
+
+
+def pin_sum_to_one_and_row0(L):
+    """Weights over W_t sum to 1; row t = 0 attends only to itself, so y_0 = v_0
+    exactly; t = 1 has the two-element closed form."""
+    rng = np.random.default_rng(16)
+    B, H, N, D = 2, 2, 50, 8
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    gate = rng.uniform(-1, 1, (B, H, N)).astype(np.float32)
+    out, P = oracle.forward(q, k, v, gate, 6, 13, want_probs=True, L=L)
+    assert np.abs(P.sum(-1) - 1).max() <= 1e-12
+    assert (P >= 0).all()
+    assert np.array_equal(out[:, :, 0], v[:, :, 0].astype(np.float64))
+    q64, k64, v64 = (x.astype(np.float64) for x in (q, k, v))
+    for b in range(B):
+        for h in range(H):
+            z0 = q64[b, h, 1] @ k64[b, h, 0] / math.sqrt(D)
+            z1 = q64[b, h, 1] @ k64[b, h, 1] / math.sqrt(D)
+            y = (math.exp(z0) * v64[b, h, 0] + math.exp(z1) * v64[b, h, 1]) / (math.exp(z0) + math.exp(z1))
+            assert np.abs(out[b, h, 1] - y).max() <= 1e-12
+
+
+def pin_causality(L):
+    """Perturbing or NaN-poisoning positions > t changes no output at t."""
+    rng = np.random.default_rng(17)
+    B, H, N, D = 1, 2, 64, 8
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    gate = rng.uniform(-1, 1, H).astype(np.float32)
+    base = oracle.forward(q, k, v, gate, 5, 12, L=L)
+    for cut in (0, 7, 31, 63):
+        q2, k2, v2 = q.copy(), k.copy(), v.copy()
+        q2[:, :, cut + 1:] = np.nan
+        k2[:, :, cut + 1:] = np.nan
+        v2[:, :, cut + 1:] = np.inf
+        out = oracle.forward(q2, k2, v2, gate, 5, 12, L=L)
+        assert np.array_equal(out[:, :, :cut + 1], base[:, :, :cut + 1]), cut
+
+
+def pin_head_batch_independence(L):
+    """Permuting heads (with their gates) and batches permutes the outputs."""
+    rng = np.random.default_rng(18)
+    B, H, N, D = 2, 4, 24, 8
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    gate = rng.uniform(-1, 1, H).astype(np.float32)
+    out = oracle.forward(q, k, v, gate, 3, 7, L=L)
+    ph, pb = np.array([2, 0, 3, 1]), np.array([1, 0])
+    out2 = oracle.forward(q[pb][:, ph], k[pb][:, ph], v[pb][:, ph], gate[ph], 3, 7, L=L)
+    assert np.array_equal(out2, out[pb][:, ph])
+
+
+def pin_decode_matches_last_row(L):
+    """A decode step at t = len is the forward's row t over the sequence whose
+    row t is the new key/value (Sec. 3.5, online working set); the step writes
+    that row into the cache."""
+    rng = np.random.default_rng(19)
+    S, H, D, cap = 3, 2, 8, 64
+    kk, pi = 5, 13
+    lens = np.array([0, 20, 47], np.int32)
+    Kc = rng.standard_normal((S, H, cap, D)).astype(np.float32)
+    Vc = rng.standard_normal((S, H, cap, D)).astype(np.float32)
+    qn, kn, vn = (rng.standard_normal((S, H, D)).astype(np.float32) for _ in range(3))
+    gate = rng.uniform(-1, 1, (S, H)).astype(np.float32)
+    K2, V2 = Kc.copy(), Vc.copy()
+    out, lse = oracle.decode_step(lens, qn, kn, vn, K2, V2, gate, kk, pi, want_lse=True, L=L)
+    for s in range(S):
+        t = int(lens[s])
+        assert np.array_equal(K2[s, :, t], kn[s]) and np.array_equal(V2[s, :, t], vn[s])
+        keep = np.ones(cap, bool)
+        keep[t] = False
+        assert np.array_equal(K2[s][:, keep], Kc[s][:, keep])
+        seqK, seqV = K2[s:s + 1, :, :t + 1], V2[s:s + 1, :, :t + 1]
+        seqQ = np.zeros_like(seqK)
+        seqQ[0, :, t] = qn[s]
+        g = np.broadcast_to(gate[s][None, :, None], (1, H, t + 1)).astype(np.float32).copy()
+        ref, lref = oracle.forward(seqQ, seqK, seqV, g, kk, pi, want_lse=True, L=L)
+        assert np.array_equal(out[s], ref[0, :, t])
+        assert np.array_equal(lse[s], lref[0, :, t])
+    # and the last row agrees with the multiplicative form on the full sequence
+    s = 2
+    t = int(lens[s])
+    seqQ = np.zeros((1, H, t + 1, D), np.float32)
+    seqQ[0, :, t] = qn[s]
+    ref, _ = multiplicative_fusion(seqQ, K2[s:s + 1, :, :t + 1], V2[s:s + 1, :, :t + 1],
+                                   np.broadcast_to(gate[s][None, :, None], (1, H, t + 1)),
+                                   kk, pi, 1 / math.sqrt(D))
+    assert np.abs(out[s] - ref[0, :, t]).max() <= 1e-12
+
+
+def pin_clamp_reading(L):
+    """Reading of the logit clamp (hyper-parameter table, L_c = 20): clamp the
+    fused logits of valid entries to [-L_c, L_c]; with every |delta| < L_c the
+    clamp changes nothing."""
+    rng = np.random.default_rng(20)
+    B, H, N, D = 1, 2, 30, 8
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    gate = rng.uniform(-1, 1, H).astype(np.float32)
+    a = oracle.forward(q, k, v, gate, 4, 9, L=L)
+    b = oracle.forward(q, k, v, gate, 4, 9, clamp=20.0, L=L)
+    assert np.array_equal(a, b)
+    big = oracle.forward(q, k, v, gate, 4, 9, scale=40.0, clamp=20.0, L=L)
+    _, P = oracle.forward(q, k, v, gate, 4, 9, scale=40.0, clamp=20.0, want_probs=True, L=L)
+    idx = oracle.index_set(N, 4, 9, L)
+    Z = (q.astype(np.float64) @ np.swapaxes(k, -1, -2).astype(np.float64)) * 40.0
+    a_t = EPS + (1 - 2 * EPS) / (1 + np.exp(-gate.astype(np.float64)))
+    for h in range(H):
+        for t in range(N):
+            js = idx[t]
+            dl = np.array([Z[0, h, t, j] + (math.log(a_t[h]) if s <= 4 else math.log(1 - a_t[h]))
+                           for s, j in enumerate(js) if j >= 0])
+            dl = np.clip(dl, -20.0, 20.0)
+            w = np.exp(dl - dl.max())
+            w /= w.sum()
+            got = P[0, h, t][js >= 0]
+            assert np.abs(got - w).max() <= 1e-12
+            assert np.abs(big[0, h, t] - w @ v[0, h, js[js >= 0]].astype(np.float64)).max() <= 1e-12
+
+
+ALL_PINS = [pin_index_set_scan, pin_working_set_sizes, pin_dense_reduction, pin_local_reduction,
+            pin_basic_union_g0, pin_multiplicative_form, pin_gate_limits, pin_sum_to_one_and_row0,
+            pin_causality, pin_head_batch_independence, pin_decode_matches_last_row,
+            pin_clamp_reading]
+
+
+def pin_reachability(L):
+    """Composing the per-layer working-set graphs reproduces eq. (reachable)
+    exactly (up to truncation at position 0), for many (k, pi, L)."""
+    for kk in (1, 2, 3):
+        for pi in (kk + 1, 2 * kk + 3, 7):
+            for depth in (1, 2, 3):
+                n = 40
+                idx = oracle.index_set(n, kk, pi, L)
+                A = np.zeros((n, n), np.int64)
+                for t in range(n):
+                    for j in idx[t]:
+                        if j >= 0:
+                            A[t, j] = 1
+                R = np.eye(n, dtype=np.int64)
+                for _ in range(depth):
+                    R = np.minimum(R @ A, 1)
+                assert np.array_equal(R.astype(bool), reach.reach_closed_form(n, kk, pi, depth)), (kk, pi, depth)
+
+
+ALL_PINS.append(pin_reachability)

@@ -1,0 +1,70 @@
+"""Planted mistakes: each build of the oracle below carries one plausible
+error (dropped term, wrong sign, wrong index, swapped operand, ...), planted
+in a temporary copy of the C source on the CPU.  The pin battery must reject
+every one of them, and must accept the unmodified source."""
+import os
+import shutil
+import subprocess
+
+import pytest
+
+import oracle
+from tests import oracle_pins as P
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "pi_oracle.c")
+
+MUTANTS = {
+    "prior_dropped": [("double dl = z + (s <= k ? log_local : log_skip);", "double dl = z;")],
+    "priors_swapped": [("(s <= k ? log_local : log_skip)", "(s <= k ? log_skip : log_local)")],
+    "skip_prior_sign": [("log_skip = log1p(-at);", "log_skip = -log1p(-at);")],
+    "eps_clip_dropped": [("return ORACLE_EPS + (1.0 - 2.0 * ORACLE_EPS) * a;", "return a;")],
+    "sigmoid_sign": [("double a = 1.0 / (1.0 + exp(-g));", "double a = 1.0 / (1.0 + exp(g));")],
+    "scale_dropped": [("z *= scale;", ";")],
+    "window_short_by_one": [("int lo = t - k > 0 ? t - k : 0;", "int lo = t - k + 1 > 0 ? t - k + 1 : 0;")],
+    "partner_off_by_one": [("slot[k + 1] = t - pi; ++cnt;", "slot[k + 1] = t - pi + 1; ++cnt;")],
+    "partner_not_deduplicated": [
+        ("int oracle_ws_width(int k, int pi) { return k + 1 + (pi > k ? 1 : 0); }",
+         "int oracle_ws_width(int k, int pi) { return k + 1 + (pi > 0 ? 1 : 0); }"),
+        ("if (pi > k && t - pi >= 0)", "if (pi > 0 && t - pi >= 0)")],
+    "keys_values_swapped": [("const float *kj = krows + (int64_t)slot[s] * D;",
+                             "const float *kj = vrows + (int64_t)slot[s] * D;")],
+    "values_from_keys": [("const float *vj = vrows + (int64_t)slot[s] * D;",
+                          "const float *vj = krows + (int64_t)slot[s] * D;")],
+    "softmax_unnormalised": [("if (slot[s] >= 0) Z += exp(delta[s] - mu);",
+                              "if (slot[s] >= 0) Z += exp(delta[s]);")],
+    "max_not_subtracted_in_lse": [("return mu + log(Z);", "return log(Z);")],
+}
+
+
+def _build(tmp_path, name, edits):
+    src = open(SRC).read()
+    for old, new in edits:
+        assert src.count(old) == 1, f"{name}: pattern must occur exactly once: {old!r}"
+        src = src.replace(old, new)
+    c = tmp_path / f"{name}.c"
+    c.write_text(src)
+    so = str(tmp_path / f"lib{name}.so")
+    oracle.build(str(c), so)
+    return oracle.load_library(so)
+
+
+def _failures(L):
+    failed = []
+    for pin in P.ALL_PINS:
+        try:
+            pin(L)
+        except (AssertionError, ValueError, FloatingPointError):
+            failed.append(pin.__name__)
+    return failed
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="needs gcc")
+def test_unmodified_source_passes(tmp_path):
+    assert _failures(_build(tmp_path, "control", [])) == []
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="needs gcc")
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_rejected(tmp_path, name):
+    failed = _failures(_build(tmp_path, name, MUTANTS[name]))
+    assert failed, f"planted mistake {name!r} passed every pin"
