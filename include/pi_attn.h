@@ -1,0 +1,142 @@
+/*
+ * pi_attn.h -- C ABI of the MI355X (gfx950) pi-Attention operator.
+ *
+ * pi-Attention (arXiv 2511.10696) evaluates causal attention of query t on
+ * the online working set W_t = N_r(t) u N_pi(t) (Sec. 3.5, eq. online_ws):
+ *   - the local window N_r(t) = { j : max(0, t-k) <= j <= t }, radius k,
+ *     self included (Sec. 3.2, eq. Nr, causal case);
+ *   - the long-range partner N_pi(t) = { t - pi } (Sec. 3.4, eq. Npi), kept
+ *     only when it lies in [0, t] and outside the window (pi > k; a partner
+ *     inside the window is not counted twice, App. A offset list).
+ * Adaptive fusion (Sec. 3.5 Variant 3, eqs. gate..attn_adapt; App. A eqs.
+ * app_gate..app_out): with gate logit g (pre-sigmoid),
+ *   alpha~ = eps + (1 - 2 eps) * sigmoid(g),  eps = 1e-4,
+ *   delta_tj = scale * <q_t, k_j> + log(alpha~)      for j in the window,
+ *   delta_tj = scale * <q_t, k_j> + log(1 - alpha~)  for the partner,
+ *   y_t = sum_j softmax_j(delta_t) v_j                 (one shared softmax).
+ * scale is 1/sqrt(D) in the paper (Sec. 3.2, eq. z); it is an argument here.
+ *
+ * Conventions for every entry point
+ *   - Device pointers are HIP device (or managed) memory owned by the caller;
+ *     the library allocates nothing and keeps no state between calls.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the default stream)
+ *     and is asynchronous: argument errors are returned before anything is
+ *     enqueued, execution errors surface at the caller's next synchronise.
+ *   - Return value: PI_ATTN_OK (0) or a negative status (pi_attn_strerror).
+ *   - Element types: PI_ATTN_F32 (float32) or PI_ATTN_BF16 (bfloat16); the
+ *     arithmetic is fp32 in both (bf16 operands are multiplied on MFMA with
+ *     fp32 accumulation; softmax weights enter the value product as bf16).
+ *   - Supported head dimensions D: 64 and 128.
+ *   - Rows of q/k/v/out (the D elements of one position) are contiguous and
+ *     start 16-byte aligned: base pointers 16-byte aligned and every stride a
+ *     multiple of 16 bytes.
+ *   - Zero-sized problems (N == 0, B == 0, ...) are valid no-ops.
+ *   - Calls on different streams may run concurrently; calls that write the
+ *     same buffers must be ordered by the caller.
+ */
+#ifndef PI_ATTN_H
+#define PI_ATTN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { PI_ATTN_F32 = 0, PI_ATTN_BF16 = 1 } pi_attn_dtype;
+
+enum {
+    PI_ATTN_OK = 0,
+    PI_ATTN_EINVAL = -1,       /* null pointer, negative size, bad stride or alignment */
+    PI_ATTN_EUNSUPPORTED = -2, /* valid request outside what is built (D, dtype)       */
+    PI_ATTN_EHIP = -3          /* the HIP runtime refused a launch                      */
+};
+
+/* Human-readable text for a status code (static storage, never NULL). */
+const char *pi_attn_strerror(int status);
+
+/* Slots per query in the index-set layout: k+1 window slots, plus one
+ * partner slot iff pi > k.  Returns -1 for k < 0 or pi < 0. */
+int32_t pi_attn_ws_width(int32_t k, int32_t pi);
+
+/*
+ * pi_attn_index_set -- the working sets W_t of a length-n causal sequence
+ * (Sec. 3.2 eq. Nr; Sec. 3.4 eqs. U, Npi; App. A offset list).
+ *   idx   device int32 [n][m], m = pi_attn_ws_width(k, pi), written fully:
+ *         idx[t*m + s] = t - k + s for s in [0, k] (window offsets -k..0),
+ *         idx[t*m + k + 1] = t - pi (only when pi > k),
+ *         and -1 wherever that position is < 0.
+ *   Errors: EINVAL for n < 0, k < 0, pi < 0, idx == NULL with n > 0, or
+ *   n*m beyond 2^31 entries.
+ */
+int pi_attn_index_set(int32_t n, int32_t k, int32_t pi, int32_t *idx, void *stream);
+
+/*
+ * pi_attn_forward -- full-sequence causal pi-Attention with adaptive fusion
+ * (Sec. 3.5 Variant 3; App. A eqs. app_gate..app_out).
+ *   dtype        PI_ATTN_F32 or PI_ATTN_BF16: element type of q, k, v and out.
+ *   B, H, N, D   batch, heads, sequence length, head dimension.
+ *   k, pi        window radius (k >= 0) and partner period (pi >= 0; pi <= k
+ *                means no separate partner, i.e. sliding-window attention;
+ *                k >= N-1 is dense causal attention).
+ *   q, kk, v     device [B][H][N][D] through element strides (sb, sh, sn)
+ *                shared by the three tensors; the D elements are contiguous.
+ *   gate         device float32 pre-sigmoid gate logits g, read at
+ *                gate[b*gsb + h*gsh + t*gsn] (element strides): per-head
+ *                gates [H] use (0, 1, 0), per-query gates [B][H][N] use
+ *                (H*N, N, 1).
+ *   scale        score scale (1/sqrt(D) in the paper).
+ *   logit_clamp  > 0: clamp every fused logit delta to [-clamp, clamp]
+ *                (hyper-parameter L_c of App. B; off when <= 0).
+ *   out          device [B][H][N][D] through (osb, osh, osn), same dtype.
+ *   lse          optional device float32 [B][H][N] contiguous: natural-log
+ *                sum over W_t of exp(delta), or NULL.
+ * Errors: EINVAL (null pointer with non-empty problem, negative size or
+ * stride, misalignment), EUNSUPPORTED (D not 64/128, unknown dtype),
+ * EHIP (launch refused).
+ */
+int pi_attn_forward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D,
+                    int32_t k, int32_t pi,
+                    const void *q, const void *kk, const void *v,
+                    int64_t sb, int64_t sh, int64_t sn,
+                    const float *gate, int64_t gsb, int64_t gsh, int64_t gsn,
+                    float scale, float logit_clamp,
+                    void *out, int64_t osb, int64_t osh, int64_t osn,
+                    float *lse, void *stream);
+
+/*
+ * pi_attn_decode_step -- one KV-cached decode step of the online operator
+ * (Sec. 3.5, eq. online_ws): for each sequence s and head h, with
+ * t = len_in[s], first store the new key/value as cache row t, then attend
+ * the new query over W_t (window rows max(0,t-k)..t, partner row t-pi when
+ * pi > k and t >= pi).
+ *   dtype        PI_ATTN_BF16 or PI_ATTN_F32 (q/k/v/out/caches).
+ *   S, H, D      sequences, heads, head dimension; cap = cache rows.
+ *   len_in       device int32 [S]: current lengths (0 <= len_in[s] < cap).
+ *   len_out      optional device int32 [S] (NULL to skip): receives
+ *                len_in[s] + 1.  Must not alias len_in (other work-groups
+ *                of the same step still read it).
+ *   q_new, k_new, v_new   device [S][H][D] contiguous.
+ *   k_cache, v_cache      device [S][H][cap][D] contiguous; row len_in[s]
+ *                of every head is overwritten, nothing else is written.
+ *   gate         device float32 gate logits gate[s*gss + h*gsh].
+ *   out          device [S][H][D] contiguous; lse optional float32 [S][H].
+ * A length outside [0, cap) cannot be checked on the host (it lives in
+ * device memory): the step then writes NaN to that sequence's outputs (and
+ * lse), leaves its caches untouched and stores len_out[s] = len_in[s].
+ * Errors: as pi_attn_forward, plus EINVAL for cap < 1.
+ */
+int pi_attn_decode_step(int32_t dtype, int32_t S, int32_t H, int32_t D, int32_t cap,
+                        int32_t k, int32_t pi,
+                        const int32_t *len_in, int32_t *len_out,
+                        const void *q_new, const void *k_new, const void *v_new,
+                        void *k_cache, void *v_cache,
+                        const float *gate, int64_t gss, int64_t gsh,
+                        float scale, float logit_clamp,
+                        void *out, float *lse, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PI_ATTN_H */

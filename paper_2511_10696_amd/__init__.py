@@ -1,0 +1,208 @@
+"""MI355X (gfx950) pi-Attention operator: Python binding of libpi_attn.so.
+
+The binding only marshals arguments (device pointers, strides, the current
+HIP stream) into the C ABI declared in ``include/pi_attn.h``; every step of
+the operator runs in the library's HIP kernels.  There is no fallback: if the
+library is missing or the tensors are not on the GPU, the calls raise.
+
+Entry points (same names as the C ABI):
+    pi_attn_index_set(n, k, pi)                      -> int32 [n, m] (device)
+    pi_attn_forward(q, k, v, gate, k_window, pi)     -> out [B,H,N,D] (and lse)
+    pi_attn_decode_step(len_in, q_new, k_new, v_new, k_cache, v_cache, gate, k, pi)
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import threading
+
+__all__ = ["pi_attn_index_set", "pi_attn_forward", "pi_attn_decode_step", "pi_attn_ws_width",
+           "pi_attn_strerror", "library", "LIB_PATH", "EXPORTED_SYMBOLS", "PiAttnError"]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpi_attn.so")
+EXPORTED_SYMBOLS = ("pi_attn_strerror", "pi_attn_ws_width", "pi_attn_index_set",
+                    "pi_attn_forward", "pi_attn_decode_step")
+
+PI_ATTN_F32, PI_ATTN_BF16 = 0, 1
+
+_lock = threading.Lock()
+_lib = None
+
+
+class PiAttnError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: status {status} ({pi_attn_strerror(status)})")
+        self.status = status
+
+
+def library() -> ctypes.CDLL:
+    """Load libpi_attn.so (built by ``paper_2511_10696_amd.build``)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2511_10696_amd.build`")
+            lib = ctypes.CDLL(LIB_PATH)
+            i32, i64, f32, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
+            lib.pi_attn_strerror.argtypes = [ctypes.c_int]
+            lib.pi_attn_strerror.restype = ctypes.c_char_p
+            lib.pi_attn_ws_width.argtypes = [i32, i32]
+            lib.pi_attn_ws_width.restype = i32
+            lib.pi_attn_index_set.argtypes = [i32, i32, i32, vp, vp]
+            lib.pi_attn_index_set.restype = ctypes.c_int
+            lib.pi_attn_forward.argtypes = ([i32] * 7 + [vp, vp, vp, i64, i64, i64, vp, i64, i64, i64,
+                                                        f32, f32, vp, i64, i64, i64, vp, vp])
+            lib.pi_attn_forward.restype = ctypes.c_int
+            lib.pi_attn_decode_step.argtypes = ([i32] * 7 + [vp, vp, vp, vp, vp, vp, vp, vp, i64, i64,
+                                                            f32, f32, vp, vp, vp])
+            lib.pi_attn_decode_step.restype = ctypes.c_int
+            _lib = lib
+    return _lib
+
+
+def pi_attn_strerror(status: int) -> str:
+    return library().pi_attn_strerror(int(status)).decode()
+
+
+def pi_attn_ws_width(k: int, pi: int) -> int:
+    return int(library().pi_attn_ws_width(int(k), int(pi)))
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_handle(stream, device):
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(dt):
+    torch = _torch()
+    if dt == torch.float32:
+        return PI_ATTN_F32
+    if dt == torch.bfloat16:
+        return PI_ATTN_BF16
+    raise TypeError(f"unsupported dtype {dt} (float32 or bfloat16)")
+
+
+def _require_cuda(*ts):
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise RuntimeError("pi_attn tensors must be on the GPU (no CPU path exists)")
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise PiAttnError(status, where)
+
+
+def pi_attn_index_set(n: int, k: int, pi: int, out=None, device=None, stream=None):
+    """W_t for t in [0, n) as a device int32 tensor [n, m] (m = pi_attn_ws_width(k, pi)):
+    columns 0..k hold t-k..t, column k+1 (present iff pi > k) holds t-pi, -1 where < 0."""
+    torch = _torch()
+    m = pi_attn_ws_width(k, pi)
+    if m < 0:
+        raise PiAttnError(-1, "pi_attn_index_set")
+    if out is None:
+        out = torch.empty((n, m), dtype=torch.int32, device=device or "cuda")
+    _require_cuda(out)
+    if out.dtype != torch.int32 or tuple(out.shape) != (n, m) or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous int32 tensor of shape {(n, m)}")
+    _check(library().pi_attn_index_set(n, k, pi, _ptr(out), _stream_handle(stream, out.device)),
+           "pi_attn_index_set")
+    return out
+
+
+def pi_attn_forward(q, k, v, gate, k_window: int, pi: int, scale: float | None = None,
+                    logit_clamp: float = 0.0, out=None, return_lse: bool = False, lse=None, stream=None):
+    """Causal pi-Attention forward.
+
+    q, k, v: [B, H, N, D] float32 or bfloat16 on the GPU, identical strides,
+    last dimension contiguous.  gate: float32 pre-sigmoid gate logits, [H]
+    (per head) or [B, H, N] (per query), any strides.  Returns out
+    [B, H, N, D] in the input dtype (and lse [B, H, N] float32 on request).
+    """
+    torch = _torch()
+    _require_cuda(q, k, v, gate, out, lse)
+    if q.dim() != 4 or k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k, v must share one [B, H, N, D] shape")
+    if k.dtype != q.dtype or v.dtype != q.dtype:
+        raise TypeError("q, k, v must share one dtype")
+    if k.stride() != q.stride() or v.stride() != q.stride():
+        raise ValueError("q, k, v must share strides (use .contiguous())")
+    if q.stride(3) != 1:
+        raise ValueError("the head dimension must be contiguous")
+    B, H, N, D = q.shape
+    if gate.dtype != torch.float32:
+        raise TypeError("gate logits must be float32")
+    if tuple(gate.shape) == (H,):
+        g = gate.view(1, H, 1).expand(B, H, N)
+    elif tuple(gate.shape) == (B, H, N):
+        g = gate
+    else:
+        raise ValueError(f"gate must be [H] or [B, H, N], got {tuple(gate.shape)}")
+    if out is None:
+        out = torch.empty_like(q, memory_format=torch.contiguous_format)
+    if out.shape != q.shape or out.dtype != q.dtype or out.stride(3) != 1:
+        raise ValueError("out must match q's shape and dtype with a contiguous last dimension")
+    if return_lse and lse is None:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, N)
+                            or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous float32 [B, H, N] tensor")
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    st = library().pi_attn_forward(
+        _dtype_code(q.dtype), B, H, N, D, int(k_window), int(pi),
+        _ptr(q), _ptr(k), _ptr(v), q.stride(0), q.stride(1), q.stride(2),
+        _ptr(g), g.stride(0), g.stride(1), g.stride(2), float(scale), float(logit_clamp),
+        _ptr(out), out.stride(0), out.stride(1), out.stride(2), _ptr(lse),
+        _stream_handle(stream, q.device))
+    _check(st, "pi_attn_forward")
+    return (out, lse) if (return_lse or lse is not None) else out
+
+
+def pi_attn_decode_step(len_in, q_new, k_new, v_new, k_cache, v_cache, gate, k: int, pi: int,
+                        scale: float | None = None, logit_clamp: float = 0.0, len_out=None,
+                        out=None, lse=None, stream=None):
+    """One decode step: appends k_new/v_new [S, H, D] as row len_in[s] of the
+    caches [S, H, cap, D] and attends q_new over W_t.  Returns out [S, H, D]."""
+    torch = _torch()
+    _require_cuda(len_in, q_new, k_new, v_new, k_cache, v_cache, gate, len_out, out, lse)
+    S, H, cap, D = k_cache.shape
+    for name, t in (("q_new", q_new), ("k_new", k_new), ("v_new", v_new)):
+        if tuple(t.shape) != (S, H, D) or not t.is_contiguous() or t.dtype != k_cache.dtype:
+            raise ValueError(f"{name} must be a contiguous [S, H, D] tensor of the cache dtype")
+    if v_cache.shape != k_cache.shape or v_cache.dtype != k_cache.dtype:
+        raise ValueError("k_cache and v_cache must match")
+    if not (k_cache.is_contiguous() and v_cache.is_contiguous()):
+        raise ValueError("caches must be contiguous")
+    if len_in.dtype != torch.int32 or tuple(len_in.shape) != (S,) or not len_in.is_contiguous():
+        raise ValueError("len_in must be a contiguous int32 [S] tensor")
+    if gate.dtype != torch.float32:
+        raise TypeError("gate logits must be float32")
+    if tuple(gate.shape) == (H,):
+        gss, gsh = 0, gate.stride(0)
+    elif tuple(gate.shape) == (S, H):
+        gss, gsh = gate.stride(0), gate.stride(1)
+    else:
+        raise ValueError("decode gate must be [H] or [S, H]")
+    if out is None:
+        out = torch.empty_like(q_new)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    st = library().pi_attn_decode_step(
+        _dtype_code(k_cache.dtype), S, H, D, cap, int(k), int(pi), _ptr(len_in), _ptr(len_out),
+        _ptr(q_new), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(gate), gss, gsh,
+        float(scale), float(logit_clamp), _ptr(out), _ptr(lse), _stream_handle(stream, q_new.device))
+    _check(st, "pi_attn_decode_step")
+    return out

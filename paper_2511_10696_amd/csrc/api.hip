@@ -1,0 +1,118 @@
+// api.hip -- the C ABI (include/pi_attn.h): argument validation and dispatch.
+// Nothing here allocates; every launch goes on the caller's stream.
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/pi_attn.h"
+#include "kernels.h"
+#include "pi_common.h"
+
+using namespace pi_attn;
+
+namespace {
+
+constexpr int64_t kMaxRows = (int64_t)1 << 31;   // B*H*N (and S*H) limit
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+int elem_size(int32_t dtype) { return dtype == PI_ATTN_F32 ? 4 : dtype == PI_ATTN_BF16 ? 2 : 0; }
+
+bool stride16(int64_t stride_elems, int es) { return stride_elems >= 0 && ((stride_elems * es) & 15) == 0; }
+
+int from_hip(hipError_t e) { return e == hipSuccess ? PI_ATTN_OK : PI_ATTN_EHIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char *pi_attn_strerror(int status) {
+    switch (status) {
+        case PI_ATTN_OK: return "ok";
+        case PI_ATTN_EINVAL: return "invalid argument (null pointer, negative size or stride, misalignment)";
+        case PI_ATTN_EUNSUPPORTED: return "unsupported configuration (head dimension must be 64 or 128; dtype f32/bf16)";
+        case PI_ATTN_EHIP: return "HIP runtime refused the launch";
+        default: return "unknown status";
+    }
+}
+
+int32_t pi_attn_ws_width(int32_t k, int32_t pi) {
+    if (k < 0 || pi < 0) return -1;
+    return ws_width(k, pi);
+}
+
+int pi_attn_index_set(int32_t n, int32_t k, int32_t pi, int32_t *idx, void *stream) {
+    if (n < 0 || k < 0 || pi < 0) return PI_ATTN_EINVAL;
+    if ((int64_t)n * ws_width(k, pi) >= kMaxRows) return PI_ATTN_EINVAL;
+    if (n == 0) return PI_ATTN_OK;
+    if (!idx || !aligned4(idx)) return PI_ATTN_EINVAL;
+    return from_hip(launch_index_set(n, k, pi, idx, (hipStream_t)stream));
+}
+
+int pi_attn_forward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, int32_t k, int32_t pi,
+                    const void *q, const void *kk, const void *v, int64_t sb, int64_t sh, int64_t sn,
+                    const float *gate, int64_t gsb, int64_t gsh, int64_t gsn, float scale, float logit_clamp,
+                    void *out, int64_t osb, int64_t osh, int64_t osn, float *lse, void *stream) {
+    const int es = elem_size(dtype);
+    if (es == 0) return PI_ATTN_EUNSUPPORTED;
+    if (B < 0 || H < 0 || N < 0 || k < 0 || pi < 0) return PI_ATTN_EINVAL;
+    if (D != 64 && D != 128) return PI_ATTN_EUNSUPPORTED;
+    if (!isfinite(scale) || scale <= 0.0f || isnan(logit_clamp)) return PI_ATTN_EINVAL;
+    const int64_t rows = (int64_t)B * H * N;
+    if (rows >= kMaxRows) return PI_ATTN_EINVAL;
+    if (rows == 0) return PI_ATTN_OK;
+    if (!q || !kk || !v || !gate || !out) return PI_ATTN_EINVAL;
+    if (!aligned16(q) || !aligned16(kk) || !aligned16(v) || !aligned16(out)) return PI_ATTN_EINVAL;
+    if (!stride16(sb, es) || !stride16(sh, es) || !stride16(sn, es)) return PI_ATTN_EINVAL;
+    if (!stride16(osb, es) || !stride16(osh, es) || !stride16(osn, es)) return PI_ATTN_EINVAL;
+    if (!aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
+    if (lse && !aligned4(lse)) return PI_ATTN_EINVAL;
+
+    FwdParams p{};
+    p.B = B; p.H = H; p.N = N; p.D = D; p.k = k; p.pi = pi;
+    p.q = q; p.k_ptr = kk; p.v = v;
+    p.sb = sb; p.sh = sh; p.sn = sn;
+    p.gate = gate; p.gsb = gsb; p.gsh = gsh; p.gsn = gsn;
+    p.scale = scale;
+    p.clamp = logit_clamp > 0.0f ? logit_clamp : 0.0f;
+    p.out = out; p.osb = osb; p.osh = osh; p.osn = osn;
+    p.lse = lse;
+    const hipStream_t st = (hipStream_t)stream;
+    return from_hip(dtype == PI_ATTN_BF16 ? launch_forward_bf16(p, st) : launch_forward_f32(p, st));
+}
+
+int pi_attn_decode_step(int32_t dtype, int32_t S, int32_t H, int32_t D, int32_t cap, int32_t k, int32_t pi,
+                        const int32_t *len_in, int32_t *len_out, const void *q_new, const void *k_new,
+                        const void *v_new, void *k_cache, void *v_cache, const float *gate, int64_t gss,
+                        int64_t gsh, float scale, float logit_clamp, void *out, float *lse, void *stream) {
+    const int es = elem_size(dtype);
+    if (es == 0) return PI_ATTN_EUNSUPPORTED;
+    if (S < 0 || H < 0 || cap < 1 || k < 0 || pi < 0) return PI_ATTN_EINVAL;
+    if (D != 64 && D != 128) return PI_ATTN_EUNSUPPORTED;
+    if (!isfinite(scale) || scale <= 0.0f || isnan(logit_clamp)) return PI_ATTN_EINVAL;
+    const int64_t n = (int64_t)S * H;
+    if (n >= kMaxRows) return PI_ATTN_EINVAL;
+    if (n == 0) return PI_ATTN_OK;
+    if (!len_in || !q_new || !k_new || !v_new || !k_cache || !v_cache || !gate || !out) return PI_ATTN_EINVAL;
+    if ((const void *)len_out == (const void *)len_in) return PI_ATTN_EINVAL;
+    if (!aligned4(len_in) || (len_out && !aligned4(len_out))) return PI_ATTN_EINVAL;
+    if (!aligned16(q_new) || !aligned16(k_new) || !aligned16(v_new) || !aligned16(k_cache) ||
+        !aligned16(v_cache) || !aligned16(out))
+        return PI_ATTN_EINVAL;
+    if (!aligned4(gate) || gss < 0 || gsh < 0) return PI_ATTN_EINVAL;
+    if (lse && !aligned4(lse)) return PI_ATTN_EINVAL;
+
+    DecodeParams p{};
+    p.S = S; p.H = H; p.D = D; p.cap = cap; p.k = k; p.pi = pi;
+    p.len_in = len_in; p.len_out = len_out;
+    p.q_new = q_new; p.k_new = k_new; p.v_new = v_new;
+    p.k_cache = k_cache; p.v_cache = v_cache;
+    p.gate = gate; p.gss = gss; p.gsh = gsh;
+    p.scale = scale;
+    p.clamp = logit_clamp > 0.0f ? logit_clamp : 0.0f;
+    p.out = out; p.lse = lse;
+    const hipStream_t st = (hipStream_t)stream;
+    return from_hip(dtype == PI_ATTN_BF16 ? launch_decode_bf16(p, st) : launch_decode_f32(p, st));
+}
+
+}  // extern "C"

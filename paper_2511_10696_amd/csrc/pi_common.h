@@ -1,0 +1,88 @@
+// pi_common.h -- working-set enumeration and fusion prior shared by every
+// kernel of the library and by pi_attn_index_set, so that the exported index
+// set is the one the attention kernels use.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pi_attn {
+
+// Gate clip of Variant 3 (Sec. 3.5): alpha~ = eps + (1 - 2 eps) sigmoid(g).
+constexpr float kGateEps = 1e-4f;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// Window N_r(t) (Sec. 3.2, eq. Nr, causal): j in [window_lo(t,k), t].
+__host__ __device__ inline int window_lo(int t, int k) { return t - k > 0 ? t - k : 0; }
+
+__host__ __device__ inline bool in_window(int j, int t, int k) { return j <= t && j >= t - k && j >= 0; }
+
+// A partner slot exists only when t - pi can lie outside the window.
+__host__ __device__ inline bool partner_enabled(int k, int pi) { return pi > k; }
+
+// Partner N_pi(t) = {t - pi} (Sec. 3.4, eq. Npi); -1 when absent.
+__host__ __device__ inline int partner_of(int t, int k, int pi) {
+    return (partner_enabled(k, pi) && t >= pi) ? t - pi : -1;
+}
+
+// Slots per query: k+1 window slots (offsets -k..0) then the partner slot.
+__host__ __device__ inline int ws_width(int k, int pi) { return k + 1 + (partner_enabled(k, pi) ? 1 : 0); }
+
+// Slot s of W_t in the exported layout; -1 for an absent entry.
+__host__ __device__ inline int ws_slot(int t, int s, int k, int pi) {
+    if (s <= k) {
+        int j = t - k + s;
+        return j >= 0 ? j : -1;
+    }
+    return partner_of(t, k, pi);
+}
+
+// Per-query fusion biases, natural-log units.
+//   exact:    local = log alpha~, partner = log(1 - alpha~)
+//   shifted:  local = 0,          partner = log(1 - alpha~) - log alpha~
+// The shifted form differs from the exact one by the common log alpha~ on
+// every entry of W_t, which the softmax removes; lse adds it back.
+struct FusionBias {
+    float local;
+    float partner;
+    float lse_shift;
+};
+
+__device__ inline FusionBias fusion_bias(float g, bool exact) {
+    float a = 1.0f / (1.0f + __expf(-g));
+    float at = kGateEps + (1.0f - 2.0f * kGateEps) * a;
+    float ll = __logf(at);
+    float lp = __logf(1.0f - at);
+    FusionBias fb;
+    if (exact) {
+        fb.local = ll;
+        fb.partner = lp;
+        fb.lse_shift = 0.0f;
+    } else {
+        fb.local = 0.0f;
+        fb.partner = lp - ll;
+        fb.lse_shift = ll;
+    }
+    return fb;
+}
+
+// XCD-aware work-group order.  Consecutive work-group ids are dispatched
+// round-robin over the 8 XCDs; this remaps them so that each XCD receives a
+// contiguous range of logical tiles (neighbouring query tiles share most of
+// their keys, which then stay in that XCD's L2).  The grid is padded to a
+// multiple of 8; ids mapping past n_logical return -1.
+constexpr int kNumXcd = 8;
+
+__device__ inline int64_t xcd_remap(int64_t bid, int64_t n_logical) {
+    int64_t per = (n_logical + kNumXcd - 1) / kNumXcd;
+    int64_t logical = (bid % kNumXcd) * per + bid / kNumXcd;
+    return logical < n_logical ? logical : -1;
+}
+
+inline int64_t xcd_grid(int64_t n_logical) {
+    int64_t per = (n_logical + kNumXcd - 1) / kNumXcd;
+    return per * kNumXcd;
+}
+
+}  // namespace pi_attn

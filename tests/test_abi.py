@@ -1,0 +1,135 @@
+"""The C ABI on the host: the library loads, exports every entry point that
+include/pi_attn.h declares, and rejects invalid arguments before touching the
+GPU (none of these calls enqueues work, so they run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2511_10696_amd as pa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pi_attn.h")
+
+EINVAL, EUNSUP = -1, -2
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(pa.LIB_PATH):
+        from paper_2511_10696_amd import build
+        build.build()
+    return pa.library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pi_attn_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    assert declared_functions() == sorted(pa.EXPORTED_SYMBOLS)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+        assert ctypes.cast(getattr(lib, name), ctypes.c_void_p).value
+
+
+def test_strerror(lib):
+    for st in (0, -1, -2, -3, -99):
+        assert isinstance(pa.pi_attn_strerror(st), str) and pa.pi_attn_strerror(st)
+
+
+@pytest.mark.parametrize("k,pi,m", [(0, 0, 1), (4, 16, 6), (4, 4, 5), (4, 3, 5), (512, 1024, 514),
+                                    (128, 256, 130), (3, 0, 4), (-1, 2, -1), (2, -1, -1)])
+def test_ws_width(lib, k, pi, m):
+    assert pa.pi_attn_ws_width(k, pi) == m
+
+
+def fwd(lib, **kw):
+    a = dict(dtype=1, B=1, H=2, N=256, D=64, k=32, pi=64, q=16, kk=16, v=16, sb=32768, sh=16384, sn=64,
+             gate=16, gsb=0, gsh=1, gsn=0, scale=0.125, clamp=0.0, out=16, osb=32768, osh=16384, osn=64,
+             lse=None, stream=None)
+    a.update(kw)
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.pi_attn_forward(a["dtype"], a["B"], a["H"], a["N"], a["D"], a["k"], a["pi"], vp(a["q"]),
+                               vp(a["kk"]), vp(a["v"]), a["sb"], a["sh"], a["sn"], vp(a["gate"]), a["gsb"],
+                               a["gsh"], a["gsn"], a["scale"], a["clamp"], vp(a["out"]), a["osb"], a["osh"],
+                               a["osn"], vp(a["lse"]), vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=7), EUNSUP), (dict(D=96), EUNSUP), (dict(D=256), EUNSUP),
+    (dict(B=-1), EINVAL), (dict(N=-5), EINVAL), (dict(k=-1), EINVAL), (dict(pi=-2), EINVAL),
+    (dict(q=None), EINVAL), (dict(kk=None), EINVAL), (dict(v=None), EINVAL), (dict(gate=None), EINVAL),
+    (dict(out=None), EINVAL), (dict(q=24), EINVAL), (dict(out=8), EINVAL), (dict(sn=68), EINVAL),
+    (dict(sn=-64), EINVAL), (dict(osn=4), EINVAL), (dict(gate=18), EINVAL), (dict(gsn=-1), EINVAL),
+    (dict(scale=0.0), EINVAL), (dict(scale=-1.0), EINVAL), (dict(scale=float("inf")), EINVAL),
+    (dict(scale=float("nan")), EINVAL), (dict(clamp=float("nan")), EINVAL), (dict(lse=2), EINVAL),
+    (dict(dtype=0, sn=66), EINVAL),
+])
+def test_forward_rejects(lib, kw, code):
+    assert fwd(lib, **kw) == code
+
+
+@pytest.mark.parametrize("kw", [dict(N=0), dict(B=0), dict(H=0), dict(N=0, q=None, out=None)])
+def test_forward_empty_is_noop(lib, kw):
+    assert fwd(lib, **kw) == 0
+
+
+def dec(lib, **kw):
+    a = dict(dtype=1, S=2, H=2, D=128, cap=64, k=4, pi=8, len_in=64, len_out=128, q=16, kn=16, vn=16,
+             kc=16, vc=16, gate=16, gss=0, gsh=1, scale=0.1, clamp=0.0, out=16, lse=None, stream=None)
+    a.update(kw)
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.pi_attn_decode_step(a["dtype"], a["S"], a["H"], a["D"], a["cap"], a["k"], a["pi"],
+                                   vp(a["len_in"]), vp(a["len_out"]), vp(a["q"]), vp(a["kn"]), vp(a["vn"]),
+                                   vp(a["kc"]), vp(a["vc"]), vp(a["gate"]), a["gss"], a["gsh"], a["scale"],
+                                   a["clamp"], vp(a["out"]), vp(a["lse"]), vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=3), EUNSUP), (dict(D=32), EUNSUP), (dict(S=-1), EINVAL), (dict(cap=0), EINVAL),
+    (dict(k=-1), EINVAL), (dict(len_in=None), EINVAL), (dict(len_out=64), EINVAL), (dict(len_in=66), EINVAL),
+    (dict(q=None), EINVAL), (dict(kc=None), EINVAL), (dict(vc=8), EINVAL), (dict(out=4), EINVAL),
+    (dict(gate=None), EINVAL), (dict(gsh=-1), EINVAL), (dict(scale=0.0), EINVAL), (dict(lse=1), EINVAL),
+])
+def test_decode_rejects(lib, kw, code):
+    assert dec(lib, **kw) == code
+
+
+@pytest.mark.parametrize("kw", [dict(S=0), dict(H=0)])
+def test_decode_empty_is_noop(lib, kw):
+    assert dec(lib, **kw) == 0
+
+
+def test_index_set_rejects(lib):
+    assert lib.pi_attn_index_set(-1, 2, 3, ctypes.c_void_p(16), None) == EINVAL
+    assert lib.pi_attn_index_set(5, -2, 3, ctypes.c_void_p(16), None) == EINVAL
+    assert lib.pi_attn_index_set(5, 2, -3, ctypes.c_void_p(16), None) == EINVAL
+    assert lib.pi_attn_index_set(5, 2, 3, None, None) == EINVAL
+    assert lib.pi_attn_index_set(5, 2, 3, ctypes.c_void_p(2), None) == EINVAL
+    assert lib.pi_attn_index_set(1 << 30, 8, 16, ctypes.c_void_p(16), None) == EINVAL
+    assert lib.pi_attn_index_set(0, 2, 3, None, None) == 0
+
+
+def test_binding_refuses_cpu_tensors(lib):
+    import torch
+    q = torch.zeros(1, 1, 4, 64)
+    with pytest.raises(RuntimeError, match="GPU"):
+        pa.pi_attn_forward(q, q, q, torch.zeros(1), 2, 3)
+
+
+def test_product_does_not_import_oracle():
+    """The product package must not reach the oracle (test infrastructure)."""
+    pkg = os.path.join(ROOT, "paper_2511_10696_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"^\s*(import|from)\s+oracle\b", text, flags=re.M), f
+                assert "pi_oracle" not in text and "liboracle" not in text, f

@@ -1,0 +1,30 @@
+"""Host-side pieces of the benchmark: algorithmic work counts and the
+refusal to run on more than one GPU."""
+import subprocess
+import sys
+
+import bench
+from paper_2511_10696_amd import workloads as W
+
+
+def test_attended_keys_match_closed_form():
+    # sum over t of |W_t| per (b, h): window min(t,k)+1 plus the partner for t >= pi
+    per_bh = {"tiny": 8112, "fwd4k": 523968, "fwd16k": 4193664, "fwd32k": 16710400}
+    for name, cfg in W.FORWARD.items():
+        keys, flops, nbytes = bench.forward_algorithmic(cfg)
+        assert keys == per_bh[name] * cfg.B * cfg.H
+        assert flops == 4 * cfg.D * keys
+        assert nbytes == 4 * cfg.B * cfg.H * cfg.N * cfg.D * 2
+
+
+def test_decode_bytes_per_step():
+    cfg = W.DECODE["decode"]
+    keys, nbytes = bench.decode_algorithmic(cfg, cfg.cache_len)
+    assert keys == 514 * cfg.S * cfg.H
+    assert nbytes == (2 * 513 + 6) * cfg.D * 2 * cfg.S * cfg.H
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, "bench.py", "--gpus", "2"], capture_output=True, text=True,
+                       cwd=bench.ROOT)
+    assert r.returncode == 2 and "one GPU" in r.stderr
