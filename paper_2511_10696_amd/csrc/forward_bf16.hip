@@ -59,10 +59,12 @@ struct Stage {
 
 __device__ inline uint4 ld16(const __bf16 *p) { return *reinterpret_cast<const uint4 *>(p); }
 
-// Issue the global loads of key/value rows [row0, row0+64) (rows outside
-// [0, N) read as zero).
+// Issue the global loads of key/value rows [row0, row0+64); rows outside
+// [0, lim) are not read and stage as zero.  For window tiles lim is the end
+// of the query tile, so no row later than every query of the tile is ever
+// touched (a masked weight is 0, but 0 times a non-finite value is not).
 template <int D>
-__device__ inline void stage_load(Stage<D> &st, const __bf16 *kb, const __bf16 *vb, int64_t sn, int row0, int N,
+__device__ inline void stage_load(Stage<D> &st, const __bf16 *kb, const __bf16 *vb, int64_t sn, int row0, int lim,
                                   int tid) {
     constexpr int CPR = D / 8;   // chunks per row
 #pragma unroll
@@ -71,13 +73,13 @@ __device__ inline void stage_load(Stage<D> &st, const __bf16 *kb, const __bf16 *
         int cid = tid + NT * c;
         int r = cid / CPR, col = cid % CPR;
         int gr = row0 + r;
-        st.kc[c] = (gr >= 0 && gr < N) ? ld16(kb + gr * sn + col * 8) : make_uint4(0, 0, 0, 0);
+        st.kc[c] = (gr >= 0 && gr < lim) ? ld16(kb + gr * sn + col * 8) : make_uint4(0, 0, 0, 0);
         // V: thread owns CH consecutive rows of one 8-dim chunk (for the
         // transposed store); each load instruction still reads whole rows.
         int vcol = tid % CPR, vrg = tid / CPR;
         int vr = vrg * Stage<D>::CH + c;
         int gv = row0 + vr;
-        st.vc[c] = (gv >= 0 && gv < N) ? ld16(vb + gv * sn + vcol * 8) : make_uint4(0, 0, 0, 0);
+        st.vc[c] = (gv >= 0 && gv < lim) ? ld16(vb + gv * sn + vcol * 8) : make_uint4(0, 0, 0, 0);
     }
 }
 
@@ -245,7 +247,7 @@ __global__ __launch_bounds__(NT, 2) void forward_bf16_kernel(FwdParams p, int n_
     const int kstart = window_lo(t0, kw);
     const int kend = min(t0 + BM, N);
     const int ntiles = kend > kstart ? (kend - kstart + BN - 1) / BN : 0;
-    if (ntiles > 0) stage_load<D>(st, kp, vp, sn, kstart, N, tid);
+    if (ntiles > 0) stage_load<D>(st, kp, vp, sn, kstart, kend, tid);
     if (has_partner) {
         __syncthreads();
         // wavefront w's partner rows are rows 32w.. of the 128-row tile:
@@ -281,7 +283,7 @@ __global__ __launch_bounds__(NT, 2) void forward_bf16_kernel(FwdParams p, int n_
     for (int it = 0; it < ntiles; ++it) {
         const int buf = it & 1;
         const int j0 = kstart + BN * it;
-        if (it + 1 < ntiles) stage_load<D>(st, kp, vp, sn, j0 + BN, N, tid);
+        if (it + 1 < ntiles) stage_load<D>(st, kp, vp, sn, j0 + BN, kend, tid);
 
         // blocks of this tile that intersect the wavefront's band
         // [qw0 - k, qw0 + 31]
