@@ -26,7 +26,9 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
-PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "forward_bf16_fwd32k_traffic.json")
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "forward_bf16_fwd32k_hbm_traffic.txt")
+DECODE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_bf16_s64_hbm_traffic.txt")
+COPY_PROBE_BYTES = 1 << 30      # plain device copy used to calibrate the HBM byte counters
 
 
 def parse():
@@ -37,6 +39,9 @@ def parse():
     ap.add_argument("--decode-steps", type=int, default=1000)
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pmc-probe", action="store_true",
+                    help="run 3 forward launches, 3 decode steps and 3 plain 1 GiB device copies, "
+                         "then exit (for hardware-counter runs)")
     return ap.parse_args()
 
 
@@ -74,15 +79,49 @@ def source_digest(paths):
     return h.hexdigest()[:16]
 
 
-def measured_traffic(digest):
-    """HBM bytes per launch from the committed rocprofv3 counter summary,
-    valid only for the kernel source it was taken on."""
-    if not os.path.exists(PROFILE_TRAFFIC):
+def measured_traffic(digest, path=PROFILE_TRAFFIC):
+    """HBM bytes per launch (calibrated FETCH_SIZE + WRITE_SIZE) from the
+    committed rocprofv3 counter summary; valid only for the kernel source it
+    was taken on, so None once the source digest differs."""
+    if not os.path.exists(path):
         return None
-    rec = json.load(open(PROFILE_TRAFFIC))
-    if rec.get("source_digest") != digest:
+    rec = {}
+    for line in open(path):
+        if "=" in line and not line.lstrip().startswith("#"):
+            key, val = line.split("=", 1)
+            rec[key.strip()] = val.strip()
+    if rec.get("source_digest") != digest or "hbm_bytes_per_launch" not in rec:
         return None
-    return rec.get("bytes_per_launch")
+    return int(float(rec["hbm_bytes_per_launch"]))
+
+
+def pmc_probe(W, pa, torch, dev):
+    """Launch each kernel a few times (and a plain copy of known size) so a
+    counter run can read per-dispatch HBM bytes and calibrate them."""
+    cfg = W.FORWARD["fwd32k"]
+    q, k, v, gate = W.forward_inputs(cfg, 0, dev)
+    out = torch.empty_like(q)
+    for _ in range(3):
+        pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi, out=out)
+    torch.cuda.synchronize()
+    print(f"probe: 3 x forward fwd32k", flush=True)
+    del q, k, v, out
+    dcfg = W.DECODE["decode"]
+    kc, vc, lens, dgate = W.decode_state(dcfg, 0, dev)
+    qs, ks, vs = W.decode_tokens(dcfg, 3, 1, dev)
+    lbuf = [lens, torch.empty_like(lens)]
+    for i in range(3):
+        pa.pi_attn_decode_step(lbuf[i % 2], qs[i], ks[i], vs[i], kc, vc, dgate, dcfg.k, dcfg.pi,
+                               len_out=lbuf[(i + 1) % 2])
+    torch.cuda.synchronize()
+    print(f"probe: 3 x decode step", flush=True)
+    del kc, vc, qs, ks, vs
+    src = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(f"probe: 3 x device copy of {COPY_PROBE_BYTES} bytes", flush=True)
 
 
 def main():
@@ -99,6 +138,9 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.pmc_probe:
+        pmc_probe(W, pa, torch, dev)
+        return
     cfg = W.FORWARD["fwd32k"]
     q, k, v, gate = W.forward_inputs(cfg, 0, dev)
     out = torch.empty_like(q)
@@ -167,13 +209,17 @@ def main():
         torch.cuda.synchronize()
         dms = d0.elapsed_time(d1) / nsteps
         dkeys, dbytes = decode_algorithmic(dcfg, dcfg.cache_len)
+        ddigest = source_digest([os.path.join(ROOT, "paper_2511_10696_amd", "csrc", f)
+                                 for f in ("decode_bf16.hip", "pi_common.h", "kernels.h")])
+        dtraffic = measured_traffic(ddigest, DECODE_TRAFFIC)
         dgbs = dbytes / (dms / 1e3) / 1e9
         decode = {"workload": "decode S64 H32 D128 k512 pi1024 cache32768 bf16", "steps": nsteps,
                   "ms_per_step": round(dms, 5), "us_per_step": round(dms * 1e3, 2),
                   "queries_per_s": round(dcfg.S / (dms / 1e3), 1),
                   "roofline": {"bound": "hbm", "kernel": "decode_bf16_kernel<128>",
                                "achieved": round(dgbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                               "frac": round(dgbs / HBM_PEAK_GBS, 4), "bytes_per_step": dbytes}}
+                               "frac": round(dgbs / HBM_PEAK_GBS, 4), "bytes_per_step": dbytes,
+                               "traffic": dtraffic}}
         del kc, vc, qs, ks, vs
         torch.cuda.empty_cache()
 
