@@ -21,8 +21,11 @@ LIB_PATH = os.path.join(PKG, "libpi_attn.so")
 ARCH = "gfx950"
 
 # Packed-FP32 VALU instructions are disabled for every kernel (hipcc would
-# otherwise form them from float2-style code).
-DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# otherwise form them from float2-style code).  MFMA accumulators are kept in
+# ordinary VGPRs (the softmax rescales them with VALU instructions; the AGPR
+# form would copy them back and forth).
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-amdgpu-mfma-vgpr-form"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
           "-I", os.path.join(ROOT, "include")] + DEVICE_FLAGS
 

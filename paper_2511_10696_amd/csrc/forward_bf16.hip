@@ -2,28 +2,42 @@
 // fp32 accumulate, for head dimension D = 64 or 128.
 //
 // Work decomposition.  One work-group (4 wavefronts) owns a query tile of
-// BM = 128 consecutive positions [t0, t0+128) of one (b, h).  Wavefront w owns
-// the 32 queries t0 + 32w + [0, 32).  The working sets of the tile are
-//   window keys   [max(0, t0-k), t0+127]  -- a band, streamed in 64-key tiles
-//   partner keys  [t0-pi, t0-pi+127]      -- one contiguous shifted tile
-// (Sec. 3.5, eq. online_ws: the partner rows of consecutive queries are
-// consecutive, so the long-range fetch is a coalesced tile, not a gather).
+// BM = 128 consecutive positions [t0, t0+128) of one (b, h); wavefront w owns
+// the 32 queries q0 = t0 + 32w + [0, 32).  The window keys of the tile,
+// [max(0, t0-k), t0+127], form a band that is streamed through LDS in 64-row
+// tiles (two 32-key blocks, aligned to multiples of 32); each wavefront works
+// on the blocks that meet its own band [q0 - k, q0 + 31].  Two work-groups
+// share a CU, so each SIMD interleaves two wavefronts.
 //
-// Scores are computed transposed, S^T = K Q^T, on v_mfma_f32_32x32x16_bf16:
-//   A = K tile rows (32 keys x 16 dims, from LDS),
-//   B = Q^T (16 dims x 32 queries, resident in registers for the whole tile),
-//   C = 32 keys x 32 queries; lane l holds query column l%32 and key rows
-//       8i + 4(l/32) + j in accumulator slot 4i+j.
-// A lane therefore holds one query's scores, so the softmax row reductions
-// are in-lane plus one exchange with lane l^32.  The output is O^T = V^T P^T
-// on the same instruction: B = P^T comes straight from the score registers
-// (slots 8c..8c+7 of a 32-key block are the B operand of key chunk c, with
-// the key order permuted inside the chunk), A = V^T read from a transposed
-// LDS copy of the value tile with the same permutation.
+// MFMA layout (v_mfma_f32_32x32x16_bf16).  Scores are computed transposed,
+// S^T = K Q^T: A = 32 key rows x 16 dims read from LDS, B = Q^T kept in
+// registers for the whole tile, C = 32 keys x 32 queries, so lane l holds the
+// scores of query l%32 for keys 8i + 4(l/32) + j in accumulator slot 4i+j;
+// the softmax row reductions are in-lane plus one exchange between the two
+// halves of the wavefront.  The output is O^T = V^T P^T on the same
+// instruction: B = P^T is taken straight from the score registers (slots
+// 8c..8c+7 feed key chunk c, with the key order permuted inside the chunk)
+// and A = V^T comes from the LDS transpose read (ds_read_b64_tr_b16) of the
+// row-major value tile, with the same permutation.
 //
-// The partner block joins the same online softmax: it is processed first, as
-// a 32x32 score block whose only valid entries are on the diagonal (query i
-// of the wavefront pairs with key row i of its partner rows).
+// Tiles are staged global -> registers -> LDS, the next tile in two halves
+// while the two blocks of the current one are consumed, row-major with the
+// 16-byte chunks of row r XOR-swizzled (K: chunk ^ (r mod chunks-per-row);
+// V: chunk ^ 2(r mod 4)) so that the fragment reads and the transpose reads
+// are free of bank conflicts.
+//
+// The long-range partner (Sec. 3.4, eq. Npi; Sec. 3.5, eq. online_ws): the
+// partner rows of a wavefront's 32 queries are 32 consecutive rows shifted by
+// pi, read straight from global memory into the MFMA operand layout.  Its
+// score (the diagonal of one 32x32 MFMA block) seeds the online softmax:
+// running max = partner logit, running sum = 1, accumulator = partner value.
+//
+// Online softmax with a lazily updated maximum: a lane raises its reference
+// maximum m only when a block's maximum exceeds it by more than 2^8 (exp2
+// units); otherwise probabilities exp2(s - m) <= 256 are accumulated against
+// the stale m, which changes nothing in exact arithmetic (numerator and
+// denominator share the reference) and keeps the rescale of the accumulators
+// out of the common path.
 #include "kernels.h"
 #include "pi_common.h"
 
@@ -33,178 +47,171 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr int BM = 128;       // queries per work-group
-constexpr int BN = 64;        // keys per LDS tile
-constexpr int QW = 32;        // queries per wavefront
-constexpr int NT = 256;       // threads per work-group
-constexpr int KPAD = 8;       // K tile row padding (elements)
-constexpr int VPAD = 4;       // V^T tile row padding (elements)
+constexpr int WAVES = 4;
+constexpr int NT = 64 * WAVES;   // threads per work-group
+constexpr int BM = 32 * WAVES;   // queries per work-group
+constexpr int TK = 64;           // key rows per LDS tile
+constexpr float kTau = 8.0f;     // lazy-max threshold, log2 units
 
 template <int D>
-struct Smem {
-    __bf16 k[2][BN][D + KPAD];     // key rows, row-major
-    __bf16 vt[2][D][BN + VPAD];    // value tile, transposed (dim-major)
+struct Tile {
+    static constexpr int CPR = D / 8;   // 16-byte chunks per row
+    static constexpr int ROW_BYTES = 2 * D;
+    static constexpr int BYTES = TK * ROW_BYTES;
 };
 
-// Register staging of one 64-key tile: K and V rows as 16-byte chunks.
+// One LDS tile buffer: 64 key rows and 64 value rows.  The kernel declares
+// two of them (double buffering) as separate objects.
 template <int D>
-struct Stage {
-    static constexpr int CH = BN * D / 8 / NT;   // 16-byte chunks per thread (4 or 2)
-    uint4 kc[CH];
-    uint4 vc[CH];
+struct TileBuf {
+    alignas(16) unsigned char k[Tile<D>::BYTES];
+    alignas(16) unsigned char v[Tile<D>::BYTES];
 };
+
+__device__ inline int k_swz(int row, int chunk, int cpr) { return chunk ^ (row & (cpr - 1)); }
+__device__ inline int v_swz(int row, int chunk) { return chunk ^ ((row & 3) << 1); }
 
 __device__ inline uint4 ld16(const __bf16 *p) { return *reinterpret_cast<const uint4 *>(p); }
 
-// Issue the global loads of key/value rows [row0, row0+64); rows outside
-// [0, lim) are not read and stage as zero.  For window tiles lim is the end
-// of the query tile, so no row later than every query of the tile is ever
-// touched (a masked weight is 0, but 0 times a non-finite value is not).
+// Register staging of half a 64-row tile.  Chunk u of half hf for thread i
+// is tile chunk cid = i + NT*(hf*CH + u): physical chunk cid % CPR of tile
+// row cid / CPR, so consecutive threads read consecutive 16 bytes of a row
+// (the swizzle only permutes the chunks of a row among themselves).
 template <int D>
-__device__ inline void stage_load(Stage<D> &st, const __bf16 *kb, const __bf16 *vb, int64_t sn, int row0, int lim,
-                                  int tid) {
-    constexpr int CPR = D / 8;   // chunks per row
-#pragma unroll
-    for (int c = 0; c < Stage<D>::CH; ++c) {
-        // K: consecutive threads take consecutive chunks of a row.
-        int cid = tid + NT * c;
-        int r = cid / CPR, col = cid % CPR;
-        int gr = row0 + r;
-        st.kc[c] = (gr >= 0 && gr < lim) ? ld16(kb + gr * sn + col * 8) : make_uint4(0, 0, 0, 0);
-        // V: thread owns CH consecutive rows of one 8-dim chunk (for the
-        // transposed store); each load instruction still reads whole rows.
-        int vcol = tid % CPR, vrg = tid / CPR;
-        int vr = vrg * Stage<D>::CH + c;
-        int gv = row0 + vr;
-        st.vc[c] = (gv >= 0 && gv < lim) ? ld16(vb + gv * sn + vcol * 8) : make_uint4(0, 0, 0, 0);
-    }
-}
-
-template <int D>
-__device__ inline void stage_store(const Stage<D> &st, Smem<D> &sm, int buf, int tid) {
-    constexpr int CPR = D / 8;
-    constexpr int CH = Stage<D>::CH;
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-        int cid = tid + NT * c;
-        int r = cid / CPR, col = cid % CPR;
-        *reinterpret_cast<uint4 *>(&sm.k[buf][r][col * 8]) = st.kc[c];
-    }
-    int vcol = tid % CPR, vrg = tid / CPR;
-    const bf16x8 *rows = reinterpret_cast<const bf16x8 *>(st.vc);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        if constexpr (CH == 4) {
-            bf16x4 w = {rows[0][i], rows[1][i], rows[2][i], rows[3][i]};
-            *reinterpret_cast<bf16x4 *>(&sm.vt[buf][vcol * 8 + i][vrg * 4]) = w;
-        } else {
-            bf16x2 w = {rows[0][i], rows[1][i]};
-            *reinterpret_cast<bf16x2 *>(&sm.vt[buf][vcol * 8 + i][vrg * 2]) = w;
-        }
-    }
-}
-
-// Per-wavefront online-softmax state for its 32 queries (lane = query l%32).
-template <int D>
-struct WaveState {
-    static constexpr int DB = D / 32;   // 32-dim output blocks
-    static constexpr int KS = D / 16;   // 16-dim k-steps of the score MFMA
-    bf16x8 qb[KS];                      // B operand: Q[t][16s + 8g .. +8]
-    f32x16 o[DB];                       // O^T accumulators
-    float m;                            // running max (log2 domain)
-    float l;                            // this lane's partial running sum
+struct Stage {
+    static constexpr int CH = TK * Tile<D>::CPR / NT / 2;   // chunks per thread, tensor and half
+    uint4 k[CH];
+    uint4 v[CH];
 };
 
-// S^T block (32 keys x 32 queries) for key rows [r0, r0+32) of LDS buffer buf.
+// Load half hf of key/value rows [row0, row0 + 64) of one (b, h).  Rows at
+// or beyond `lim` (the end of the query tile, or N) are not read and stage as
+// zeros: no row later than every query of the tile is ever touched (a masked
+// weight is 0, but 0 times a non-finite value is not).
 template <int D>
-__device__ inline f32x16 score_block(const Smem<D> &sm, int buf, int r0, const WaveState<D> &ws, int lane) {
-    f32x16 acc = {};
-    const int row = r0 + (lane & 31), g = lane >> 5;
+__device__ inline void tile_load(Stage<D> &st, const __bf16 *kb, const __bf16 *vb, int64_t sn, int row0, int lim,
+                                 int hf, int tid) {
+    using T = Tile<D>;
 #pragma unroll
-    for (int s = 0; s < WaveState<D>::KS; ++s) {
-        bf16x8 a = *reinterpret_cast<const bf16x8 *>(&sm.k[buf][row][16 * s + 8 * g]);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, ws.qb[s], acc, 0, 0, 0);
+    for (int u = 0; u < Stage<D>::CH; ++u) {
+        const int cid = tid + NT * (hf * Stage<D>::CH + u);
+        const int row = cid / T::CPR, pc = cid % T::CPR;
+        const int grow = row0 + row;
+        const bool ok = grow < lim;
+        st.k[u] = ok ? ld16(kb + grow * sn + k_swz(row, pc, T::CPR) * 8) : make_uint4(0, 0, 0, 0);
+        st.v[u] = ok ? ld16(vb + grow * sn + v_swz(row, pc) * 8) : make_uint4(0, 0, 0, 0);
     }
-    return acc;
 }
 
-// O^T += V^T P^T over key rows [r0, r0+32) of buffer buf.  pb[c] is the B
-// operand of key chunk c (keys 16c + {4g..4g+3, 8+4g..8+4g+3}).
 template <int D>
-__device__ inline void pv_block(const Smem<D> &sm, int buf, int r0, const bf16x8 pb[2], WaveState<D> &ws,
-                                int lane) {
-    const int dl = lane & 31, g = lane >> 5;
+__device__ inline void tile_store(const Stage<D> &st, TileBuf<D> &tb, int hf, int tid) {
+#pragma unroll
+    for (int u = 0; u < Stage<D>::CH; ++u) {
+        const int cid = tid + NT * (hf * Stage<D>::CH + u);   // = row * CPR + physical chunk
+        *reinterpret_cast<uint4 *>(tb.k + cid * 16) = st.k[u];
+        *reinterpret_cast<uint4 *>(tb.v + cid * 16) = st.v[u];
+    }
+}
+
+// The value held by the other half of the wavefront (lane l ^ 32).
+__device__ inline float other_half(float x) {
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(__lane_id() < 32 ? p[1] : p[0]);
+}
+
+__device__ inline float max16(const f32x16 &a) {
+    float m0 = fmaxf(fmaxf(a[0], a[1]), a[2]), m1 = fmaxf(fmaxf(a[3], a[4]), a[5]);
+    float m2 = fmaxf(fmaxf(a[6], a[7]), a[8]), m3 = fmaxf(fmaxf(a[9], a[10]), a[11]);
+    float m4 = fmaxf(fmaxf(a[12], a[13]), a[14]);
+    return fmaxf(fmaxf(fmaxf(m0, m1), fmaxf(m2, m3)), fmaxf(m4, a[15]));
+}
+
+// Per-wavefront state: lane (c, g) = (l % 32, l / 32) belongs to query q0 + c.
+template <int D>
+struct Wave {
+    static constexpr int DB = D / 32;   // 32-dim output blocks
+    static constexpr int KS = D / 16;   // 16-dim k-steps of the score MFMA
+    bf16x8 qf[KS];                      // B operand: Q[t][16s + 8g .. +8]
+    f32x16 o[DB];                       // O^T accumulators: dims 32db + 8i + 4g + j
+    float m;                            // reference (lazy) maximum, log2 units
+    float l;                            // this lane's part of the running sum
+};
+
+// Scores of one 32-key block -> log2-unit logits (masked to -inf on edge
+// blocks), running state update, and bf16 probabilities for the value product.
+template <int D, bool CLAMP>
+__device__ inline void softmax_block(Wave<D> &ws, f32x16 &s, bool edge, int j0, int t, int kw, bool t_ok, float c2,
+                                     float scale, float bias, float clampv, int g, bf16x8 pb[2]) {
+    if constexpr (CLAMP) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) s[e] = fminf(fmaxf(s[e] * scale + bias, -clampv), clampv) * kLog2e;
+    }
+    if (edge) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int j = j0 + 8 * (e >> 2) + 4 * g + (e & 3);
+            const bool ok = t_ok && j <= t && j >= t - kw;
+            s[e] = ok ? s[e] : -INFINITY;
+        }
+    }
+    float mx = max16(s);
+    mx = fmaxf(mx, other_half(mx));
+    if constexpr (!CLAMP) mx *= c2;
+    // Only lanes whose own maximum moved update their reference (the others
+    // scale by exactly 1), so a query's result never depends on the data of
+    // the other queries sharing the wavefront.
+    const bool need = mx > ws.m + kTau;
+    if (__builtin_amdgcn_ballot_w64(need)) {
+        const float m_new = need ? mx : ws.m;
+        const float alpha = need ? __builtin_amdgcn_exp2f(ws.m - m_new) : 1.0f;
+        ws.m = m_new;
+        ws.l *= alpha;
+#pragma unroll
+        for (int db = 0; db < Wave<D>::DB; ++db) ws.o[db] *= alpha;
+    }
+    const float mu = ws.m == -INFINITY ? 0.0f : ws.m;
+    float lsum = 0.0f;
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-        const int kc = r0 + 16 * c + 4 * g;
 #pragma unroll
-        for (int db = 0; db < WaveState<D>::DB; ++db) {
-            const __bf16 *vrow = &sm.vt[buf][32 * db + dl][0];
-            bf16x4 lo = *reinterpret_cast<const bf16x4 *>(vrow + kc);
-            bf16x4 hi = *reinterpret_cast<const bf16x4 *>(vrow + kc + 8);
-            bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-            ws.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[c], ws.o[db], 0, 0, 0);
-        }
-    }
-}
-
-__device__ inline float xor32_max(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
-
-// Fold up to two scored 32-key blocks (already in log2 units, -inf where
-// invalid) into the running state and accumulate their values.
-template <int D, int NBLK>
-__device__ inline void softmax_pv(const Smem<D> &sm, int buf, const int r0[NBLK], const bool act[NBLK],
-                                  f32x16 sc[NBLK], WaveState<D> &ws, int lane) {
-    float mx = -INFINITY;
-#pragma unroll
-    for (int b = 0; b < NBLK; ++b)
-        if (act[b]) {
-#pragma unroll
-            for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc[b][e]);
-        }
-    mx = xor32_max(mx);
-    const float m_new = fmaxf(ws.m, mx);
-    const float m_use = m_new == -INFINITY ? 0.0f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(ws.m - m_use);
-    ws.m = m_new;
-    ws.l *= alpha;
-#pragma unroll
-    for (int db = 0; db < WaveState<D>::DB; ++db) ws.o[db] *= alpha;
-#pragma unroll
-    for (int b = 0; b < NBLK; ++b) {
-        if (!act[b]) continue;
-        bf16x8 pb[2];
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                float pr = __builtin_amdgcn_exp2f(sc[b][8 * c + e] - m_use);
-                ws.l += pr;
-                pb[c][e] = (__bf16)pr;
+        for (int e = 0; e < 8; ++e) {
+            float v;
+            if constexpr (CLAMP) {
+                v = s[8 * c + e] - mu;
+            } else {
+                v = __builtin_fmaf(s[8 * c + e], c2, -mu);
             }
+            const float p = __builtin_amdgcn_exp2f(v);
+            lsum += p;
+            pb[c][e] = (__bf16)p;
         }
-        pv_block<D>(sm, buf, r0[b], pb, ws, lane);
     }
+    ws.l += lsum;
 }
 
 template <int D, bool CLAMP>
 __global__ __launch_bounds__(NT, 2) void forward_bf16_kernel(FwdParams p, int n_qt, int64_t n_logical) {
-    __shared__ Smem<D> sm;
+    using T = Tile<D>;
+    using W = Wave<D>;
+    __shared__ TileBuf<D> tA, tB;
     const int64_t logical = xcd_remap(blockIdx.x, n_logical);
     if (logical < 0) return;
     const int qt = (int)(logical % n_qt);
     const int64_t bh = logical / n_qt;
     const int h = (int)(bh % p.H), b = (int)(bh / p.H);
 
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x;
+    const int lane = __lane_id();
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 5, c = lane & 31;
-    const int N = p.N, kw = p.k;
+    const int N = p.N, kw = p.k, pi = p.pi;
     const int t0 = qt * BM;
-    const int qw0 = t0 + QW * w;    // first query of this wavefront
-    const int t = qw0 + c;          // this lane's query
+    const int q0 = t0 + 32 * w;   // first query of this wavefront
+    const int t = q0 + c;         // this lane's query
     const bool t_ok = t < N;
 
     const int64_t base = b * p.sb + h * p.sh;
@@ -213,127 +220,151 @@ __global__ __launch_bounds__(NT, 2) void forward_bf16_kernel(FwdParams p, int n_
     const __bf16 *vp = (const __bf16 *)p.v + base;
     const int64_t sn = p.sn;
 
-    WaveState<D> ws;
-#pragma unroll
-    for (int s = 0; s < WaveState<D>::KS; ++s) {
-        if (t_ok) {
-            ws.qb[s] = *reinterpret_cast<const bf16x8 *>(qp + t * sn + 16 * s + 8 * g);
-        } else {
-            ws.qb[s] = bf16x8{};
-        }
-    }
-#pragma unroll
-    for (int db = 0; db < WaveState<D>::DB; ++db) ws.o[db] = f32x16{};
-    ws.m = -INFINITY;
-    ws.l = 0.0f;
+    // Window tiles: rows [kb0, kend) in 64-row steps, blocks aligned to 32.
+    const int kb0 = window_lo(t0, kw) & ~31;
+    const int kend = min(t0 + BM, N);
+    const int ntiles = (kend - kb0 + TK - 1) / TK;
+    Stage<D> st;
+    tile_load<D>(st, kp, vp, sn, kb0, kend, 0, tid);
 
+    // ---- query fragments, gate, partner seed --------------------------------
+    W ws;
+#pragma unroll
+    for (int s = 0; s < W::KS; ++s)
+        ws.qf[s] = t_ok ? *reinterpret_cast<const bf16x8 *>(qp + t * sn + 16 * s + 8 * g) : bf16x8{};
     const float gl = p.gate[b * p.gsb + h * p.gsh + (t_ok ? t : 0) * p.gsn];
     const FusionBias fb = fusion_bias(gl, CLAMP);
-    const float c2 = p.scale * kLog2e;          // score -> log2 units
-    const float clampv = p.clamp;
+    const float c2 = p.scale * kLog2e;
 
-    // ---- partner tile: rows [t0 - pi, t0 - pi + 128) -------------------
-    const bool has_partner = partner_enabled(kw, p.pi) && (t0 + BM - 1) >= p.pi && t0 < N;
-    Stage<D> st;
-    if (has_partner) {
-        const int prow0 = t0 - p.pi;
+    // Partner rows: A-operand row c of the wavefront is row q0 + c - pi, the
+    // partner of query q0 + c.
+    const int prow = t - pi;
+    const bool has_p = partner_enabled(kw, pi) && prow >= 0 && t_ok;   // depends on c only
+    ws.m = -INFINITY;
+    if (__builtin_amdgcn_ballot_w64(has_p)) {
+        f32x16 acc = {};
 #pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            stage_load<D>(st, kp, vp, sn, prow0 + BN * half, N, tid);
-            stage_store<D>(st, sm, half, tid);
+        for (int s = 0; s < W::KS; ++s) {
+            const bf16x8 a = has_p ? *reinterpret_cast<const bf16x8 *>(kp + prow * sn + 16 * s + 8 * g) : bf16x8{};
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, ws.qf[s], acc, 0, 0, 0);
+        }
+        // The diagonal entry (row c, column c) sits in half (c/4)%2 at slot
+        // 4(c/8) + c%4.
+        const int slot = 4 * (c >> 3) + (c & 3);
+        float mine = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) mine = (e == slot) ? acc[e] : mine;
+        const float theirs = other_half(mine);
+        const float diag = (g == ((c >> 2) & 1)) ? mine : theirs;
+        float sp;
+        if constexpr (CLAMP) {
+            sp = fminf(fmaxf(diag * p.scale + fb.partner, -p.clamp), p.clamp) * kLog2e;
+        } else {
+            sp = diag * c2 + fb.partner * kLog2e;
+        }
+        ws.m = has_p ? sp : -INFINITY;
+    }
+    ws.l = (has_p && g == 0) ? 1.0f : 0.0f;
+    // Accumulator seed: lane (c, g) holds dims 32db + 8i + 4g + [0, 4).
+#pragma unroll
+    for (int db = 0; db < W::DB; ++db) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            uint2 raw = make_uint2(0, 0);
+            if (has_p) raw = *reinterpret_cast<const uint2 *>(vp + prow * sn + 32 * db + 8 * i + 4 * g);
+            ws.o[db][4 * i + 0] = __uint_as_float(raw.x << 16);
+            ws.o[db][4 * i + 1] = __uint_as_float(raw.x & 0xffff0000u);
+            ws.o[db][4 * i + 2] = __uint_as_float(raw.y << 16);
+            ws.o[db][4 * i + 3] = __uint_as_float(raw.y & 0xffff0000u);
         }
     }
-    // window tiles: [kstart, kend) in 64-key steps
-    const int kstart = window_lo(t0, kw);
-    const int kend = min(t0 + BM, N);
-    const int ntiles = kend > kstart ? (kend - kstart + BN - 1) / BN : 0;
-    if (ntiles > 0) stage_load<D>(st, kp, vp, sn, kstart, kend, tid);
-    if (has_partner) {
-        __syncthreads();
-        // wavefront w's partner rows are rows 32w.. of the 128-row tile:
-        // buffer w/2, block (w%2)
-        if (qw0 + QW - 1 >= p.pi && qw0 < N) {
-            const int buf = w >> 1, r0 = QW * (w & 1);
-            f32x16 raw = score_block<D>(sm, buf, r0, ws, lane);
-            f32x16 sc[1];
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int r = 8 * (e >> 2) + 4 * g + (e & 3);   // key row in block
-                const bool valid = (r == c) && t_ok && t >= p.pi;
-                float v;
-                if constexpr (CLAMP) {
-                    v = fminf(fmaxf(raw[e] * p.scale + fb.partner, -clampv), clampv) * kLog2e;
-                } else {
-                    v = raw[e] * c2 + fb.partner * kLog2e;
-                }
-                sc[0][e] = valid ? v : -INFINITY;
-            }
-            const int r0a[1] = {r0};
-            const bool act[1] = {true};
-            softmax_pv<D, 1>(sm, buf, r0a, act, sc, ws, lane);
-        }
-        __syncthreads();
-    }
-    if (ntiles > 0) {
-        stage_store<D>(st, sm, 0, tid);
-        __syncthreads();
-    }
 
-    // ---- window band ----------------------------------------------------
-    for (int it = 0; it < ntiles; ++it) {
-        const int buf = it & 1;
-        const int j0 = kstart + BN * it;
-        if (it + 1 < ntiles) stage_load<D>(st, kp, vp, sn, j0 + BN, kend, tid);
+    tile_store<D>(st, tA, 0, tid);
+    tile_load<D>(st, kp, vp, sn, kb0, kend, 1, tid);
+    tile_store<D>(st, tA, 1, tid);
+    __syncthreads();
 
-        // blocks of this tile that intersect the wavefront's band
-        // [qw0 - k, qw0 + 31]
-        bool act[2];
-        int r0a[2];
-        bool any = false;
+    // ---- window band -------------------------------------------------------
+    // One 32-key block: rows [32 blk, 32 blk + 32) of the tile at kt / vt,
+    // keys [j0, j0 + 32).
+    auto block = [&](const unsigned char *kt, const unsigned char *vt, int j0, int blk) {
+        // Wave-uniform: does the block meet the band, is it wholly inside it?
+        const bool act = j0 < kend && q0 < N && j0 <= q0 + 31 && j0 + 31 >= q0 - kw;
+        if (!act) return;
+        const bool edge = !(j0 + 31 <= q0 && j0 >= q0 + 31 - kw) || q0 + 31 >= N;
+
+        // Fragment reads of the whole block are issued together, ahead of
+        // the MFMAs, so their LDS latency overlaps: K rows (A operand of
+        // the scores) and, by transpose reads, V^T (A operand of O^T).
+        const int krow = 32 * blk + c;
+        bf16x8 kf[W::KS];
 #pragma unroll
-        for (int bb = 0; bb < 2; ++bb) {
-            const int jb = j0 + QW * bb;
-            r0a[bb] = QW * bb;
-            act[bb] = (jb <= qw0 + QW - 1) && (jb + QW - 1 >= qw0 - kw) && (jb < N) && (qw0 < N);
-            any |= act[bb];
-        }
-        if (any) {
-            f32x16 sc[2];
+        for (int s = 0; s < W::KS; ++s)
+            kf[s] = *reinterpret_cast<const bf16x8 *>(kt + krow * T::ROW_BYTES + k_swz(krow, 2 * s + g, T::CPR) * 16);
+        const int G = lane >> 4, r = (lane >> 2) & 3, qd = lane & 3;
+        bf16x8 vf[2][W::DB];
 #pragma unroll
-            for (int bb = 0; bb < 2; ++bb) {
-                if (!act[bb]) continue;
-                f32x16 raw = score_block<D>(sm, buf, r0a[bb], ws, lane);
-                const int jb = j0 + QW * bb;
-                // interior: every key of the block is in every query's window
-                const bool interior = (jb + QW - 1 <= qw0) && (jb >= qw0 + QW - 1 - kw);
+        for (int cc = 0; cc < 2; ++cc) {
 #pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    float v;
-                    if constexpr (CLAMP) {
-                        v = fminf(fmaxf(raw[e] * p.scale + fb.local, -clampv), clampv) * kLog2e;
-                    } else {
-                        v = raw[e] * c2;
-                    }
-                    if (!interior) {
-                        const int j = jb + 8 * (e >> 2) + 4 * g + (e & 3);
-                        v = in_window(j, t, kw) ? v : -INFINITY;
-                    }
-                    sc[bb][e] = v;
+            for (int db = 0; db < W::DB; ++db) {
+#pragma unroll
+                for (int hh = 0; hh < 2; ++hh) {
+                    const int vrow = 32 * blk + 16 * cc + 8 * hh + 4 * g + r;
+                    const int chunk = 4 * db + 2 * (G & 1) + (qd >> 1);
+                    const unsigned char *src = vt + vrow * T::ROW_BYTES + v_swz(vrow, chunk) * 16 + (qd & 1) * 8;
+                    const bf16x4 y =
+                        __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)src));
+                    vf[cc][db][4 * hh + 0] = y[0];
+                    vf[cc][db][4 * hh + 1] = y[1];
+                    vf[cc][db][4 * hh + 2] = y[2];
+                    vf[cc][db][4 * hh + 3] = y[3];
                 }
             }
-            softmax_pv<D, 2>(sm, buf, r0a, act, sc, ws, lane);
         }
-        if (it + 1 < ntiles) stage_store<D>(st, sm, buf ^ 1, tid);
+        __builtin_amdgcn_sched_barrier(0);
+
+        f32x16 sc = {};
+#pragma unroll
+        for (int s = 0; s < W::KS; ++s) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], ws.qf[s], sc, 0, 0, 0);
+        bf16x8 pb[2];
+        softmax_block<D, CLAMP>(ws, sc, edge, j0, t, kw, t_ok, c2, p.scale, fb.local, p.clamp, g, pb);
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc) {
+#pragma unroll
+            for (int db = 0; db < W::DB; ++db)
+                ws.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[cc][db], pb[cc], ws.o[db], 0, 0, 0);
+        }
+    };
+    // One 64-row tile; while block blk is consumed, half blk of the next tile
+    // (if any) is loaded into registers and then stored to the other buffer,
+    // which every wavefront finished reading before the last barrier.
+    auto tile = [&](const TileBuf<D> &cur, int row0, TileBuf<D> &nxt, bool has_next) {
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk) {
+            if (has_next) tile_load<D>(st, kp, vp, sn, row0 + TK, kend, blk, tid);
+            block(cur.k, cur.v, row0 + 32 * blk, blk);
+            if (has_next) tile_store<D>(st, nxt, blk, tid);
+        }
+    };
+    // Double buffering, unrolled by two so that every store and every read
+    // names its buffer statically.
+    for (int it = 0; it < ntiles; it += 2) {
+        const int row0 = kb0 + TK * it;
+        tile(tA, row0, tB, it + 1 < ntiles);
+        if (it + 1 >= ntiles) break;
+        __syncthreads();
+        tile(tB, row0 + TK, tA, it + 2 < ntiles);
+        if (it + 2 >= ntiles) break;
         __syncthreads();
     }
 
-    // ---- normalise and store ---------------------------------------------
-    const float l_tot = ws.l + __shfl_xor(ws.l, 32);
+    // ---- normalise and store -----------------------------------------------
+    const float l_tot = ws.l + other_half(ws.l);
     if (t_ok) {
         const float inv = 1.0f / l_tot;
         __bf16 *op = (__bf16 *)p.out + b * p.osb + h * p.osh + t * p.osn;
 #pragma unroll
-        for (int db = 0; db < WaveState<D>::DB; ++db) {
+        for (int db = 0; db < W::DB; ++db) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 bf16x4 o4;
@@ -342,9 +373,7 @@ __global__ __launch_bounds__(NT, 2) void forward_bf16_kernel(FwdParams p, int n_
                 *reinterpret_cast<bf16x4 *>(op + 32 * db + 8 * i + 4 * g) = o4;
             }
         }
-        if (p.lse && g == 0) {
-            p.lse[bh * N + t] = (ws.m + __log2f(l_tot)) * kLn2 + fb.lse_shift;
-        }
+        if (p.lse && g == 0) p.lse[bh * N + t] = (ws.m + __log2f(l_tot)) * kLn2 + fb.lse_shift;
     }
 }
 
