@@ -55,6 +55,7 @@ constexpr int WAVES = 4;
 constexpr int NT = 64 * WAVES;   // threads per work-group
 constexpr int BM = 32 * WAVES;   // queries per work-group
 constexpr int TK = 64;           // key rows per LDS tile
+constexpr int BPT = TK / 32;     // 32-key blocks per tile
 constexpr float kTau = 8.0f;     // lazy-max threshold, log2 units
 
 template <int D>
@@ -83,15 +84,14 @@ __device__ inline uint4 ld16(const __bf16 *p) { return *reinterpret_cast<const u
 // (the swizzle only permutes the chunks of a row among themselves).
 template <int D>
 struct Stage {
-    static constexpr int CH = TK * Tile<D>::CPR / NT / 2;   // chunks per thread, tensor and half
+    static constexpr int CH = TK * Tile<D>::CPR / NT / BPT;   // chunks per thread, tensor and part
     uint4 k[CH];
     uint4 v[CH];
 };
 
-// Load half hf of key/value rows [row0, row0 + 64) of one (b, h).  Rows at
-// or beyond `lim` (the end of the query tile, or N) are not read and stage as
-// zeros: no row later than every query of the tile is ever touched (a masked
-// weight is 0, but 0 times a non-finite value is not).
+// Load half hf of key/value rows [row0, row0 + 64) of one (b, h).  The
+// loads are unconditional: a row at or beyond `lim` (the end of the query
+// tile, or N) reads row0 instead, and tile_store writes zeros for it.
 template <int D>
 __device__ inline void tile_load(Stage<D> &st, const __bf16 *kb, const __bf16 *vb, int64_t sn, int row0, int lim,
                                  int hf, int tid) {
@@ -101,19 +101,26 @@ __device__ inline void tile_load(Stage<D> &st, const __bf16 *kb, const __bf16 *v
         const int cid = tid + NT * (hf * Stage<D>::CH + u);
         const int row = cid / T::CPR, pc = cid % T::CPR;
         const int grow = row0 + row;
-        const bool ok = grow < lim;
-        st.k[u] = ok ? ld16(kb + grow * sn + k_swz(row, pc, T::CPR) * 8) : make_uint4(0, 0, 0, 0);
-        st.v[u] = ok ? ld16(vb + grow * sn + v_swz(row, pc) * 8) : make_uint4(0, 0, 0, 0);
+        const int lrow = grow < lim ? grow : row0;
+        st.k[u] = ld16(kb + lrow * sn + k_swz(row, pc, T::CPR) * 8);
+        st.v[u] = ld16(vb + lrow * sn + v_swz(row, pc) * 8);
     }
 }
 
+// Store half hf of a staged tile.  Rows at or beyond `lim` are stored as
+// zeros, so no data of a row later than every query of the tile is ever
+// used (a masked weight is 0, but 0 times a non-finite value is not); whole
+// tiles below `lim` (all but the last) skip the check.
 template <int D>
-__device__ inline void tile_store(const Stage<D> &st, TileBuf<D> &tb, int hf, int tid) {
+__device__ inline void tile_store(const Stage<D> &st, TileBuf<D> &tb, int hf, int tid, int row0, int lim) {
+    using T = Tile<D>;
+    const bool full = row0 + TK <= lim;   // wave-uniform
 #pragma unroll
     for (int u = 0; u < Stage<D>::CH; ++u) {
         const int cid = tid + NT * (hf * Stage<D>::CH + u);   // = row * CPR + physical chunk
-        *reinterpret_cast<uint4 *>(tb.k + cid * 16) = st.k[u];
-        *reinterpret_cast<uint4 *>(tb.v + cid * 16) = st.v[u];
+        const bool ok = full || row0 + cid / T::CPR < lim;
+        *reinterpret_cast<uint4 *>(tb.k + cid * 16) = ok ? st.k[u] : make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4 *>(tb.v + cid * 16) = ok ? st.v[u] : make_uint4(0, 0, 0, 0);
     }
 }
 
@@ -224,30 +231,52 @@ __global__ __launch_bounds__(NT, 2) void forward_bf16_kernel(FwdParams p, int n_
     const int kb0 = window_lo(t0, kw) & ~31;
     const int kend = min(t0 + BM, N);
     const int ntiles = (kend - kb0 + TK - 1) / TK;
+    // ---- prologue: every load is issued before any is waited for ----------
+    // (the first tile, the query fragments, the gate logit and the partner
+    // key/value rows), so the prologue costs one memory round trip.
     Stage<D> st;
-    tile_load<D>(st, kp, vp, sn, kb0, kend, 0, tid);
-
-    // ---- query fragments, gate, partner seed --------------------------------
-    W ws;
+    Stage<D> st0[BPT];
 #pragma unroll
-    for (int s = 0; s < W::KS; ++s)
-        ws.qf[s] = t_ok ? *reinterpret_cast<const bf16x8 *>(qp + t * sn + 16 * s + 8 * g) : bf16x8{};
-    const float gl = p.gate[b * p.gsb + h * p.gsh + (t_ok ? t : 0) * p.gsn];
-    const FusionBias fb = fusion_bias(gl, CLAMP);
-    const float c2 = p.scale * kLog2e;
+    for (int hf = 0; hf < BPT; ++hf) tile_load<D>(st0[hf], kp, vp, sn, kb0, kend, hf, tid);
+
+    // Loads use a clamped, always-readable row; lanes without a query or a
+    // partner zero the data afterwards.
+    W ws;
+    const int tq = t_ok ? t : 0;
+    bf16x8 qraw[W::KS];
+#pragma unroll
+    for (int s = 0; s < W::KS; ++s) qraw[s] = *reinterpret_cast<const bf16x8 *>(qp + tq * sn + 16 * s + 8 * g);
+    const float gl = p.gate[b * p.gsb + h * p.gsh + tq * p.gsn];
 
     // Partner rows: A-operand row c of the wavefront is row q0 + c - pi, the
-    // partner of query q0 + c.
+    // partner of query q0 + c; the accumulator seed is that row's value, of
+    // which lane (c, g) holds dims 32db + 8i + 4g + [0, 4).
     const int prow = t - pi;
     const bool has_p = partner_enabled(kw, pi) && prow >= 0 && t_ok;   // depends on c only
+    const bool any_p = __builtin_amdgcn_ballot_w64(has_p) != 0;       // wave-uniform
+    const int prc = has_p ? prow : 0;
+    bf16x8 kpf[W::KS];
+    uint2 vraw[W::DB][4];
+    if (any_p) {
+#pragma unroll
+        for (int s = 0; s < W::KS; ++s) kpf[s] = *reinterpret_cast<const bf16x8 *>(kp + prc * sn + 16 * s + 8 * g);
+#pragma unroll
+        for (int db = 0; db < W::DB; ++db)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                vraw[db][i] = *reinterpret_cast<const uint2 *>(vp + prc * sn + 32 * db + 8 * i + 4 * g);
+    }
+#pragma unroll
+    for (int s = 0; s < W::KS; ++s) ws.qf[s] = t_ok ? qraw[s] : bf16x8{};
+
+    const FusionBias fb = fusion_bias(gl, CLAMP);
+    const float c2 = p.scale * kLog2e;
     ws.m = -INFINITY;
-    if (__builtin_amdgcn_ballot_w64(has_p)) {
+    if (any_p) {
         f32x16 acc = {};
 #pragma unroll
-        for (int s = 0; s < W::KS; ++s) {
-            const bf16x8 a = has_p ? *reinterpret_cast<const bf16x8 *>(kp + prow * sn + 16 * s + 8 * g) : bf16x8{};
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, ws.qf[s], acc, 0, 0, 0);
-        }
+        for (int s = 0; s < W::KS; ++s)
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(has_p ? kpf[s] : bf16x8{}, ws.qf[s], acc, 0, 0, 0);
         // The diagonal entry (row c, column c) sits in half (c/4)%2 at slot
         // 4(c/8) + c%4.
         const int slot = 4 * (c >> 3) + (c & 3);
@@ -265,23 +294,19 @@ __global__ __launch_bounds__(NT, 2) void forward_bf16_kernel(FwdParams p, int n_
         ws.m = has_p ? sp : -INFINITY;
     }
     ws.l = (has_p && g == 0) ? 1.0f : 0.0f;
-    // Accumulator seed: lane (c, g) holds dims 32db + 8i + 4g + [0, 4).
 #pragma unroll
     for (int db = 0; db < W::DB; ++db) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            uint2 raw = make_uint2(0, 0);
-            if (has_p) raw = *reinterpret_cast<const uint2 *>(vp + prow * sn + 32 * db + 8 * i + 4 * g);
-            ws.o[db][4 * i + 0] = __uint_as_float(raw.x << 16);
-            ws.o[db][4 * i + 1] = __uint_as_float(raw.x & 0xffff0000u);
-            ws.o[db][4 * i + 2] = __uint_as_float(raw.y << 16);
-            ws.o[db][4 * i + 3] = __uint_as_float(raw.y & 0xffff0000u);
+            if (!has_p) vraw[db][i] = make_uint2(0, 0);
+            ws.o[db][4 * i + 0] = __uint_as_float(vraw[db][i].x << 16);
+            ws.o[db][4 * i + 1] = __uint_as_float(vraw[db][i].x & 0xffff0000u);
+            ws.o[db][4 * i + 2] = __uint_as_float(vraw[db][i].y << 16);
+            ws.o[db][4 * i + 3] = __uint_as_float(vraw[db][i].y & 0xffff0000u);
         }
     }
-
-    tile_store<D>(st, tA, 0, tid);
-    tile_load<D>(st, kp, vp, sn, kb0, kend, 1, tid);
-    tile_store<D>(st, tA, 1, tid);
+#pragma unroll
+    for (int hf = 0; hf < BPT; ++hf) tile_store<D>(st0[hf], tA, hf, tid, kb0, kend);
     __syncthreads();
 
     // ---- window band -------------------------------------------------------
@@ -340,10 +365,10 @@ __global__ __launch_bounds__(NT, 2) void forward_bf16_kernel(FwdParams p, int n_
     // which every wavefront finished reading before the last barrier.
     auto tile = [&](const TileBuf<D> &cur, int row0, TileBuf<D> &nxt, bool has_next) {
 #pragma unroll
-        for (int blk = 0; blk < 2; ++blk) {
+        for (int blk = 0; blk < BPT; ++blk) {
             if (has_next) tile_load<D>(st, kp, vp, sn, row0 + TK, kend, blk, tid);
             block(cur.k, cur.v, row0 + 32 * blk, blk);
-            if (has_next) tile_store<D>(st, nxt, blk, tid);
+            if (has_next) tile_store<D>(st, nxt, blk, tid, row0 + TK, kend);
         }
     };
     // Double buffering, unrolled by two so that every store and every read
