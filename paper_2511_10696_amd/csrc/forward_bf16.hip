@@ -201,7 +201,7 @@ __device__ inline void softmax_block(Wave<D> &ws, f32x16 &s, bool edge, int j0, 
 }
 
 template <int D, bool CLAMP>
-__global__ __launch_bounds__(NT, 2) void forward_bf16_kernel(FwdParams p, int n_qt, int64_t n_logical) {
+__global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdParams p, int n_qt, int64_t n_logical) {
     using T = Tile<D>;
     using W = Wave<D>;
     __shared__ TileBuf<D> tA, tB;
@@ -318,14 +318,20 @@ __global__ __launch_bounds__(NT, 2) void forward_bf16_kernel(FwdParams p, int n_
         if (!act) return;
         const bool edge = !(j0 + 31 <= q0 && j0 >= q0 + 31 - kw) || q0 + 31 >= N;
 
-        // Fragment reads of the whole block are issued together, ahead of
-        // the MFMAs, so their LDS latency overlaps: K rows (A operand of
-        // the scores) and, by transpose reads, V^T (A operand of O^T).
+        // Fragment reads: the K rows (A operand of the scores) are issued
+        // together ahead of the score MFMAs; the V^T reads (A operand of
+        // O^T, by transpose reads) go out behind the score MFMAs and land
+        // during the softmax.
         const int krow = 32 * blk + c;
         bf16x8 kf[W::KS];
 #pragma unroll
         for (int s = 0; s < W::KS; ++s)
             kf[s] = *reinterpret_cast<const bf16x8 *>(kt + krow * T::ROW_BYTES + k_swz(krow, 2 * s + g, T::CPR) * 16);
+        __builtin_amdgcn_sched_barrier(0);
+
+        f32x16 sc = {};
+#pragma unroll
+        for (int s = 0; s < W::KS; ++s) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], ws.qf[s], sc, 0, 0, 0);
         const int G = lane >> 4, r = (lane >> 2) & 3, qd = lane & 3;
         bf16x8 vf[2][W::DB];
 #pragma unroll
@@ -346,11 +352,6 @@ __global__ __launch_bounds__(NT, 2) void forward_bf16_kernel(FwdParams p, int n_
                 }
             }
         }
-        __builtin_amdgcn_sched_barrier(0);
-
-        f32x16 sc = {};
-#pragma unroll
-        for (int s = 0; s < W::KS; ++s) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s], ws.qf[s], sc, 0, 0, 0);
         bf16x8 pb[2];
         softmax_block<D, CLAMP>(ws, sc, edge, j0, t, kw, t_ok, c2, p.scale, fb.local, p.clamp, g, pb);
 #pragma unroll
