@@ -92,8 +92,8 @@ int pi_attn_index_set(int32_t n, int32_t k, int32_t pi, int32_t *idx, void *stre
  *   lse          optional device float32 [B][H][N] contiguous: natural-log
  *                sum over W_t of exp(delta), or NULL.
  * Errors: EINVAL (null pointer with non-empty problem, negative size or
- * stride, misalignment), EUNSUPPORTED (D not 64/128, unknown dtype),
- * EHIP (launch refused).
+ * stride, misalignment), EUNSUPPORTED (D not 64/128, unknown dtype; for
+ * bf16, (min(k, N) + 256) * sn * 2 bytes >= 2 GiB), EHIP (launch refused).
  */
 int pi_attn_forward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D,
                     int32_t k, int32_t pi,

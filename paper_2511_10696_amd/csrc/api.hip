@@ -1,6 +1,7 @@
 // api.hip -- the C ABI (include/pi_attn.h): argument validation and dispatch.
 // Nothing here allocates; every launch goes on the caller's stream.
 #include <math.h>
+#include <algorithm>
 #include <stdint.h>
 
 #include "../../include/pi_attn.h"
@@ -30,7 +31,9 @@ const char *pi_attn_strerror(int status) {
     switch (status) {
         case PI_ATTN_OK: return "ok";
         case PI_ATTN_EINVAL: return "invalid argument (null pointer, negative size or stride, misalignment)";
-        case PI_ATTN_EUNSUPPORTED: return "unsupported configuration (head dimension must be 64 or 128; dtype f32/bf16)";
+        case PI_ATTN_EUNSUPPORTED:
+            return "unsupported configuration (head dimension must be 64 or 128; dtype f32/bf16; bf16 forward: "
+                   "(k + 256) rows of keys must span under 2 GiB)";
         case PI_ATTN_EHIP: return "HIP runtime refused the launch";
         default: return "unknown status";
     }
@@ -67,6 +70,10 @@ int pi_attn_forward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, i
     if (!stride16(osb, es) || !stride16(osh, es) || !stride16(osn, es)) return PI_ATTN_EINVAL;
     if (!aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
     if (lse && !aligned4(lse)) return PI_ATTN_EINVAL;
+    // The bf16 kernel addresses one query tile's key/value rows (at most
+    // k + 256 of them) with 32-bit byte offsets.
+    if (dtype == PI_ATTN_BF16 && ((int64_t)std::min(k, N) + 256) * sn * es >= ((int64_t)1 << 31))
+        return PI_ATTN_EUNSUPPORTED;
 
     FwdParams p{};
     p.B = B; p.H = H; p.N = N; p.D = D; p.k = k; p.pi = pi;

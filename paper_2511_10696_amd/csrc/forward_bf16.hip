@@ -24,7 +24,10 @@
 // while the two blocks of the current one are consumed, row-major with the
 // 16-byte chunks of row r XOR-swizzled (K: chunk ^ (r mod chunks-per-row);
 // V: chunk ^ 2(r mod 4)) so that the fragment reads and the transpose reads
-// are free of bank conflicts.
+// are free of bank conflicts.  The global side uses buffer loads whose
+// descriptor range ends at the tile's last usable row: the hardware range
+// check zero-fills rows past it, and offsets are 32-bit with no per-load
+// clamping or 64-bit address arithmetic.
 //
 // The long-range partner (Sec. 3.4, eq. Npi; Sec. 3.5, eq. online_ws): the
 // partner rows of a wavefront's 32 queries are 32 consecutive rows shifted by
@@ -76,7 +79,6 @@ struct TileBuf {
 __device__ inline int k_swz(int row, int chunk, int cpr) { return chunk ^ (row & (cpr - 1)); }
 __device__ inline int v_swz(int row, int chunk) { return chunk ^ ((row & 3) << 1); }
 
-__device__ inline uint4 ld16(const __bf16 *p) { return *reinterpret_cast<const uint4 *>(p); }
 
 // Register staging of half a 64-row tile.  Chunk u of half hf for thread i
 // is tile chunk cid = i + NT*(hf*CH + u): physical chunk cid % CPR of tile
@@ -89,38 +91,35 @@ struct Stage {
     uint4 v[CH];
 };
 
-// Load half hf of key/value rows [row0, row0 + 64) of one (b, h).  The
-// loads are unconditional: a row at or beyond `lim` (the end of the query
-// tile, or N) reads row0 instead, and tile_store writes zeros for it.
+// Load half hf of the tile whose first row is `row0` rows past the window
+// start, through buffer descriptors that begin at the window start and end at
+// the last row the query tile may use: rows beyond it read as zeros, so no
+// data of a row later than every query of the tile is ever used (a masked
+// weight is 0, but 0 times a non-finite value is not).  Offsets are 32-bit
+// and span at most k + BM rows; `rowb` is the row stride in bytes.
 template <int D>
-__device__ inline void tile_load(Stage<D> &st, const __bf16 *kb, const __bf16 *vb, int64_t sn, int row0, int lim,
-                                 int hf, int tid) {
+__device__ inline void tile_load(Stage<D> &st, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv, int rowb,
+                                 int row0, int hf, int tid) {
     using T = Tile<D>;
 #pragma unroll
     for (int u = 0; u < Stage<D>::CH; ++u) {
         const int cid = tid + NT * (hf * Stage<D>::CH + u);
         const int row = cid / T::CPR, pc = cid % T::CPR;
-        const int grow = row0 + row;
-        const int lrow = grow < lim ? grow : row0;
-        st.k[u] = ld16(kb + lrow * sn + k_swz(row, pc, T::CPR) * 8);
-        st.v[u] = ld16(vb + lrow * sn + v_swz(row, pc) * 8);
+        const int off = (row0 + row) * rowb + k_swz(row, pc, T::CPR) * 16;
+        const int offv = (row0 + row) * rowb + v_swz(row, pc) * 16;
+        st.k[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, 0));
+        st.v[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, offv, 0, 0));
     }
 }
 
-// Store half hf of a staged tile.  Rows at or beyond `lim` are stored as
-// zeros, so no data of a row later than every query of the tile is ever
-// used (a masked weight is 0, but 0 times a non-finite value is not); whole
-// tiles below `lim` (all but the last) skip the check.
+// Store half hf of a staged tile.
 template <int D>
-__device__ inline void tile_store(const Stage<D> &st, TileBuf<D> &tb, int hf, int tid, int row0, int lim) {
-    using T = Tile<D>;
-    const bool full = row0 + TK <= lim;   // wave-uniform
+__device__ inline void tile_store(const Stage<D> &st, TileBuf<D> &tb, int hf, int tid) {
 #pragma unroll
     for (int u = 0; u < Stage<D>::CH; ++u) {
         const int cid = tid + NT * (hf * Stage<D>::CH + u);   // = row * CPR + physical chunk
-        const bool ok = full || row0 + cid / T::CPR < lim;
-        *reinterpret_cast<uint4 *>(tb.k + cid * 16) = ok ? st.k[u] : make_uint4(0, 0, 0, 0);
-        *reinterpret_cast<uint4 *>(tb.v + cid * 16) = ok ? st.v[u] : make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4 *>(tb.k + cid * 16) = st.k[u];
+        *reinterpret_cast<uint4 *>(tb.v + cid * 16) = st.v[u];
     }
 }
 
@@ -234,10 +233,17 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
     // ---- prologue: every load is issued before any is waited for ----------
     // (the first tile, the query fragments, the gate logit and the partner
     // key/value rows), so the prologue costs one memory round trip.
+    // Buffer descriptors over rows [kb0, kend) of this head's keys and values
+    // (word 3 is the gfx9 raw-buffer format: 32-bit data, range checked).
+    const int rowb = (int)(2 * sn);
+    const __amdgpu_buffer_rsrc_t rk =
+        __builtin_amdgcn_make_buffer_rsrc((void *)(kp + (int64_t)kb0 * sn), (short)0, (kend - kb0) * rowb, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rv =
+        __builtin_amdgcn_make_buffer_rsrc((void *)(vp + (int64_t)kb0 * sn), (short)0, (kend - kb0) * rowb, 0x00020000);
     Stage<D> st;
     Stage<D> st0[BPT];
 #pragma unroll
-    for (int hf = 0; hf < BPT; ++hf) tile_load<D>(st0[hf], kp, vp, sn, kb0, kend, hf, tid);
+    for (int hf = 0; hf < BPT; ++hf) tile_load<D>(st0[hf], rk, rv, rowb, 0, hf, tid);
 
     // Loads use a clamped, always-readable row; lanes without a query or a
     // partner zero the data afterwards.
@@ -306,7 +312,7 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
         }
     }
 #pragma unroll
-    for (int hf = 0; hf < BPT; ++hf) tile_store<D>(st0[hf], tA, hf, tid, kb0, kend);
+    for (int hf = 0; hf < BPT; ++hf) tile_store<D>(st0[hf], tA, hf, tid);
     __syncthreads();
 
     // ---- window band -------------------------------------------------------
@@ -367,9 +373,9 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
     auto tile = [&](const TileBuf<D> &cur, int row0, TileBuf<D> &nxt, bool has_next) {
 #pragma unroll
         for (int blk = 0; blk < BPT; ++blk) {
-            if (has_next) tile_load<D>(st, kp, vp, sn, row0 + TK, kend, blk, tid);
+            if (has_next) tile_load<D>(st, rk, rv, rowb, row0 - kb0 + TK, blk, tid);
             block(cur.k, cur.v, row0 + 32 * blk, blk);
-            if (has_next) tile_store<D>(st, nxt, blk, tid, row0 + TK, kend);
+            if (has_next) tile_store<D>(st, nxt, blk, tid);
         }
     };
     // Double buffering, unrolled by two so that every store and every read

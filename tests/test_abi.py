@@ -71,6 +71,9 @@ def fwd(lib, **kw):
     (dict(scale=0.0), EINVAL), (dict(scale=-1.0), EINVAL), (dict(scale=float("inf")), EINVAL),
     (dict(scale=float("nan")), EINVAL), (dict(clamp=float("nan")), EINVAL), (dict(lse=2), EINVAL),
     (dict(dtype=0, sn=66), EINVAL),
+    # bf16: one query tile's (min(k, N) + 256) key rows must span < 2 GiB
+    (dict(sn=1 << 22, sh=1 << 32, sb=1 << 33, k=32), EUNSUP),
+    (dict(N=1 << 16, k=1 << 16, sn=1 << 14, sh=1 << 30, sb=1 << 31), EUNSUP),
 ])
 def test_forward_rejects(lib, kw, code):
     assert fwd(lib, **kw) == code
