@@ -47,6 +47,9 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_forward_rows.argtypes = (
         [ctypes.c_int] * 6 + [vp, vp, vp, vp, i64, i64, i64, dbl, dbl, vp, i64, vp, vp, vp])
     lib.oracle_forward_rows.restype = None
+    lib.oracle_backward.argtypes = (
+        [ctypes.c_int] * 6 + [vp, vp, vp, vp, i64, i64, i64, dbl, dbl, vp, vp, vp, vp, vp])
+    lib.oracle_backward.restype = None
     lib.oracle_decode_step.argtypes = (
         [ctypes.c_int] * 6 + [vp, vp, vp, vp, vp, vp, vp, i64, i64, dbl, dbl, vp, vp])
     lib.oracle_decode_step.restype = ctypes.c_int
@@ -149,6 +152,29 @@ def forward(q, k_, v, gate, k: int, pi: int, scale: float | None = None,
     if want_probs:
         res.append(probs.reshape(out_shape[:-1] + (m,)))
     return res[0] if len(res) == 1 else tuple(res)
+
+
+def backward(q, k_, v, gate, k: int, pi: int, dout, scale: float | None = None,
+             clamp: float = 0.0, L=None):
+    """Oracle gradients for a loss L with dL/dy = ``dout`` [B,H,N,D].
+
+    Returns (dq, dk, dv) [B,H,N,D] and dgate [B,H,N] (dL/dg of the gate logit
+    as seen by each query; a per-head gate's gradient is the sum over its
+    queries), all float64.  See the backward block of pi_oracle.c's header.
+    """
+    L = L or lib()
+    q, k_, v, gate, dout = _f32(q), _f32(k_), _f32(v), _f32(gate), _f32(dout)
+    B, H, N, D = q.shape
+    assert k_.shape == q.shape and v.shape == q.shape and dout.shape == q.shape
+    gsb, gsh, gsn = _gate_strides(gate, B, H, N)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    dq, dk, dv = (np.empty((B, H, N, D), dtype=np.float64) for _ in range(3))
+    dg = np.empty((B, H, N), dtype=np.float64)
+    if B * H * N:
+        L.oracle_backward(B, H, N, D, k, pi, _ptr(q), _ptr(k_), _ptr(v), _ptr(gate), gsb, gsh, gsn,
+                          float(scale), float(clamp), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg))
+    return dq, dk, dv, dg
 
 
 def decode_step(len_in, q_new, k_new, v_new, k_cache, v_cache, gate, k: int, pi: int,

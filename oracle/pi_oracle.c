@@ -25,6 +25,17 @@
  *     App. B; not in the equations, off unless clamp > 0)
  *   - alpha^ = softmax(delta over U(t)), y_t = sum_j alpha^_j v_j    (eqs. alphahat_adapt, attn_adapt)
  *   - lse_t = log sum_j exp(delta_j)  (natural log, fused logits)
+ * Backward (gradient of a loss L with dL/dy given), from the same forward:
+ *   - dL/dalpha^_tj = <dL/dy_t, v_j>                                  (eq. attn_adapt)
+ *   - softmax Jacobian on the fused logits:
+ *       dL/ddelta_tj = alpha^_tj (dL/dalpha^_tj - sum_i alpha^_ti dL/dalpha^_ti)   (eq. jac)
+ *   - dL/dz_tj = dL/ddelta_tj where delta is not clamped, else 0; dz/dq and
+ *     dz/dk carry the factor scale                                    (eqs. z, delta_adapt)
+ *   - dL/dv_j = sum_t alpha^_tj dL/dy_t                               (eq. attn_adapt)
+ *   - gate: ddelta/dalpha~ = 1/alpha~ on local keys, -1/(1-alpha~) on
+ *     the partner (eq. ddelta_da, written for the clipped gate the forward
+ *     uses), dalpha~/dalpha = 1 - 2 eps, dalpha/dg = alpha (1 - alpha); the
+ *     clamp cuts these paths too                                      (eqs. ddelta_da, dalpha_da; Sec. 3.5)
  * Decode step (Sec. 3.5, online working set eq. online_ws): query at
  * position t = len[s] attends to cache rows W_t, where row t is the new
  * key/value, which the step first writes into the cache.
@@ -141,6 +152,74 @@ void oracle_forward_rows(int B, int H, int N, int D, int k, int pi,
         }
         free(slot);
         free(delta);
+    }
+}
+
+/* Backward over whole heads.  dout [B][H][N][D] is dL/dy.  Writes dq, dk,
+ * dv [B][H][N][D] and dgate [B][H][N] (dL/dg for the gate logit as seen by
+ * query t; a per-head gate's gradient is the sum over its queries).
+ * Every (b, h) is independent; within one, queries are visited in order. */
+void oracle_backward(int B, int H, int N, int D, int k, int pi,
+                     const float *q, const float *kk, const float *v,
+                     const float *gate, int64_t gsb, int64_t gsh, int64_t gsn,
+                     double scale, double clamp, const float *dout,
+                     double *dq, double *dk, double *dv, double *dgate)
+{
+    int m = oracle_ws_width(k, pi);
+#pragma omp parallel
+    {
+        int32_t *slot = (int32_t *)malloc(sizeof(int32_t) * (size_t)m);
+        double *delta = (double *)malloc(sizeof(double) * (size_t)m);
+        double *p = (double *)malloc(sizeof(double) * (size_t)m);
+        double *dp = (double *)malloc(sizeof(double) * (size_t)m);
+        double *y = (double *)malloc(sizeof(double) * (size_t)D);
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t bh = 0; bh < (int64_t)B * H; ++bh) {
+            int h = (int)(bh % H), b = (int)(bh / H);
+            const float *qb = q + bh * (int64_t)N * D, *kb = kk + bh * (int64_t)N * D;
+            const float *vb = v + bh * (int64_t)N * D, *ob = dout + bh * (int64_t)N * D;
+            double *dqb = dq + bh * (int64_t)N * D, *dkb = dk + bh * (int64_t)N * D;
+            double *dvb = dv + bh * (int64_t)N * D;
+            for (int64_t i = 0; i < (int64_t)N * D; ++i) dqb[i] = dkb[i] = dvb[i] = 0.0;
+            for (int t = 0; t < N; ++t) {
+                const float *qt = qb + (int64_t)t * D, *gt = ob + (int64_t)t * D;
+                working_set(t, N, k, pi, slot);
+                double g = gate[b * gsb + h * gsh + (int64_t)t * gsn];
+                attend(D, qt, kb, vb, slot, m, k, g, scale, clamp, delta, y, p);
+                /* dL/dalpha^ per slot and its weighted mean */
+                double mean = 0.0;
+                for (int s = 0; s < m; ++s) {
+                    dp[s] = 0.0;
+                    if (slot[s] < 0) continue;
+                    const float *vj = vb + (int64_t)slot[s] * D;
+                    for (int d = 0; d < D; ++d) dp[s] += (double)gt[d] * (double)vj[d];
+                    mean += p[s] * dp[s];
+                }
+                double a = 1.0 / (1.0 + exp(-g)), at = clipped_gate(g);
+                double dg_local = (1.0 - 2.0 * ORACLE_EPS) * a * (1.0 - a) / at;
+                double dg_skip = -(1.0 - 2.0 * ORACLE_EPS) * a * (1.0 - a) / (1.0 - at);
+                double dgt = 0.0;
+                for (int s = 0; s < m; ++s) {
+                    if (slot[s] < 0) continue;
+                    int j = slot[s];
+                    double dd = p[s] * (dp[s] - mean); /* dL/ddelta (eq. jac) */
+                    if (clamp > 0.0 && fabs(delta[s]) >= clamp) dd = 0.0;
+                    const float *kj = kb + (int64_t)j * D;
+                    for (int d = 0; d < D; ++d) {
+                        dqb[(int64_t)t * D + d] += scale * dd * (double)kj[d];
+                        dkb[(int64_t)j * D + d] += scale * dd * (double)qt[d];
+                        dvb[(int64_t)j * D + d] += p[s] * (double)gt[d];
+                    }
+                    dgt += dd * (s <= k ? dg_local : dg_skip);
+                }
+                dgate[bh * (int64_t)N + t] = dgt;
+            }
+        }
+        free(slot);
+        free(delta);
+        free(p);
+        free(dp);
+        free(y);
     }
 }
 

@@ -363,3 +363,102 @@ def pin_reachability(L):
 
 
 ALL_PINS.append(pin_reachability)
+
+
+# ---------------------------------------------------------------------------
+# backward pins
+# ---------------------------------------------------------------------------
+def _loss(L, q, k, v, gate, kk, pi, dout, clamp=0.0):
+    y = oracle.forward(q, k, v, gate, kk, pi, clamp=clamp, L=L)
+    return float(np.sum(y * np.asarray(dout, np.float64)))
+
+
+def _central_difference(L, arrays, which, idx, h, kk, pi, dout, clamp=0.0):
+    """d loss / d arrays[which][idx] by a central difference whose two steps
+    are the exact float32 increments actually applied (the oracle takes
+    float32 inputs)."""
+    x = arrays[which]
+    base = np.float32(x[idx])
+    up, dn = np.float32(base + np.float32(h)), np.float32(base - np.float32(h))
+    a, b = float(up) - float(base), float(base) - float(dn)
+    xs = [arr.copy() for arr in arrays]
+    xs[which][idx] = up
+    f_up = _loss(L, *xs, kk, pi, dout, clamp)
+    xs[which][idx] = dn
+    f_dn = _loss(L, *xs, kk, pi, dout, clamp)
+    return (f_up - f_dn) / (a + b)
+
+
+def pin_backward_finite_differences(L):
+    """The oracle gradients (Sec. 3.5 eqs. jac, ddelta_da, dalpha_da) equal
+    central differences of the oracle's own forward, for q, k, v and the gate
+    logit, with the partner inside and outside the window and with per-head
+    and per-query gates."""
+    rng = np.random.default_rng(11)
+    for (B, H, N, D, kk, pi, per_query) in [(1, 2, 24, 8, 4, 8, False), (2, 1, 20, 8, 3, 3, True),
+                                            (1, 1, 17, 16, 2, 5, True)]:
+        q, k, v = rand_qkv(rng, B, H, N, D)
+        gate = (rng.uniform(-1, 1, (B, H, N)) if per_query else rng.uniform(-1, 1, H)).astype(np.float32)
+        dout = rng.standard_normal((B, H, N, D)).astype(np.float32)
+        dq, dk, dv, dg = oracle.backward(q, k, v, gate, kk, pi, dout, L=L)
+        grads = [dq, dk, dv]
+        arrays = [q, k, v, gate]
+        for which in range(4):
+            for _ in range(6 if which < 3 else 4):
+                idx = tuple(int(rng.integers(0, n)) for n in arrays[which].shape)
+                fd = _central_difference(L, arrays, which, idx, 2.0 ** -8, kk, pi, dout)
+                if which < 3:
+                    an = grads[which][idx]
+                elif per_query:
+                    an = dg[idx]
+                else:  # a per-head gate collects the gradient of every query of head h
+                    an = dg[:, idx[0], :].sum()
+                assert abs(fd - an) <= 5e-5 + 1e-3 * abs(an), (B, H, N, D, kk, pi, which, idx, fd, an)
+
+
+def pin_backward_dense_reduction(L):
+    """With k >= N-1 and no partner the prior cancels and pi-Attention is dense
+    causal attention (Sec. 3.2): q, k, v gradients equal torch autograd of the
+    textbook softmax attention in fp64, and the gate gradient vanishes (the
+    softmax Jacobian's rows sum to zero, eq. jac)."""
+    import torch
+    rng = np.random.default_rng(5)
+    B, H, N, D = 2, 2, 19, 8
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    gate = rng.uniform(-2, 2, H).astype(np.float32)
+    dout = rng.standard_normal((B, H, N, D)).astype(np.float32)
+    scale = 1.0 / math.sqrt(D)
+    dq, dk, dv, dg = oracle.backward(q, k, v, gate, N - 1, 0, dout, L=L)
+    tq, tk, tv = (torch.tensor(x, dtype=torch.float64, requires_grad=True) for x in (q, k, v))
+    S = (tq @ tk.transpose(-1, -2)) * scale
+    S = S.masked_fill(~torch.tril(torch.ones(N, N, dtype=torch.bool)), float("-inf"))
+    y = torch.softmax(S, dim=-1) @ tv
+    y.backward(torch.tensor(dout, dtype=torch.float64))
+    for got, ref in ((dq, tq.grad), (dk, tk.grad), (dv, tv.grad)):
+        assert np.allclose(got, ref.numpy(), rtol=1e-10, atol=1e-12)
+    assert np.abs(dg).max() < 1e-12
+
+
+def pin_backward_clamp_limits(L):
+    """Logit clamp (App. B reading): a clamp that never binds changes no
+    gradient; a clamp that binds everywhere cuts every path through the
+    logits (dq = dk = 0, gate gradient 0) and leaves uniform weights, so dv_j
+    is the mean of dL/dy over the queries whose working set holds j."""
+    rng = np.random.default_rng(9)
+    B, H, N, D, kk, pi = 1, 2, 18, 8, 3, 7
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    gate = rng.uniform(-1, 1, H).astype(np.float32)
+    dout = rng.standard_normal((B, H, N, D)).astype(np.float32)
+    free = oracle.backward(q, k, v, gate, kk, pi, dout, L=L)
+    loose = oracle.backward(q, k, v, gate, kk, pi, dout, clamp=1e6, L=L)
+    for a, b in zip(free, loose):
+        assert np.array_equal(a, b)
+    dq, dk, dv, dg = oracle.backward(q, k, v, gate, kk, pi, dout, clamp=1e-7, L=L)
+    assert not dq.any() and not dk.any() and not dg.any()
+    M = scan_membership(N, kk, pi).astype(np.float64)           # [t, j]
+    W = M / M.sum(-1, keepdims=True)
+    ref = np.einsum("tj,bhtd->bhjd", W, np.asarray(dout, np.float64))
+    assert np.allclose(dv, ref, atol=1e-5)
+
+
+ALL_PINS += [pin_backward_finite_differences, pin_backward_dense_reduction, pin_backward_clamp_limits]

@@ -33,6 +33,24 @@ MUTANTS = {
     "softmax_unnormalised": [("if (slot[s] >= 0) Z += exp(delta[s] - mu);",
                               "if (slot[s] >= 0) Z += exp(delta[s]);")],
     "max_not_subtracted_in_lse": [("return mu + log(Z);", "return log(Z);")],
+    # backward
+    "bwd_softmax_mean_dropped": [("double dd = p[s] * (dp[s] - mean);", "double dd = p[s] * dp[s];")],
+    "bwd_dv_weighted_by_logit_grad": [("dvb[(int64_t)j * D + d] += p[s] * (double)gt[d];",
+                                       "dvb[(int64_t)j * D + d] += dd * (double)gt[d];")],
+    "bwd_dk_scale_dropped": [("dkb[(int64_t)j * D + d] += scale * dd * (double)qt[d];",
+                              "dkb[(int64_t)j * D + d] += dd * (double)qt[d];")],
+    "bwd_dq_from_query": [("dqb[(int64_t)t * D + d] += scale * dd * (double)kj[d];",
+                           "dqb[(int64_t)t * D + d] += scale * dd * (double)qt[d];")],
+    "bwd_dp_from_keys": [("const float *vj = vb + (int64_t)slot[s] * D;\n                    for (int d = 0; d < D; ++d) dp[s]",
+                          "const float *vj = kb + (int64_t)slot[s] * D;\n                    for (int d = 0; d < D; ++d) dp[s]")],
+    "bwd_gate_skip_sign": [("double dg_skip = -(1.0 - 2.0 * ORACLE_EPS)", "double dg_skip = (1.0 - 2.0 * ORACLE_EPS)")],
+    "bwd_gate_sigmoid_chain_dropped": [
+        ("double dg_local = (1.0 - 2.0 * ORACLE_EPS) * a * (1.0 - a) / at;",
+         "double dg_local = (1.0 - 2.0 * ORACLE_EPS) / at;"),
+        ("double dg_skip = -(1.0 - 2.0 * ORACLE_EPS) * a * (1.0 - a) / (1.0 - at);",
+         "double dg_skip = -(1.0 - 2.0 * ORACLE_EPS) / (1.0 - at);")],
+    "bwd_gate_priors_swapped": [("dgt += dd * (s <= k ? dg_local : dg_skip);", "dgt += dd * (s <= k ? dg_skip : dg_local);")],
+    "bwd_clamp_not_cut": [("if (clamp > 0.0 && fabs(delta[s]) >= clamp) dd = 0.0;", ";")],
 }
 
 
