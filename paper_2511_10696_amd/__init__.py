@@ -17,12 +17,12 @@ import math
 import os
 import threading
 
-__all__ = ["pi_attn_index_set", "pi_attn_forward", "pi_attn_decode_step", "pi_attn_ws_width",
+__all__ = ["pi_attn_index_set", "pi_attn_forward", "pi_attn_backward", "pi_attn_decode_step", "pi_attn_ws_width",
            "pi_attn_strerror", "library", "LIB_PATH", "EXPORTED_SYMBOLS", "PiAttnError"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpi_attn.so")
 EXPORTED_SYMBOLS = ("pi_attn_strerror", "pi_attn_ws_width", "pi_attn_index_set",
-                    "pi_attn_forward", "pi_attn_decode_step")
+                    "pi_attn_forward", "pi_attn_decode_step", "pi_attn_backward")
 
 PI_ATTN_F32, PI_ATTN_BF16 = 0, 1
 
@@ -57,6 +57,10 @@ def library() -> ctypes.CDLL:
             lib.pi_attn_decode_step.argtypes = ([i32] * 7 + [vp, vp, vp, vp, vp, vp, vp, vp, i64, i64,
                                                             f32, f32, vp, vp, vp])
             lib.pi_attn_decode_step.restype = ctypes.c_int
+            lib.pi_attn_backward.argtypes = ([i32] * 7 + [vp, vp, vp, i64, i64, i64, vp, i64, i64, i64,
+                                                         f32, f32, vp, vp, i64, i64, i64,
+                                                         vp, vp, vp, vp, vp, vp])
+            lib.pi_attn_backward.restype = ctypes.c_int
             _lib = lib
     return _lib
 
@@ -169,6 +173,56 @@ def pi_attn_forward(q, k, v, gate, k_window: int, pi: int, scale: float | None =
         _stream_handle(stream, q.device))
     _check(st, "pi_attn_forward")
     return (out, lse) if (return_lse or lse is not None) else out
+
+
+def pi_attn_backward(q, k, v, gate, k_window: int, pi: int, dout, lse, scale: float | None = None,
+                     logit_clamp: float = 0.0, gate_grad_per_query: bool = False, stream=None):
+    """Gradients of the causal pi-Attention forward for dL/dy = ``dout``.
+
+    q, k, v, gate, k_window, pi, scale and logit_clamp as passed to
+    pi_attn_forward; ``lse`` is the [B, H, N] float32 lse that forward call
+    returned; ``dout`` has q's shape and dtype.  Returns float32
+    (dq, dk, dv) [B, H, N, D] and dgate shaped like ``gate`` (summed over
+    b and t for a per-head gate), or [B, H, N] per query when
+    ``gate_grad_per_query``.
+    """
+    torch = _torch()
+    _require_cuda(q, k, v, gate, dout, lse)
+    if q.dim() != 4 or k.shape != q.shape or v.shape != q.shape or dout.shape != q.shape:
+        raise ValueError("q, k, v, dout must share one [B, H, N, D] shape")
+    if k.dtype != q.dtype or v.dtype != q.dtype or dout.dtype != q.dtype:
+        raise TypeError("q, k, v, dout must share one dtype")
+    if k.stride() != q.stride() or v.stride() != q.stride():
+        raise ValueError("q, k, v must share strides (use .contiguous())")
+    if q.stride(3) != 1 or dout.stride(3) != 1:
+        raise ValueError("the head dimension must be contiguous")
+    B, H, N, D = q.shape
+    if gate.dtype != torch.float32:
+        raise TypeError("gate logits must be float32")
+    if tuple(gate.shape) == (H,):
+        g = gate.view(1, H, 1).expand(B, H, N)
+    elif tuple(gate.shape) == (B, H, N):
+        g = gate
+    else:
+        raise ValueError(f"gate must be [H] or [B, H, N], got {tuple(gate.shape)}")
+    if lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, N) or not lse.is_contiguous():
+        raise ValueError("lse must be the contiguous float32 [B, H, N] lse of the forward")
+    f32 = dict(dtype=torch.float32, device=q.device)
+    dq, dk, dv = (torch.empty((B, H, N, D), **f32) for _ in range(3))
+    dg = torch.empty((B, H, N), **f32)
+    rowterm = torch.empty((B, H, N), **f32)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    st = library().pi_attn_backward(
+        _dtype_code(q.dtype), B, H, N, D, int(k_window), int(pi),
+        _ptr(q), _ptr(k), _ptr(v), q.stride(0), q.stride(1), q.stride(2),
+        _ptr(g), g.stride(0), g.stride(1), g.stride(2), float(scale), float(logit_clamp), _ptr(lse),
+        _ptr(dout), dout.stride(0), dout.stride(1), dout.stride(2),
+        _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg), _ptr(rowterm), _stream_handle(stream, q.device))
+    _check(st, "pi_attn_backward")
+    if tuple(gate.shape) == (H,) and not gate_grad_per_query:
+        dg = dg.sum(dim=(0, 2))
+    return dq, dk, dv, dg
 
 
 def pi_attn_decode_step(len_in, q_new, k_new, v_new, k_cache, v_cache, gate, k: int, pi: int,

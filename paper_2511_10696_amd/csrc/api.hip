@@ -88,6 +88,44 @@ int pi_attn_forward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, i
     return from_hip(dtype == PI_ATTN_BF16 ? launch_forward_bf16(p, st) : launch_forward_f32(p, st));
 }
 
+int pi_attn_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, int32_t k, int32_t pi,
+                     const void *q, const void *kk, const void *v, int64_t sb, int64_t sh, int64_t sn,
+                     const float *gate, int64_t gsb, int64_t gsh, int64_t gsn, float scale, float logit_clamp,
+                     const float *lse, const void *dout, int64_t osb, int64_t osh, int64_t osn, float *dq,
+                     float *dk, float *dv, float *dgate, float *rowterm, void *stream) {
+    const int es = elem_size(dtype);
+    if (es == 0) return PI_ATTN_EUNSUPPORTED;
+    if (B < 0 || H < 0 || N < 0 || k < 0 || pi < 0) return PI_ATTN_EINVAL;
+    if (D != 64 && D != 128) return PI_ATTN_EUNSUPPORTED;
+    if (!isfinite(scale) || scale <= 0.0f || isnan(logit_clamp)) return PI_ATTN_EINVAL;
+    const int64_t rows = (int64_t)B * H * N;
+    if (rows >= kMaxRows) return PI_ATTN_EINVAL;
+    if (rows == 0) return PI_ATTN_OK;
+    if (!q || !kk || !v || !gate || !lse || !dout || !dq || !dk || !dv || !dgate || !rowterm)
+        return PI_ATTN_EINVAL;
+    if (!aligned16(q) || !aligned16(kk) || !aligned16(v) || !aligned16(dout)) return PI_ATTN_EINVAL;
+    if (!stride16(sb, es) || !stride16(sh, es) || !stride16(sn, es)) return PI_ATTN_EINVAL;
+    if (!stride16(osb, es) || !stride16(osh, es) || !stride16(osn, es)) return PI_ATTN_EINVAL;
+    if (!aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
+    if (!aligned4(lse) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv) || !aligned4(dgate) ||
+        !aligned4(rowterm))
+        return PI_ATTN_EINVAL;
+
+    BwdParams p{};
+    FwdParams &f = p.f;
+    f.B = B; f.H = H; f.N = N; f.D = D; f.k = k; f.pi = pi;
+    f.q = q; f.k_ptr = kk; f.v = v;
+    f.sb = sb; f.sh = sh; f.sn = sn;
+    f.gate = gate; f.gsb = gsb; f.gsh = gsh; f.gsn = gsn;
+    f.scale = scale;
+    f.clamp = logit_clamp > 0.0f ? logit_clamp : 0.0f;
+    p.dtype = dtype == PI_ATTN_BF16 ? 1 : 0;
+    p.lse = lse;
+    p.dout = dout; p.osb = osb; p.osh = osh; p.osn = osn;
+    p.dq = dq; p.dk = dk; p.dv = dv; p.dgate = dgate; p.rowterm = rowterm;
+    return from_hip(launch_backward(p, (hipStream_t)stream));
+}
+
 int pi_attn_decode_step(int32_t dtype, int32_t S, int32_t H, int32_t D, int32_t cap, int32_t k, int32_t pi,
                         const int32_t *len_in, int32_t *len_out, const void *q_new, const void *k_new,
                         const void *v_new, void *k_cache, void *v_cache, const float *gate, int64_t gss,

@@ -1,0 +1,215 @@
+// backward.hip -- gradients of the full-sequence operator: one wavefront per
+// row, fp32 arithmetic for float32 and bf16 inputs.
+//
+// For a loss L with dL/dy given, the weights are recomputed from the
+// forward's lse as alpha^_tj = exp(delta_tj - lse_t), and
+//   dp_tj    = <dL/dy_t, v_j>                    (eq. attn_adapt)
+//   r_t      = sum_j alpha^_tj dp_tj
+//   ddelta_tj = alpha^_tj (dp_tj - r_t)          (softmax Jacobian, eq. jac)
+// with ddelta cut to 0 where the optional clamp saturates.  Then
+//   dq_t = scale sum_j ddelta_tj k_j,  dk_j = scale sum_t ddelta_tj q_t,
+//   dv_j = sum_t alpha^_tj dL/dy_t,
+//   dg_t = sum_j ddelta_tj d(log omega_tj)/dg    (eqs. ddelta_da, dalpha_da)
+// where d log alpha~/dg = (1 - 2 eps) a (1 - a) / alpha~ on the window and
+// d log(1 - alpha~)/dg = -(1 - 2 eps) a (1 - a) / (1 - alpha~) on the partner,
+// a = sigmoid(g).
+//
+// Query pass: wavefront per (b, h, t), lane l holding elements l, l+64, ...;
+// two sweeps over W_t (r_t first, then the gradients).  Key pass: wavefront
+// per (b, h, j) over the queries whose working set holds j: t in
+// [j, j + k] and, when pi > k, t = j + pi.  This is the correctness-first
+// path; every dot product is a wavefront reduction.
+#include "kernels.h"
+#include "pi_common.h"
+
+namespace pi_attn {
+
+namespace {
+
+__device__ inline float wave_sum(float x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+    return x;
+}
+
+template <typename T>
+__device__ inline float ld(const void *p, int64_t i) {
+    if constexpr (sizeof(T) == 4) {
+        return reinterpret_cast<const float *>(p)[i];
+    } else {
+        return (float)reinterpret_cast<const __bf16 *>(p)[i];
+    }
+}
+
+// Prior derivatives of one gate logit (natural-log units).
+struct GateGrad {
+    float local, partner;
+};
+
+__device__ inline GateGrad gate_grad(float g) {
+    const float a = 1.0f / (1.0f + __expf(-g));
+    const float at = kGateEps + (1.0f - 2.0f * kGateEps) * a;
+    const float c = (1.0f - 2.0f * kGateEps) * a * (1.0f - a);
+    return GateGrad{c / at, -c / (1.0f - at)};
+}
+
+// Fused logit of one (t, j) pair from its partial dot product; `bias` and
+// the clamp as in the forward.  Returns delta and sets `cut` when the clamp
+// saturates.
+__device__ inline float fused_logit(float dot, float scale, float bias, float clamp, bool &cut) {
+    float d = dot * scale + bias;
+    cut = false;
+    if (clamp > 0.0f) {
+        const float c = fminf(fmaxf(d, -clamp), clamp);
+        cut = fabsf(c) >= clamp;
+        d = c;
+    }
+    return d;
+}
+
+template <int D, typename T>
+__global__ __launch_bounds__(256) void backward_q_kernel(BwdParams p) {
+    constexpr int E = D / 64;
+    const FwdParams &f = p.f;
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= (int64_t)f.B * f.H * f.N) return;
+    const int t = (int)(row % f.N);
+    const int64_t bh = row / f.N;
+    const int h = (int)(bh % f.H), b = (int)(bh / f.H);
+    const int64_t base = b * f.sb + h * f.sh;
+    const int64_t obase = b * p.osb + h * p.osh + t * p.osn;
+
+    float q[E], go[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        q[e] = ld<T>(f.q, base + t * f.sn + lane + 64 * e);
+        go[e] = ld<T>(p.dout, obase + lane + 64 * e);
+    }
+    const bool exact = f.clamp > 0.0f;
+    const float g = f.gate[b * f.gsb + h * f.gsh + t * f.gsn];
+    const FusionBias fb = fusion_bias(g, exact);
+    const GateGrad gg = gate_grad(g);
+    const float shift = fb.lse_shift - p.lse[row];   // alpha^ = exp(delta + shift)
+    const int jp = partner_of(t, f.k, f.pi);
+    const int lo = window_lo(t, f.k);
+
+    // (weight, dp) of one working-set entry
+    auto entry = [&](int j, float bias, float &w, float &dp, bool &cut) {
+        float pk = 0.0f, pv = 0.0f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            pk += q[e] * ld<T>(f.k_ptr, base + j * f.sn + lane + 64 * e);
+            pv += go[e] * ld<T>(f.v, base + j * f.sn + lane + 64 * e);
+        }
+        const float delta = fused_logit(wave_sum(pk), f.scale, bias, f.clamp, cut);
+        w = __expf(delta + shift);
+        dp = wave_sum(pv);
+    };
+
+    float r = 0.0f;
+    bool cut;
+    float w, dp;
+    if (jp >= 0) {
+        entry(jp, fb.partner, w, dp, cut);
+        r += w * dp;
+    }
+    for (int j = lo; j <= t; ++j) {
+        entry(j, fb.local, w, dp, cut);
+        r += w * dp;
+    }
+
+    float dq[E] = {};
+    float dg = 0.0f;
+    auto grad = [&](int j, float bias, float dlogw) {
+        entry(j, bias, w, dp, cut);
+        const float dd = cut ? 0.0f : w * (dp - r);
+#pragma unroll
+        for (int e = 0; e < E; ++e) dq[e] += dd * ld<T>(f.k_ptr, base + j * f.sn + lane + 64 * e);
+        dg += dd * dlogw;
+    };
+    if (jp >= 0) grad(jp, fb.partner, gg.partner);
+    for (int j = lo; j <= t; ++j) grad(j, fb.local, gg.local);
+
+#pragma unroll
+    for (int e = 0; e < E; ++e) p.dq[row * D + lane + 64 * e] = dq[e] * f.scale;
+    if (lane == 0) {
+        p.dgate[row] = dg;
+        p.rowterm[row] = r;
+    }
+}
+
+template <int D, typename T>
+__global__ __launch_bounds__(256) void backward_kv_kernel(BwdParams p) {
+    constexpr int E = D / 64;
+    const FwdParams &f = p.f;
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= (int64_t)f.B * f.H * f.N) return;
+    const int j = (int)(row % f.N);
+    const int64_t bh = row / f.N;
+    const int h = (int)(bh % f.H), b = (int)(bh / f.H);
+    const int64_t base = b * f.sb + h * f.sh;
+    const int64_t rbase = bh * f.N;   // row index of (b, h, 0)
+
+    float kj[E], vj[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        kj[e] = ld<T>(f.k_ptr, base + j * f.sn + lane + 64 * e);
+        vj[e] = ld<T>(f.v, base + j * f.sn + lane + 64 * e);
+    }
+    const bool exact = f.clamp > 0.0f;
+    float dk[E] = {}, dv[E] = {};
+
+    // Query t sees key j as a window entry (partner == false) or as its partner.
+    auto visit = [&](int t, bool partner) {
+        const FusionBias fb = fusion_bias(f.gate[b * f.gsb + h * f.gsh + t * f.gsn], exact);
+        const int64_t ob = b * p.osb + h * p.osh + t * p.osn;
+        float q[E], go[E], pk = 0.0f, pv = 0.0f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            q[e] = ld<T>(f.q, base + t * f.sn + lane + 64 * e);
+            go[e] = ld<T>(p.dout, ob + lane + 64 * e);
+            pk += q[e] * kj[e];
+            pv += go[e] * vj[e];
+        }
+        bool cut;
+        const float delta = fused_logit(wave_sum(pk), f.scale, partner ? fb.partner : fb.local, f.clamp, cut);
+        const float w = __expf(delta + fb.lse_shift - p.lse[rbase + t]);
+        const float dp = wave_sum(pv);
+        const float dd = cut ? 0.0f : w * (dp - p.rowterm[rbase + t]);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            dk[e] += dd * q[e];
+            dv[e] += w * go[e];
+        }
+    };
+    const int t_hi = min(j + f.k, f.N - 1);
+    for (int t = j; t <= t_hi; ++t) visit(t, false);
+    if (partner_enabled(f.k, f.pi) && (int64_t)j + f.pi < f.N) visit(j + f.pi, true);
+
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        p.dk[row * D + lane + 64 * e] = dk[e] * f.scale;
+        p.dv[row * D + lane + 64 * e] = dv[e];
+    }
+}
+
+template <int D, typename T>
+hipError_t launch(const BwdParams &p, hipStream_t stream) {
+    const int64_t rows = (int64_t)p.f.B * p.f.H * p.f.N;
+    const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
+    hipError_t e = launch_kernel(backward_q_kernel<D, T>, grid, block, stream, p);
+    if (e != hipSuccess) return e;
+    return launch_kernel(backward_kv_kernel<D, T>, grid, block, stream, p);
+}
+
+}  // namespace
+
+hipError_t launch_backward(const BwdParams &p, hipStream_t stream) {
+    if ((int64_t)p.f.B * p.f.H * p.f.N == 0) return hipSuccess;
+    if (p.dtype == 1) return p.f.D == 64 ? launch<64, __bf16>(p, stream) : launch<128, __bf16>(p, stream);
+    return p.f.D == 64 ? launch<64, float>(p, stream) : launch<128, float>(p, stream);
+}
+
+}  // namespace pi_attn

@@ -44,6 +44,16 @@ struct DecodeParams {
     float *lse;                     // [S][H] or nullptr
 };
 
+struct BwdParams {
+    FwdParams f;                    // inputs as for the forward (out/lse unused)
+    int dtype;                      // 0 = float32, 1 = bf16 (q, k, v, dout)
+    const float *lse;               // [B][H][N]
+    const void *dout;
+    int64_t osb, osh, osn;          // element strides of dout
+    float *dq, *dk, *dv;            // [B][H][N][D] contiguous
+    float *dgate, *rowterm;         // [B][H][N] contiguous
+};
+
 hipError_t launch_index_set(int n, int k, int pi, int32_t *idx, hipStream_t stream);
 
 // Reference-style fp32 kernels: one wavefront per query, W_t visited entry by
@@ -56,5 +66,9 @@ hipError_t launch_forward_bf16(const FwdParams &p, hipStream_t stream);
 
 // bf16 decode step, working set split across wavefronts (D = 64 or 128).
 hipError_t launch_decode_bf16(const DecodeParams &p, hipStream_t stream);
+
+// Backward: a query pass (dq, dgate, rowterm) then a key pass (dk, dv),
+// one wavefront per row, fp32 arithmetic for both input dtypes.
+hipError_t launch_backward(const BwdParams &p, hipStream_t stream);
 
 }  // namespace pi_attn

@@ -100,6 +100,13 @@ def forward_inputs(cfg: ForwardConfig, seed: int = 0, device="cuda", per_query_g
     return out[0], out[1], out[2], gate
 
 
+def cotangent(shape, dtype, seed: int = 0, device="cuda"):
+    """Seeded dL/dy for the backward: N(0, 1) in ``dtype`` (its own stream,
+    seed offset so it never repeats the q/k/v draws of the same seed)."""
+    g = _gen(device, seed + 1000003)
+    return torch.randn(tuple(shape), generator=g, device=device, dtype=torch.float32).to(dtype)
+
+
 def decode_state(cfg: DecodeConfig, seed: int = 0, device="cuda"):
     """Caches [S, H, cap, D] with rows [0, cache_len) ~ N(0,1) and the rest
     zero, the int32 lengths [S] (= cache_len), and per-head gate logits."""
