@@ -7,7 +7,8 @@ H=32, N=32768, D=128, k=512, pi=1024, bf16 q/k/v ~ N(0,1), per-head gate
 logits ~ U(-1,1).  One step = one pi_attn_forward over the whole sequence.
 Also timed in the same run: the KV-cached decode step (64 sequences, 32
 heads, 32768 cached rows, k=512, pi=1024, 1000 consecutive steps), and the
-fp64 CPU oracle on a bounded sample of the forward workload.
+fp64 CPU oracle on a bounded sample of the forward workload, and the
+backward (pi_attn_backward) on the forward workload with a seeded dL/dy.
 
 Prints ONE JSON line.  value = query positions per second (B*N per step) of
 the forward, inputs resident in HBM.
@@ -26,6 +27,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
+VALU_F32_PEAK_TFLOPS = 157.3    # MI355X fp32 vector ALU, TFLOP/s
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "forward_bf16_fwd32k_hbm_traffic.txt")
 DECODE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_bf16_s64_hbm_traffic.txt")
 COPY_PROBE_BYTES = 1 << 30      # plain device copy used to calibrate the HBM byte counters
@@ -38,6 +40,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--decode-steps", type=int, default=1000)
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--backward-steps", type=int, default=3)
+    ap.add_argument("--no-backward", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pmc-probe", action="store_true",
                     help="run 3 forward launches, 3 decode steps and 3 plain 1 GiB device copies, "
@@ -60,6 +64,17 @@ def forward_algorithmic(cfg):
     es = 2
     nbytes = 4 * cfg.B * cfg.H * cfg.N * cfg.D * es
     return keys, flops, nbytes
+
+
+def backward_algorithmic(cfg):
+    """Algorithmic work of one backward: per attended key 10*D FLOPs (the
+    scores recomputed, dP = dO V^T, dV, dQ and dK: five D-long products,
+    2 FLOP per MAC); bytes: q, k, v, dO read once (input dtype), lse read,
+    dq, dk, dv (float32) and the per-query gate gradient written."""
+    keys, _, _ = forward_algorithmic(cfg)
+    rows = cfg.B * cfg.H * cfg.N
+    nbytes = rows * (4 * cfg.D * 2 + 3 * cfg.D * 4 + 4 + 4)
+    return keys, 10 * cfg.D * keys, nbytes
 
 
 def decode_algorithmic(cfg, t):
@@ -223,6 +238,10 @@ def main():
         del kc, vc, qs, ks, vs
         torch.cuda.empty_cache()
 
+    backward = None
+    if not args.no_backward:
+        backward = bench_backward(cfg, W, pa, torch, dev, stream, args.backward_steps)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(cfg, W)
@@ -243,10 +262,38 @@ def main():
         "roofline": roofline,
         "roofline_mfma": roofline_mfma,
         "decode": decode,
+        "backward": backward,
         "cpu_baseline": cpu,
         "wall_s_timed": round(t_wall, 3),
     }
     print(json.dumps(rec))
+
+
+def bench_backward(cfg, W, pa, torch, dev, stream, steps):
+    """pi_attn_backward on the forward workload (lse from one forward call,
+    a seeded dL/dy); inputs resident, one warm-up call, then ``steps``."""
+    q, k, v, gate = W.forward_inputs(cfg, 0, dev)
+    out, lse = pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi, return_lse=True)
+    dout = W.cotangent(q.shape, q.dtype, 0, dev)
+    pa.pi_attn_backward(q, k, v, gate, cfg.k, cfg.pi, out, lse, dout)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        pa.pi_attn_backward(q, k, v, gate, cfg.k, cfg.pi, out, lse, dout)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    keys, flops, nbytes = backward_algorithmic(cfg)
+    tflops = flops / (ms / 1e3) / 1e12
+    del q, k, v, out, dout, lse
+    torch.cuda.empty_cache()
+    return {"workload": "backward of fwd32k: B1 H32 N32768 D128 k512 pi1024 bf16 in, fp32 gradients",
+            "steps": steps, "ms_per_step": round(ms, 4),
+            "roofline": {"bound": "alu", "kernel": "backward_q_kernel<128> + backward_kv_kernel<128>",
+                         "achieved": round(tflops, 3), "peak": VALU_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(tflops / VALU_F32_PEAK_TFLOPS, 5), "flops_per_step": flops,
+                         "bytes_per_step": nbytes, "traffic": None}}
 
 
 def cpu_baseline(cfg, W):

@@ -144,24 +144,28 @@ int pi_attn_decode_step(int32_t dtype, int32_t S, int32_t H, int32_t D, int32_t 
  *   lse          device float32 [B][H][N] contiguous: the lse that
  *                pi_attn_forward wrote for these inputs (the weights are
  *                recomputed as exp(delta - lse)).
+ *   out          device y [B][H][N][D] in dtype: the output that
+ *                pi_attn_forward wrote for these inputs, through the same
+ *                strides as dout.
  *   dout         device dL/dy [B][H][N][D] in dtype through (osb, osh, osn).
  *   dq, dk, dv   device float32 [B][H][N][D] contiguous, overwritten.
  *   dgate        device float32 [B][H][N] contiguous, overwritten: dL/dg of
  *                the gate logit as seen by query t (a per-head gate's
  *                gradient is the sum of its entries over b and t).
  *   rowterm      device float32 [B][H][N] contiguous scratch owned by the
- *                caller: receives sum_j alpha^_tj dL/dalpha^_tj per query.
- * Two kernels on the stream, in order: a query pass (dq, dgate, rowterm)
+ *                caller: receives r_t = <dL/dy_t, y_t>, which equals
+ *                sum_j alpha^_tj dL/dalpha^_tj (y_t = sum_j alpha^_tj v_j).
+ * Kernels on the stream, in order: the row terms, a query pass (dq, dgate)
  * and a key pass (dk, dv).  Nothing is allocated; buffers must not overlap.
  * Errors: as pi_attn_forward, plus EINVAL for a null or misaligned lse,
- * dout, dq, dk, dv, dgate or rowterm.
+ * out, dout, dq, dk, dv, dgate or rowterm.
  */
 int pi_attn_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D,
                      int32_t k, int32_t pi,
                      const void *q, const void *kk, const void *v,
                      int64_t sb, int64_t sh, int64_t sn,
                      const float *gate, int64_t gsb, int64_t gsh, int64_t gsn,
-                     float scale, float logit_clamp, const float *lse,
+                     float scale, float logit_clamp, const float *lse, const void *out,
                      const void *dout, int64_t osb, int64_t osh, int64_t osn,
                      float *dq, float *dk, float *dv, float *dgate, float *rowterm,
                      void *stream);

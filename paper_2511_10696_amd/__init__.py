@@ -58,7 +58,7 @@ def library() -> ctypes.CDLL:
                                                             f32, f32, vp, vp, vp])
             lib.pi_attn_decode_step.restype = ctypes.c_int
             lib.pi_attn_backward.argtypes = ([i32] * 7 + [vp, vp, vp, i64, i64, i64, vp, i64, i64, i64,
-                                                         f32, f32, vp, vp, i64, i64, i64,
+                                                         f32, f32, vp, vp, vp, i64, i64, i64,
                                                          vp, vp, vp, vp, vp, vp])
             lib.pi_attn_backward.restype = ctypes.c_int
             _lib = lib
@@ -175,23 +175,28 @@ def pi_attn_forward(q, k, v, gate, k_window: int, pi: int, scale: float | None =
     return (out, lse) if (return_lse or lse is not None) else out
 
 
-def pi_attn_backward(q, k, v, gate, k_window: int, pi: int, dout, lse, scale: float | None = None,
+def pi_attn_backward(q, k, v, gate, k_window: int, pi: int, out, lse, dout, scale: float | None = None,
                      logit_clamp: float = 0.0, gate_grad_per_query: bool = False, stream=None):
     """Gradients of the causal pi-Attention forward for dL/dy = ``dout``.
 
     q, k, v, gate, k_window, pi, scale and logit_clamp as passed to
-    pi_attn_forward; ``lse`` is the [B, H, N] float32 lse that forward call
-    returned; ``dout`` has q's shape and dtype.  Returns float32
+    pi_attn_forward; ``out`` and ``lse`` are what that forward call returned
+    ([B, H, N, D] in q's dtype, [B, H, N] float32); ``dout`` has out's shape,
+    dtype and strides.  Returns float32
     (dq, dk, dv) [B, H, N, D] and dgate shaped like ``gate`` (summed over
     b and t for a per-head gate), or [B, H, N] per query when
     ``gate_grad_per_query``.
     """
     torch = _torch()
-    _require_cuda(q, k, v, gate, dout, lse)
-    if q.dim() != 4 or k.shape != q.shape or v.shape != q.shape or dout.shape != q.shape:
-        raise ValueError("q, k, v, dout must share one [B, H, N, D] shape")
-    if k.dtype != q.dtype or v.dtype != q.dtype or dout.dtype != q.dtype:
-        raise TypeError("q, k, v, dout must share one dtype")
+    _require_cuda(q, k, v, gate, out, dout, lse)
+    if (q.dim() != 4 or k.shape != q.shape or v.shape != q.shape or dout.shape != q.shape
+            or out.shape != q.shape):
+        raise ValueError("q, k, v, out, dout must share one [B, H, N, D] shape")
+    if k.dtype != q.dtype or v.dtype != q.dtype or dout.dtype != q.dtype or out.dtype != q.dtype:
+        raise TypeError("q, k, v, out, dout must share one dtype")
+    if out.stride() != dout.stride():
+        dout = dout.contiguous()
+        out = out.contiguous()
     if k.stride() != q.stride() or v.stride() != q.stride():
         raise ValueError("q, k, v must share strides (use .contiguous())")
     if q.stride(3) != 1 or dout.stride(3) != 1:
@@ -217,7 +222,7 @@ def pi_attn_backward(q, k, v, gate, k_window: int, pi: int, dout, lse, scale: fl
         _dtype_code(q.dtype), B, H, N, D, int(k_window), int(pi),
         _ptr(q), _ptr(k), _ptr(v), q.stride(0), q.stride(1), q.stride(2),
         _ptr(g), g.stride(0), g.stride(1), g.stride(2), float(scale), float(logit_clamp), _ptr(lse),
-        _ptr(dout), dout.stride(0), dout.stride(1), dout.stride(2),
+        _ptr(out), _ptr(dout), dout.stride(0), dout.stride(1), dout.stride(2),
         _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg), _ptr(rowterm), _stream_handle(stream, q.device))
     _check(st, "pi_attn_backward")
     if tuple(gate.shape) == (H,) and not gate_grad_per_query:

@@ -91,7 +91,8 @@ int pi_attn_forward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, i
 int pi_attn_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, int32_t k, int32_t pi,
                      const void *q, const void *kk, const void *v, int64_t sb, int64_t sh, int64_t sn,
                      const float *gate, int64_t gsb, int64_t gsh, int64_t gsn, float scale, float logit_clamp,
-                     const float *lse, const void *dout, int64_t osb, int64_t osh, int64_t osn, float *dq,
+                     const float *lse, const void *out, const void *dout, int64_t osb, int64_t osh,
+                     int64_t osn, float *dq,
                      float *dk, float *dv, float *dgate, float *rowterm, void *stream) {
     const int es = elem_size(dtype);
     if (es == 0) return PI_ATTN_EUNSUPPORTED;
@@ -101,12 +102,15 @@ int pi_attn_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, 
     const int64_t rows = (int64_t)B * H * N;
     if (rows >= kMaxRows) return PI_ATTN_EINVAL;
     if (rows == 0) return PI_ATTN_OK;
-    if (!q || !kk || !v || !gate || !lse || !dout || !dq || !dk || !dv || !dgate || !rowterm)
+    if (!q || !kk || !v || !gate || !lse || !out || !dout || !dq || !dk || !dv || !dgate || !rowterm)
         return PI_ATTN_EINVAL;
-    if (!aligned16(q) || !aligned16(kk) || !aligned16(v) || !aligned16(dout)) return PI_ATTN_EINVAL;
+    if (!aligned16(q) || !aligned16(kk) || !aligned16(v) || !aligned16(dout) || !aligned16(out))
+        return PI_ATTN_EINVAL;
     if (!stride16(sb, es) || !stride16(sh, es) || !stride16(sn, es)) return PI_ATTN_EINVAL;
     if (!stride16(osb, es) || !stride16(osh, es) || !stride16(osn, es)) return PI_ATTN_EINVAL;
     if (!aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
+    if (dtype == PI_ATTN_BF16 && ((int64_t)std::min(k, N) + 256) * sn * es >= ((int64_t)1 << 31))
+        return PI_ATTN_EUNSUPPORTED;
     if (!aligned4(lse) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv) || !aligned4(dgate) ||
         !aligned4(rowterm))
         return PI_ATTN_EINVAL;
@@ -121,7 +125,7 @@ int pi_attn_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, 
     f.clamp = logit_clamp > 0.0f ? logit_clamp : 0.0f;
     p.dtype = dtype == PI_ATTN_BF16 ? 1 : 0;
     p.lse = lse;
-    p.dout = dout; p.osb = osb; p.osh = osh; p.osn = osn;
+    p.out = out; p.dout = dout; p.osb = osb; p.osh = osh; p.osn = osn;
     p.dq = dq; p.dk = dk; p.dv = dv; p.dgate = dgate; p.rowterm = rowterm;
     return from_hip(launch_backward(p, (hipStream_t)stream));
 }

@@ -4,7 +4,7 @@
 // For a loss L with dL/dy given, the weights are recomputed from the
 // forward's lse as alpha^_tj = exp(delta_tj - lse_t), and
 //   dp_tj    = <dL/dy_t, v_j>                    (eq. attn_adapt)
-//   r_t      = sum_j alpha^_tj dp_tj
+//   r_t      = sum_j alpha^_tj dp_tj = <dL/dy_t, y_t>
 //   ddelta_tj = alpha^_tj (dp_tj - r_t)          (softmax Jacobian, eq. jac)
 // with ddelta cut to 0 where the optional clamp saturates.  Then
 //   dq_t = scale sum_j ddelta_tj k_j,  dk_j = scale sum_t ddelta_tj q_t,
@@ -14,11 +14,12 @@
 // d log(1 - alpha~)/dg = -(1 - 2 eps) a (1 - a) / (1 - alpha~) on the partner,
 // a = sigmoid(g).
 //
-// Query pass: wavefront per (b, h, t), lane l holding elements l, l+64, ...;
-// two sweeps over W_t (r_t first, then the gradients).  Key pass: wavefront
-// per (b, h, j) over the queries whose working set holds j: t in
-// [j, j + k] and, when pi > k, t = j + pi.  This is the correctness-first
-// path; every dot product is a wavefront reduction.
+// Row terms: r_t from the forward output y (a wavefront per row).  Query
+// pass: wavefront per (b, h, t), lane l holding elements l, l+64, ..., one
+// sweep over W_t.  Key pass: wavefront per (b, h, j) over the queries whose
+// working set holds j: t in [j, j + k] and, when pi > k, t = j + pi.  These
+// are the float32 kernels (every dot product a wavefront reduction); for
+// bf16 inputs the query pass is the MFMA kernel of backward_bf16.hip.
 #include "kernels.h"
 #include "pi_common.h"
 
@@ -68,6 +69,23 @@ __device__ inline float fused_logit(float dot, float scale, float bias, float cl
 }
 
 template <int D, typename T>
+__global__ __launch_bounds__(256) void rowterm_kernel(BwdParams p) {
+    const FwdParams &f = p.f;
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= (int64_t)f.B * f.H * f.N) return;
+    const int t = (int)(row % f.N);
+    const int64_t bh = row / f.N;
+    const int h = (int)(bh % f.H), b = (int)(bh / f.H);
+    const int64_t ob = b * p.osb + h * p.osh + t * p.osn;
+    float part = 0.0f;
+#pragma unroll
+    for (int e = 0; e < D / 64; ++e) part += ld<T>(p.dout, ob + lane + 64 * e) * ld<T>(p.out, ob + lane + 64 * e);
+    part = wave_sum(part);
+    if (lane == 0) p.rowterm[row] = part;
+}
+
+template <int D, typename T>
 __global__ __launch_bounds__(256) void backward_q_kernel(BwdParams p) {
     constexpr int E = D / 64;
     const FwdParams &f = p.f;
@@ -107,17 +125,9 @@ __global__ __launch_bounds__(256) void backward_q_kernel(BwdParams p) {
         dp = wave_sum(pv);
     };
 
-    float r = 0.0f;
+    const float r = p.rowterm[row];
     bool cut;
     float w, dp;
-    if (jp >= 0) {
-        entry(jp, fb.partner, w, dp, cut);
-        r += w * dp;
-    }
-    for (int j = lo; j <= t; ++j) {
-        entry(j, fb.local, w, dp, cut);
-        r += w * dp;
-    }
 
     float dq[E] = {};
     float dg = 0.0f;
@@ -133,10 +143,7 @@ __global__ __launch_bounds__(256) void backward_q_kernel(BwdParams p) {
 
 #pragma unroll
     for (int e = 0; e < E; ++e) p.dq[row * D + lane + 64 * e] = dq[e] * f.scale;
-    if (lane == 0) {
-        p.dgate[row] = dg;
-        p.rowterm[row] = r;
-    }
+    if (lane == 0) p.dgate[row] = dg;
 }
 
 template <int D, typename T>
@@ -199,7 +206,13 @@ template <int D, typename T>
 hipError_t launch(const BwdParams &p, hipStream_t stream) {
     const int64_t rows = (int64_t)p.f.B * p.f.H * p.f.N;
     const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
-    hipError_t e = launch_kernel(backward_q_kernel<D, T>, grid, block, stream, p);
+    hipError_t e = launch_kernel(rowterm_kernel<D, T>, grid, block, stream, p);
+    if (e != hipSuccess) return e;
+    if constexpr (sizeof(T) == 2) {
+        e = launch_backward_q_bf16(p, stream);
+    } else {
+        e = launch_kernel(backward_q_kernel<D, T>, grid, block, stream, p);
+    }
     if (e != hipSuccess) return e;
     return launch_kernel(backward_kv_kernel<D, T>, grid, block, stream, p);
 }

@@ -1,0 +1,375 @@
+// backward_bf16.hip -- MFMA query pass of the backward for bf16 inputs:
+// dq and the per-query gate gradient (D = 64 or 128), fp32 accumulation.
+//
+// Same decomposition and operand layouts as the bf16 forward: a work-group
+// of 4 wavefronts owns 128 queries of one (b, h), wavefront w the 32 queries
+// q0 = t0 + 32w + [0, 32); the window keys stream through LDS in 64-row
+// tiles.  Per 32-key block, on v_mfma_f32_32x32x16_bf16:
+//   S^T  = K Q^T        A = K rows (LDS), B = Q^T (registers)
+//   dP^T = V dO^T       A = V rows (LDS), B = dO^T (registers)
+// which land in the same accumulator layout (lane l: query l%32, keys
+// 8i + 4(l/32) + j at slot 4i + j).  The weights come back from the
+// forward's lse, alpha^ = exp(delta - lse), and
+//   dS^T = alpha^ (dP^T - r_t)     (softmax Jacobian, Sec. 3.5 eq. jac)
+// with r_t = <dL/dy_t, y_t> precomputed; dS^T, rounded to bf16, is the B
+// operand of
+//   dQ^T += K^T dS^T    A = K^T by LDS transpose reads of the key tile
+// with the key order permuted inside each 16-key chunk exactly as the
+// forward permutes V^T against P^T.  The gate gradient
+// sum_j dS_tj d(log omega_tj)/dg (eqs. ddelta_da, dalpha_da) nearly cancels
+// between window and partner, so it is formed at the end from the exact
+// row term r* = sum_j alpha^_tj dP_tj accumulated along the way (the r_t
+// used for dS comes from the bf16-rounded forward output): with
+// A = sum alpha^ dP and B = sum alpha^ over the unclamped entries of each
+// prior, dg = sum_prior d(log omega)/dg (A - r* B).  The partner
+// row (Sec. 3.4, eq. Npi) is the diagonal of one 32x32 block per product,
+// read straight from global memory as in the forward.
+//
+// LDS rows are padded (2D + 16 bytes): the row reads are free of bank
+// conflicts and the transpose reads of the key tile cost at most two ways.
+// Tiles are staged through range-checked buffer loads that zero-fill rows
+// past the query tile's last usable row.
+#include "kernels.h"
+#include "pi_common.h"
+
+namespace pi_attn {
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+constexpr int WAVES = 4;
+constexpr int NT = 64 * WAVES;
+constexpr int BM = 32 * WAVES;
+constexpr int TK = 64;
+constexpr int BPT = TK / 32;
+
+template <int D>
+struct Tile {
+    static constexpr int CPR = D / 8;        // 16-byte chunks per row
+    static constexpr int ROW = 2 * D + 16;   // padded LDS row stride (bytes)
+    static constexpr int BYTES = TK * ROW;
+    static constexpr int KS = D / 16;        // k-steps of the score products
+    static constexpr int DB = D / 32;        // 32-dim output blocks
+};
+
+template <int D>
+struct TileBuf {
+    alignas(16) unsigned char k[Tile<D>::BYTES];
+    alignas(16) unsigned char v[Tile<D>::BYTES];
+};
+
+template <int D>
+struct Stage {
+    static constexpr int CH = TK * Tile<D>::CPR / NT / BPT;
+    uint4 k[CH];
+    uint4 v[CH];
+};
+
+// Half hf of the tile `row0` rows past the window start (descriptors begin
+// at the window start and end at its last usable row: later rows read 0).
+template <int D>
+__device__ inline void tile_load(Stage<D> &st, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv, int rowb,
+                                 int row0, int hf, int tid) {
+#pragma unroll
+    for (int u = 0; u < Stage<D>::CH; ++u) {
+        const int cid = tid + NT * (hf * Stage<D>::CH + u);
+        const int row = cid / Tile<D>::CPR, pc = cid % Tile<D>::CPR;
+        const int off = row * rowb + pc * 16;
+        st.k[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, row0 * rowb, 0));
+        st.v[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, off, row0 * rowb, 0));
+    }
+}
+
+template <int D>
+__device__ inline void tile_store(const Stage<D> &st, TileBuf<D> &tb, int hf, int tid) {
+#pragma unroll
+    for (int u = 0; u < Stage<D>::CH; ++u) {
+        const int cid = tid + NT * (hf * Stage<D>::CH + u);
+        const int row = cid / Tile<D>::CPR, pc = cid % Tile<D>::CPR;
+        *reinterpret_cast<uint4 *>(tb.k + row * Tile<D>::ROW + pc * 16) = st.k[u];
+        *reinterpret_cast<uint4 *>(tb.v + row * Tile<D>::ROW + pc * 16) = st.v[u];
+    }
+}
+
+__device__ inline float other_half(float x) {
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(__lane_id() < 32 ? p[1] : p[0]);
+}
+
+// Diagonal (row c, column c) of a 32x32 accumulator block, for lane (c, g).
+__device__ inline float diagonal(const f32x16 &acc, int c, int g) {
+    const int slot = 4 * (c >> 3) + (c & 3);
+    float mine = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) mine = (e == slot) ? acc[e] : mine;
+    const float theirs = other_half(mine);
+    return (g == ((c >> 2) & 1)) ? mine : theirs;
+}
+
+// Row fragments (A operand, row l%32, dims 16s + 8(l/32)) of 32-row block
+// `blk` of a tile array.
+template <int D>
+__device__ inline void read_rows(bf16x8 f[Tile<D>::KS], const unsigned char *tile, int blk, int c, int g) {
+    const unsigned char *base = tile + (32 * blk + c) * Tile<D>::ROW + 16 * g;
+#pragma unroll
+    for (int s = 0; s < Tile<D>::KS; ++s) f[s] = *reinterpret_cast<const bf16x8 *>(base + 32 * s);
+}
+
+// Transposed fragments (A operand: dim 32db + l%32, keys 16cc + {4g..4g+3,
+// 8+4g..8+4g+3}) of 32-row block `blk` by LDS transpose reads.
+template <int D>
+__device__ inline void read_cols(bf16x8 f[2][Tile<D>::DB], const unsigned char *tile, int blk, int lane) {
+    const int g = lane >> 5, G = lane >> 4, r = (lane >> 2) & 3, qd = lane & 3;
+    const unsigned char *base =
+        tile + (32 * blk + 4 * g + r) * Tile<D>::ROW + (2 * (G & 1) + (qd >> 1)) * 16 + (qd & 1) * 8;
+#pragma unroll
+    for (int cc = 0; cc < 2; ++cc) {
+#pragma unroll
+        for (int db = 0; db < Tile<D>::DB; ++db) {
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+                const unsigned char *src = base + (16 * cc + 8 * hh) * Tile<D>::ROW + 64 * db;
+                const bf16x4 y = __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)src));
+                f[cc][db][4 * hh + 0] = y[0];
+                f[cc][db][4 * hh + 1] = y[1];
+                f[cc][db][4 * hh + 2] = y[2];
+                f[cc][db][4 * hh + 3] = y[3];
+            }
+        }
+    }
+}
+
+template <int D, bool CLAMP>
+__global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, int n_qt, int64_t n_logical) {
+    using T = Tile<D>;
+    constexpr int KS = T::KS, DB = T::DB;
+    const FwdParams &p = bp.f;
+    __shared__ TileBuf<D> tA, tB;
+    const int64_t logical = xcd_remap(blockIdx.x, n_logical);
+    if (logical < 0) return;
+    const int qt = (int)(logical % n_qt);
+    const int64_t bh = logical / n_qt;
+    const int h = (int)(bh % p.H), b = (int)(bh / p.H);
+
+    const int tid = threadIdx.x;
+    const int lane = __lane_id();
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 5, c = lane & 31;
+    const int N = p.N, kw = p.k, pi = p.pi;
+    const int t0 = qt * BM;
+    const int q0 = t0 + 32 * w;
+    const int t = q0 + c;
+    const bool t_ok = t < N;
+    const int tq = t_ok ? t : 0;
+    const int64_t row = bh * N + tq;
+
+    const int64_t base = b * p.sb + h * p.sh;
+    const __bf16 *qp = (const __bf16 *)p.q + base;
+    const __bf16 *kp = (const __bf16 *)p.k_ptr + base;
+    const __bf16 *vp = (const __bf16 *)p.v + base;
+    const __bf16 *op = (const __bf16 *)bp.dout + b * bp.osb + h * bp.osh;
+    const int64_t sn = p.sn;
+
+    const int kb0 = window_lo(t0, kw) & ~31;
+    const int kend = min(t0 + BM, N);
+    const int ntiles = (kend - kb0 + TK - 1) / TK;
+    const int rowb = (int)(2 * sn);
+    const __amdgpu_buffer_rsrc_t rk =
+        __builtin_amdgcn_make_buffer_rsrc((void *)(kp + (int64_t)kb0 * sn), (short)0, (kend - kb0) * rowb, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rv =
+        __builtin_amdgcn_make_buffer_rsrc((void *)(vp + (int64_t)kb0 * sn), (short)0, (kend - kb0) * rowb, 0x00020000);
+    Stage<D> st;
+    Stage<D> st0[BPT];
+#pragma unroll
+    for (int hf = 0; hf < BPT; ++hf) tile_load<D>(st0[hf], rk, rv, rowb, 0, hf, tid);
+
+    // Query and dL/dy rows as B operands (lanes without a query hold zeros).
+    bf16x8 qf[KS], of[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        const bf16x8 qv = *reinterpret_cast<const bf16x8 *>(qp + tq * sn + 16 * s + 8 * g);
+        const bf16x8 ov = *reinterpret_cast<const bf16x8 *>(op + tq * bp.osn + 16 * s + 8 * g);
+        qf[s] = t_ok ? qv : bf16x8{};
+        of[s] = t_ok ? ov : bf16x8{};
+    }
+    const float gl = p.gate[b * p.gsb + h * p.gsh + tq * p.gsn];
+    const FusionBias fb = fusion_bias(gl, CLAMP);
+    const float lse = bp.lse[row], r = bp.rowterm[row];
+    // alpha^ = exp2(delta * log2e - lse2), delta with the biases of fb
+    const float lse2 = (lse - fb.lse_shift) * kLog2e;
+    const float c2 = p.scale * kLog2e;
+    const float ga = 1.0f / (1.0f + __expf(-gl));
+    const float gat = kGateEps + (1.0f - 2.0f * kGateEps) * ga;
+    const float gcoef = (1.0f - 2.0f * kGateEps) * ga * (1.0f - ga);
+    const float dlog_local = gcoef / gat, dlog_partner = -gcoef / (1.0f - gat);
+
+    f32x16 dq[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) dq[db] = f32x16{};
+    // exact row term and per-prior sums for the gate gradient
+    float r_all = 0.0f, a_loc = 0.0f, b_loc = 0.0f, a_par = 0.0f, b_par = 0.0f;
+
+    // ---- partner: the diagonal of K_p Q^T and V_p dO^T ----------------------
+    const int prow = t - pi;
+    const bool has_p = partner_enabled(kw, pi) && prow >= 0 && t_ok;
+    if (__builtin_amdgcn_ballot_w64(has_p) != 0) {
+        const int prc = has_p ? prow : 0;
+        bf16x8 kpf[KS], vpf[KS];
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            kpf[s] = *reinterpret_cast<const bf16x8 *>(kp + prc * sn + 16 * s + 8 * g);
+            vpf[s] = *reinterpret_cast<const bf16x8 *>(vp + prc * sn + 16 * s + 8 * g);
+        }
+        f32x16 sa = {}, da = {};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(has_p ? kpf[s] : bf16x8{}, qf[s], sa, 0, 0, 0);
+            da = __builtin_amdgcn_mfma_f32_32x32x16_bf16(has_p ? vpf[s] : bf16x8{}, of[s], da, 0, 0, 0);
+        }
+        const float sd = diagonal(sa, c, g), dpd = diagonal(da, c, g);
+        float delta2;
+        bool cut = false;
+        if constexpr (CLAMP) {
+            const float dl = fminf(fmaxf(sd * p.scale + fb.partner, -p.clamp), p.clamp);
+            cut = fabsf(dl) >= p.clamp;
+            delta2 = dl * kLog2e;
+        } else {
+            delta2 = sd * c2 + fb.partner * kLog2e;
+        }
+        const float wgt = has_p ? __builtin_amdgcn_exp2f(delta2 - lse2) : 0.0f;
+        const float dd = cut ? 0.0f : wgt * (dpd - r);
+        if (g == 0) {   // one lane of the pair counts the partner
+            r_all = wgt * dpd;
+            a_par = cut ? 0.0f : wgt * dpd;
+            b_par = cut ? 0.0f : wgt;
+        }
+        // dq += dd * k_p over this lane's dims 32db + 8i + 4g + [0, 4)
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint2 raw = *reinterpret_cast<const uint2 *>(kp + prc * sn + 32 * db + 8 * i + 4 * g);
+                dq[db][4 * i + 0] += dd * __uint_as_float(raw.x << 16);
+                dq[db][4 * i + 1] += dd * __uint_as_float(raw.x & 0xffff0000u);
+                dq[db][4 * i + 2] += dd * __uint_as_float(raw.y << 16);
+                dq[db][4 * i + 3] += dd * __uint_as_float(raw.y & 0xffff0000u);
+            }
+        }
+    }
+#pragma unroll
+    for (int hf = 0; hf < BPT; ++hf) tile_store<D>(st0[hf], tA, hf, tid);
+    __syncthreads();
+
+    // ---- window band ---------------------------------------------------------
+    auto block = [&](const TileBuf<D> &tb, int j0, int blk) {
+        const bool act = j0 < kend && q0 < N && j0 <= q0 + 31 && j0 + 31 >= q0 - kw;
+        if (!act) return;
+        const bool edge = !(j0 + 31 <= q0 && j0 >= q0 + 31 - kw) || q0 + 31 >= N;
+        bf16x8 f[KS];
+        read_rows<D>(f, tb.k, blk, c, g);
+        f32x16 sc = {};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[s], qf[s], sc, 0, 0, 0);
+        read_rows<D>(f, tb.v, blk, c, g);
+        f32x16 dp = {};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[s], of[s], dp, 0, 0, 0);
+        bf16x8 kt[2][DB];
+        read_cols<D>(kt, tb.k, blk, lane);
+        float ds[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            float delta2;
+            bool cut = false;
+            if constexpr (CLAMP) {
+                const float dl = fminf(fmaxf(sc[e] * p.scale + fb.local, -p.clamp), p.clamp);
+                cut = fabsf(dl) >= p.clamp;
+                delta2 = dl * kLog2e;
+            } else {
+                delta2 = sc[e] * c2;
+            }
+            if (edge) {
+                const int j = j0 + 8 * (e >> 2) + 4 * g + (e & 3);
+                if (!(t_ok && j <= t && j >= t - kw)) delta2 = -INFINITY;
+            }
+            const float wgt = __builtin_amdgcn_exp2f(delta2 - lse2);
+            const float pd = wgt * dp[e];
+            ds[e] = cut ? 0.0f : pd - wgt * r;
+            r_all += pd;
+            a_loc += cut ? 0.0f : pd;
+            b_loc += cut ? 0.0f : wgt;
+        }
+        bf16x8 dsb[2];
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) dsb[cc][e] = (__bf16)ds[8 * cc + e];
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc)
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+                dq[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt[cc][db], dsb[cc], dq[db], 0, 0, 0);
+    };
+    auto tile = [&](const TileBuf<D> &cur, int row0, TileBuf<D> &nxt, bool has_next) {
+#pragma unroll
+        for (int blk = 0; blk < BPT; ++blk) {
+            if (has_next) tile_load<D>(st, rk, rv, rowb, row0 - kb0 + TK, blk, tid);
+            block(cur, row0 + 32 * blk, blk);
+            if (has_next) tile_store<D>(st, nxt, blk, tid);
+        }
+    };
+    for (int it = 0; it < ntiles; it += 2) {
+        const int row0 = kb0 + TK * it;
+        tile(tA, row0, tB, it + 1 < ntiles);
+        if (it + 1 >= ntiles) break;
+        __syncthreads();
+        tile(tB, row0 + TK, tA, it + 2 < ntiles);
+        if (it + 2 >= ntiles) break;
+        __syncthreads();
+    }
+
+    // ---- store ---------------------------------------------------------------
+    const float rs = r_all + other_half(r_all);
+    const float al = a_loc + other_half(a_loc), bl = b_loc + other_half(b_loc);
+    const float ap = a_par + other_half(a_par), bpar = b_par + other_half(b_par);
+    const float dg_tot = dlog_local * (al - rs * bl) + dlog_partner * (ap - rs * bpar);
+    if (t_ok) {
+        float *dqp = bp.dq + row * D;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                f32x4 o;
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) o[jj] = dq[db][4 * i + jj] * p.scale;
+                *reinterpret_cast<f32x4 *>(dqp + 32 * db + 8 * i + 4 * g) = o;
+            }
+        }
+        if (g == 0) bp.dgate[row] = dg_tot;
+    }
+}
+
+template <int D, bool CLAMP>
+hipError_t launch_q(const BwdParams &p, hipStream_t stream) {
+    const int n_qt = (p.f.N + BM - 1) / BM;
+    const int64_t n_logical = (int64_t)p.f.B * p.f.H * n_qt;
+    const int64_t grid = xcd_grid(n_logical);
+    return launch_kernel(backward_q_bf16_kernel<D, CLAMP>, dim3((unsigned)grid), dim3(NT), stream, p, n_qt,
+                         n_logical);
+}
+
+}  // namespace
+
+hipError_t launch_backward_q_bf16(const BwdParams &p, hipStream_t stream) {
+    const bool clamp = p.f.clamp > 0.0f;
+    if (p.f.D == 64) return clamp ? launch_q<64, true>(p, stream) : launch_q<64, false>(p, stream);
+    return clamp ? launch_q<128, true>(p, stream) : launch_q<128, false>(p, stream);
+}
+
+}  // namespace pi_attn

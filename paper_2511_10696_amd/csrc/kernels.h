@@ -48,8 +48,8 @@ struct BwdParams {
     FwdParams f;                    // inputs as for the forward (out/lse unused)
     int dtype;                      // 0 = float32, 1 = bf16 (q, k, v, dout)
     const float *lse;               // [B][H][N]
-    const void *dout;
-    int64_t osb, osh, osn;          // element strides of dout
+    const void *out, *dout;         // forward output and dL/dy
+    int64_t osb, osh, osn;          // element strides of out and dout
     float *dq, *dk, *dv;            // [B][H][N][D] contiguous
     float *dgate, *rowterm;         // [B][H][N] contiguous
 };
@@ -67,8 +67,11 @@ hipError_t launch_forward_bf16(const FwdParams &p, hipStream_t stream);
 // bf16 decode step, working set split across wavefronts (D = 64 or 128).
 hipError_t launch_decode_bf16(const DecodeParams &p, hipStream_t stream);
 
-// Backward: a query pass (dq, dgate, rowterm) then a key pass (dk, dv),
-// one wavefront per row, fp32 arithmetic for both input dtypes.
+// Backward: the row terms <dL/dy_t, y_t>, a query pass (dq, dgate) and a
+// key pass (dk, dv).
 hipError_t launch_backward(const BwdParams &p, hipStream_t stream);
+
+// MFMA query pass (dq, dgate) for bf16 inputs; needs the row terms.
+hipError_t launch_backward_q_bf16(const BwdParams &p, hipStream_t stream);
 
 }  // namespace pi_attn

@@ -86,20 +86,21 @@ def test_forward_empty_is_noop(lib, kw):
 
 def bwd(lib, **kw):
     a = dict(dtype=1, B=1, H=2, N=256, D=64, k=32, pi=64, q=16, kk=16, v=16, sb=32768, sh=16384, sn=64,
-             gate=16, gsb=0, gsh=1, gsn=0, scale=0.125, clamp=0.0, lse=16, dout=16, osb=32768, osh=16384,
+             gate=16, gsb=0, gsh=1, gsn=0, scale=0.125, clamp=0.0, lse=16, out=16, dout=16, osb=32768, osh=16384,
              osn=64, dq=16, dk=16, dv=16, dg=16, rt=16, stream=None)
     a.update(kw)
     vp = lambda x: None if x is None else ctypes.c_void_p(x)
     return lib.pi_attn_backward(a["dtype"], a["B"], a["H"], a["N"], a["D"], a["k"], a["pi"], vp(a["q"]),
                                 vp(a["kk"]), vp(a["v"]), a["sb"], a["sh"], a["sn"], vp(a["gate"]), a["gsb"],
-                                a["gsh"], a["gsn"], a["scale"], a["clamp"], vp(a["lse"]), vp(a["dout"]),
+                                a["gsh"], a["gsn"], a["scale"], a["clamp"], vp(a["lse"]), vp(a["out"]), vp(a["dout"]),
                                 a["osb"], a["osh"], a["osn"], vp(a["dq"]), vp(a["dk"]), vp(a["dv"]),
                                 vp(a["dg"]), vp(a["rt"]), vp(a["stream"]))
 
 
 @pytest.mark.parametrize("kw,code", [
     (dict(dtype=5), EUNSUP), (dict(D=32), EUNSUP), (dict(B=-1), EINVAL), (dict(k=-1), EINVAL),
-    (dict(lse=None), EINVAL), (dict(dout=None), EINVAL), (dict(dq=None), EINVAL), (dict(dk=None), EINVAL),
+    (dict(lse=None), EINVAL), (dict(out=None), EINVAL), (dict(out=8), EINVAL),
+    (dict(dout=None), EINVAL), (dict(dq=None), EINVAL), (dict(dk=None), EINVAL),
     (dict(dv=None), EINVAL), (dict(dg=None), EINVAL), (dict(rt=None), EINVAL), (dict(q=None), EINVAL),
     (dict(lse=18), EINVAL), (dict(dq=20), EINVAL), (dict(dout=24), EINVAL), (dict(osn=4), EINVAL),
     (dict(scale=0.0), EINVAL), (dict(clamp=float("nan")), EINVAL), (dict(gsh=-1), EINVAL),

@@ -1,14 +1,16 @@
 """GPU parity of the backward (pi_attn_backward through the C ABI) against
 the fp64 oracle gradients on the same seeded inputs and cotangent.
 
-The kernels compute in float32 for both input dtypes (bf16 data is widened
-exactly), recomputing the weights from the forward's lse, so the bar is a
-float32 one: every gradient entry within 1e-4 * max(1, max |ref|) of the
-oracle.  Each entry is a float32 sum of at most k + 2 terms of size <= that
-scale, which errs by about (k + 2) * 2^-24 * scale <= 3.1e-5 * scale at
-k = 512, plus the lse's own float32 rounding.  The gate gradient is compared
-per query; a per-head gate's sum over (b, t) is then held to 1e-4 times the
-sum of the per-query magnitudes.
+Float32 inputs run float32 kernels and are held to a float32 bar: every
+gradient entry within 1e-4 * max(1, max |ref|) of the oracle (a float32 sum
+of at most k + 2 terms of size <= that scale errs by about
+(k + 2) * 2^-24 * scale <= 3.1e-5 * scale at k = 512).  bf16 inputs take the
+bf16 forward's output y in the row term <dL/dy, y> and feed bf16-rounded
+softmax gradients to the MFMA products (2^-9 relative each), so they are
+held to the forward's bf16 bar per gradient tensor: max-abs within
+2e-2 * scale and relative L2 within 5e-3.  The gate gradient is compared per
+query; a per-head gate's sum over (b, t) is then held to the same factor
+times the sum of the per-query magnitudes.
 """
 import math
 
@@ -23,33 +25,40 @@ from paper_2511_10696_amd import workloads as W
 pytestmark = pytest.mark.gpu
 
 GRAD_TOL = 1e-4
+BF16_GRAD_MAXABS, BF16_GRAD_RELL2 = 2e-2, 5e-3
 
 
 def np32(t):
     return t.detach().float().cpu().numpy()
 
 
-def assert_grad(got, ref, what):
+def assert_grad(got, ref, what, dtype=torch.float32):
     got, ref = np.asarray(got, np.float64), np.asarray(ref, np.float64)
     assert got.shape == ref.shape, (what, got.shape, ref.shape)
     assert np.isfinite(got).all(), f"{what}: non-finite"
     scale = max(1.0, float(np.abs(ref).max()))
     err = float(np.abs(got - ref).max())
-    assert err <= GRAD_TOL * scale, f"{what}: max-abs {err:.3g} (scale {scale:.3g})"
+    if dtype == torch.float32:
+        assert err <= GRAD_TOL * scale, f"{what}: max-abs {err:.3g} (scale {scale:.3g})"
+        return
+    rel = float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30))
+    assert err <= BF16_GRAD_MAXABS * scale, f"{what}: max-abs {err:.3g} (scale {scale:.3g})"
+    assert rel <= BF16_GRAD_RELL2 or err <= 1e-3 * scale, f"{what}: rel-L2 {rel:.3g}"
 
 
 def run_case(q, k, v, gate, kw, pi, seed, clamp=0.0, scale=None):
     out, lse = pa.pi_attn_forward(q, k, v, gate, kw, pi, return_lse=True, logit_clamp=clamp, scale=scale)
     dout = W.cotangent(q.shape, q.dtype, seed, q.device)
-    dq, dk, dv, dg = pa.pi_attn_backward(q, k, v, gate, kw, pi, dout, lse, logit_clamp=clamp, scale=scale,
-                                         gate_grad_per_query=True)
+    dq, dk, dv, dg = pa.pi_attn_backward(q, k, v, gate, kw, pi, out, lse, dout, logit_clamp=clamp,
+                                         scale=scale, gate_grad_per_query=True)
     torch.cuda.synchronize()
     rq, rk, rv, rg = oracle.backward(q, k, v, gate, kw, pi, dout, scale=scale, clamp=clamp)
     for name, got, ref in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv), ("dgate", dg, rg)):
-        assert_grad(np32(got), ref, name)
+        assert_grad(np32(got), ref, name, q.dtype)
     if gate.dim() == 1:   # the per-head reduction the binding does by default
-        *_, dgh = pa.pi_attn_backward(q, k, v, gate, kw, pi, dout, lse, logit_clamp=clamp, scale=scale)
-        bound = GRAD_TOL * np.maximum(1.0, np.abs(rg).sum(axis=(0, 2)))
+        *_, dgh = pa.pi_attn_backward(q, k, v, gate, kw, pi, out, lse, dout, logit_clamp=clamp, scale=scale)
+        tol = GRAD_TOL if q.dtype == torch.float32 else BF16_GRAD_MAXABS
+        bound = tol * np.maximum(1.0, np.abs(rg).sum(axis=(0, 2)))
         assert (np.abs(np32(dgh) - rg.sum(axis=(0, 2))) <= bound).all(), "per-head dgate"
 
 
