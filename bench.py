@@ -27,7 +27,6 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
-VALU_F32_PEAK_TFLOPS = 157.3    # MI355X fp32 vector ALU, TFLOP/s
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "forward_bf16_fwd32k_hbm_traffic.txt")
 DECODE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_bf16_s64_hbm_traffic.txt")
 COPY_PROBE_BYTES = 1 << 30      # plain device copy used to calibrate the HBM byte counters
@@ -285,15 +284,24 @@ def bench_backward(cfg, W, pa, torch, dev, stream, steps):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
     keys, flops, nbytes = backward_algorithmic(cfg)
-    tflops = flops / (ms / 1e3) / 1e12
+    sec = ms / 1e3
+    tflops, gbs = flops / sec / 1e12, nbytes / sec / 1e9
+    t_hbm, t_mfma = nbytes / (HBM_PEAK_GBS * 1e9), flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
+    hbm = t_hbm >= t_mfma
     del q, k, v, out, dout, lse
     torch.cuda.empty_cache()
+    kernels = "rowterm_kernel + backward_q_bf16_kernel<128> + backward_kv_bf16_kernel<128>"
     return {"workload": "backward of fwd32k: B1 H32 N32768 D128 k512 pi1024 bf16 in, fp32 gradients",
             "steps": steps, "ms_per_step": round(ms, 4),
-            "roofline": {"bound": "alu", "kernel": "backward_q_kernel<128> + backward_kv_kernel<128>",
-                         "achieved": round(tflops, 3), "peak": VALU_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
-                         "frac": round(tflops / VALU_F32_PEAK_TFLOPS, 5), "flops_per_step": flops,
-                         "bytes_per_step": nbytes, "traffic": None}}
+            "roofline": {"bound": "hbm" if hbm else "mfma", "kernel": kernels,
+                         "achieved": round(gbs if hbm else tflops, 2),
+                         "peak": HBM_PEAK_GBS if hbm else MFMA_BF16_PEAK_TFLOPS,
+                         "unit": "GB/s" if hbm else "TFLOP/s",
+                         "frac": round((gbs / HBM_PEAK_GBS) if hbm else (tflops / MFMA_BF16_PEAK_TFLOPS), 4),
+                         "traffic": None},
+            "roofline_mfma": {"achieved": round(tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                              "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "flops_per_step": flops,
+                              "bytes_per_step": nbytes}}
 
 
 def cpu_baseline(cfg, W):

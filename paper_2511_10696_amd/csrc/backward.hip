@@ -18,8 +18,8 @@
 // pass: wavefront per (b, h, t), lane l holding elements l, l+64, ..., one
 // sweep over W_t.  Key pass: wavefront per (b, h, j) over the queries whose
 // working set holds j: t in [j, j + k] and, when pi > k, t = j + pi.  These
-// are the float32 kernels (every dot product a wavefront reduction); for
-// bf16 inputs the query pass is the MFMA kernel of backward_bf16.hip.
+// are the float32 kernels (every dot product a wavefront reduction); bf16
+// inputs run the MFMA passes of backward_bf16.hip and backward_kv_bf16.hip.
 #include "kernels.h"
 #include "pi_common.h"
 
@@ -210,11 +210,13 @@ hipError_t launch(const BwdParams &p, hipStream_t stream) {
     if (e != hipSuccess) return e;
     if constexpr (sizeof(T) == 2) {
         e = launch_backward_q_bf16(p, stream);
+        if (e != hipSuccess) return e;
+        return launch_backward_kv_bf16(p, stream);
     } else {
         e = launch_kernel(backward_q_kernel<D, T>, grid, block, stream, p);
+        if (e != hipSuccess) return e;
+        return launch_kernel(backward_kv_kernel<D, T>, grid, block, stream, p);
     }
-    if (e != hipSuccess) return e;
-    return launch_kernel(backward_kv_kernel<D, T>, grid, block, stream, p);
 }
 
 }  // namespace

@@ -1,0 +1,328 @@
+// backward_kv_bf16.hip -- MFMA key pass of the backward for bf16 inputs:
+// dk and dv (D = 64 or 128), fp32 accumulation.
+//
+// A work-group of 4 wavefronts owns 128 keys [j0, j0 + 128) of one (b, h);
+// wavefront w the 32 keys kq0 = j0 + 32w + [0, 32), whose K and V rows stay
+// in registers as B operands.  The queries that hold these keys in their
+// working set stream through LDS in 64-row tiles of Q and dL/dy, with the
+// per-query lse, row term r_t = <dL/dy_t, y_t> and prior bias: first the
+// window band, queries [j0, j0 + 127 + k] (key j is in W_t iff
+// j <= t <= j + k, Sec. 3.2 eq. Nr), then the partner run
+// [j0 + pi, j0 + pi + 128) (key j is the partner of query j + pi when
+// pi > k, Sec. 3.4 eq. Npi), in which wavefront w meets its partners on
+// the diagonal of block w.  Per 32-query block, on
+// v_mfma_f32_32x32x16_bf16:
+//   S   = Q K^T      A = Q rows (LDS), B = K^T (registers)
+//   dP  = dO V^T     A = dO rows (LDS), B = V^T (registers)
+// both with lane l holding key l%32 and queries 8i + 4(l/32) + j at slot
+// 4i + j; then alpha^ = exp(delta - lse_t), dS = alpha^ (dP - r_t) (Sec.
+// 3.5 eq. jac; 0 where the clamp saturates), and
+//   dV^T += dO^T alpha^   A = dO^T by LDS transpose reads
+//   dK^T += Q^T dS        A = Q^T by LDS transpose reads
+// with the query order permuted inside each 16-query chunk as the forward
+// permutes V^T against P^T.  dk carries the factor scale.
+//
+// The dK^T and dV^T accumulators (128 registers at D = 128) are only read
+// at the end, so this file keeps MFMA accumulators in accumulation
+// registers; one work-group per CU.
+#include "kernels.h"
+#include "pi_common.h"
+
+namespace pi_attn {
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+constexpr int WAVES = 4;
+constexpr int NT = 64 * WAVES;
+constexpr int BK = 32 * WAVES;   // keys per work-group
+constexpr int TQ = 64;           // query rows per LDS tile
+constexpr int BPT = TQ / 32;
+
+template <int D>
+struct Tile {
+    static constexpr int CPR = D / 8;
+    static constexpr int ROW = 2 * D + 16;   // padded LDS row stride (bytes)
+    static constexpr int BYTES = TQ * ROW;
+    static constexpr int KS = D / 16;
+    static constexpr int DB = D / 32;
+    static constexpr int CH = TQ * CPR / NT;  // staged chunks per thread and tensor
+};
+
+template <int D>
+struct QTile {
+    alignas(16) unsigned char q[Tile<D>::BYTES];
+    alignas(16) unsigned char o[Tile<D>::BYTES];
+    alignas(16) float lse2[TQ];   // (lse_t - lse_shift_t) * log2 e
+    alignas(16) float r[TQ];      // row term
+    alignas(16) float bias[TQ];   // prior bias of this stream (natural log)
+};
+
+template <int D>
+struct Stage {
+    uint4 q[Tile<D>::CH];
+    uint4 o[Tile<D>::CH];
+    float lse2, r, bias;
+};
+
+__device__ inline float other_half(float x) {
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(__lane_id() < 32 ? p[1] : p[0]);
+}
+
+template <int D, bool CLAMP>
+__global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, int n_kt, int64_t n_logical) {
+    using T = Tile<D>;
+    constexpr int KS = T::KS, DB = T::DB;
+    const FwdParams &p = bp.f;
+    __shared__ QTile<D> tA, tB;
+    const int64_t logical = xcd_remap(blockIdx.x, n_logical);
+    if (logical < 0) return;
+    const int kt = (int)(logical % n_kt);
+    const int64_t bh = logical / n_kt;
+    const int h = (int)(bh % p.H), b = (int)(bh / p.H);
+
+    const int tid = threadIdx.x;
+    const int lane = __lane_id();
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 5, c = lane & 31;
+    const int N = p.N, kw = p.k, pi = p.pi;
+    const int j0 = kt * BK;
+    const int kq0 = j0 + 32 * w;
+    const int j = kq0 + c;           // this lane's key
+    const bool j_ok = j < N;
+    const int jq = j_ok ? j : 0;
+
+    const int64_t base = b * p.sb + h * p.sh;
+    const __bf16 *qp = (const __bf16 *)p.q + base;
+    const __bf16 *kp = (const __bf16 *)p.k_ptr + base;
+    const __bf16 *vp = (const __bf16 *)p.v + base;
+    const __bf16 *op = (const __bf16 *)bp.dout + b * bp.osb + h * bp.osh;
+    const int64_t sn = p.sn, osn = bp.osn;
+    const int64_t rbase = bh * N;
+    const bool exact = CLAMP;
+    const float c2 = p.scale * kLog2e;
+
+    // K^T and V^T B operands of this wavefront's keys (zero past N).
+    bf16x8 kf[KS], vf[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        const bf16x8 kv = *reinterpret_cast<const bf16x8 *>(kp + jq * sn + 16 * s + 8 * g);
+        const bf16x8 vv = *reinterpret_cast<const bf16x8 *>(vp + jq * sn + 16 * s + 8 * g);
+        kf[s] = j_ok ? kv : bf16x8{};
+        vf[s] = j_ok ? vv : bf16x8{};
+    }
+    f32x16 dk[DB], dv[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+        dk[db] = f32x16{};
+        dv[db] = f32x16{};
+    }
+
+    // Query streams: the window band, then (pi > k) the partner run.
+    const int band_lo = j0, band_hi = min(N, j0 + BK + kw);   // queries [band_lo, band_hi)
+    const int nband = band_hi > band_lo ? (band_hi - band_lo + TQ - 1) / TQ : 0;
+    const bool has_par = partner_enabled(kw, pi) && (int64_t)j0 + pi < N;
+    const int par_lo = j0 + pi;
+    const int par_hi = has_par ? min(N, j0 + pi + BK) : par_lo;
+    const int npar = has_par ? (par_hi - par_lo + TQ - 1) / TQ : 0;
+    const int ntiles = nband + npar;
+
+    // Stage tile m of the combined stream: 64 query rows starting at q0m.
+    auto tile_start = [&](int m) { return m < nband ? band_lo + TQ * m : par_lo + TQ * (m - nband); };
+    auto tile_end = [&](int m) { return m < nband ? band_hi : par_hi; };
+    auto load = [&](Stage<D> &st, int m) {
+        const int q0m = tile_start(m), lim = tile_end(m);
+#pragma unroll
+        for (int u = 0; u < T::CH; ++u) {
+            const int cid = tid + NT * u;
+            const int row = cid / T::CPR, pc = cid % T::CPR;
+            const int t = q0m + row;
+            const int tc = t < lim ? t : q0m;
+            const uint4 qv = *reinterpret_cast<const uint4 *>(qp + tc * sn + 8 * pc);
+            const uint4 ov = *reinterpret_cast<const uint4 *>(op + tc * osn + 8 * pc);
+            st.q[u] = t < lim ? qv : make_uint4(0, 0, 0, 0);
+            st.o[u] = t < lim ? ov : make_uint4(0, 0, 0, 0);
+        }
+        if (tid < TQ) {
+            const int t = q0m + tid;
+            const int tc = t < lim ? t : q0m;
+            const FusionBias fb = fusion_bias(p.gate[b * p.gsb + h * p.gsh + tc * p.gsn], exact);
+            st.lse2 = (bp.lse[rbase + tc] - fb.lse_shift) * kLog2e;
+            st.r = bp.rowterm[rbase + tc];
+            st.bias = m < nband ? fb.local : fb.partner;
+        }
+    };
+    auto store = [&](const Stage<D> &st, QTile<D> &tb) {
+#pragma unroll
+        for (int u = 0; u < T::CH; ++u) {
+            const int cid = tid + NT * u;
+            const int row = cid / T::CPR, pc = cid % T::CPR;
+            *reinterpret_cast<uint4 *>(tb.q + row * T::ROW + pc * 16) = st.q[u];
+            *reinterpret_cast<uint4 *>(tb.o + row * T::ROW + pc * 16) = st.o[u];
+        }
+        if (tid < TQ) {
+            tb.lse2[tid] = st.lse2;
+            tb.r[tid] = st.r;
+            tb.bias[tid] = st.bias;
+        }
+    };
+
+    // One 32-query block (rows 32 blk.. of tile tb, first query t0b).
+    auto block = [&](const QTile<D> &tb, int t0b, int blk, bool partner, int lim) {
+        bool act;
+        if (partner) {
+            act = blk == (w & 1) && t0b == kq0 + pi;
+        } else {
+            act = t0b < lim && kq0 < N && t0b <= kq0 + 31 + kw && t0b + 31 >= kq0;
+        }
+        if (!act) return;
+        const bool edge = partner || !(t0b >= kq0 + 31 && t0b + 31 <= kq0 + kw) || t0b + 31 >= N || kq0 + 31 >= N;
+        // rows of this block (A operands: query l%32, dims 16s + 8g)
+        const unsigned char *qrow = tb.q + (32 * blk + c) * T::ROW + 16 * g;
+        const unsigned char *orow = tb.o + (32 * blk + c) * T::ROW + 16 * g;
+        f32x16 sc = {}, dp = {};
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+            sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8 *>(qrow + 32 * s), kf[s], sc,
+                                                         0, 0, 0);
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+            dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8 *>(orow + 32 * s), vf[s], dp,
+                                                         0, 0, 0);
+        // per-query terms of this lane's queries 8i + 4g + jj
+        float pr[16], ds[16];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int qi = 32 * blk + 8 * i + 4 * g;
+            const f32x4 l4 = *reinterpret_cast<const f32x4 *>(tb.lse2 + qi);
+            const f32x4 r4 = *reinterpret_cast<const f32x4 *>(tb.r + qi);
+            const f32x4 b4 = *reinterpret_cast<const f32x4 *>(tb.bias + qi);
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int e = 4 * i + jj;
+                float delta2;
+                bool cut = false;
+                if constexpr (CLAMP) {
+                    const float dl = fminf(fmaxf(sc[e] * p.scale + b4[jj], -p.clamp), p.clamp);
+                    cut = fabsf(dl) >= p.clamp;
+                    delta2 = dl * kLog2e;
+                } else {
+                    delta2 = __builtin_fmaf(sc[e], c2, b4[jj] * kLog2e);
+                }
+                if (edge) {
+                    const int t = t0b + 8 * i + 4 * g + jj;
+                    const bool ok = partner ? (t - j == pi && t < N && j_ok)
+                                            : (t >= j && t - j <= kw && t < N && j_ok);
+                    if (!ok) delta2 = -INFINITY;
+                }
+                const float wgt = __builtin_amdgcn_exp2f(delta2 - l4[jj]);
+                pr[e] = wgt;
+                ds[e] = cut ? 0.0f : wgt * (dp[e] - r4[jj]);
+            }
+        }
+        bf16x8 pb[2], db8[2];
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                pb[cc][e] = (__bf16)pr[8 * cc + e];
+                db8[cc][e] = (__bf16)ds[8 * cc + e];
+            }
+        }
+        // transposed tiles (A operands: dim 32db + l%32, queries permuted)
+        const int G = lane >> 4, rr = (lane >> 2) & 3, qd = lane & 3;
+        const int toff = (32 * blk + 4 * g + rr) * T::ROW + (2 * (G & 1) + (qd >> 1)) * 16 + (qd & 1) * 8;
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc) {
+#pragma unroll
+            for (int d = 0; d < DB; ++d) {
+                bf16x8 ao, aq;
+#pragma unroll
+                for (int hh = 0; hh < 2; ++hh) {
+                    const int off = toff + (16 * cc + 8 * hh) * T::ROW + 64 * d;
+                    const bf16x4 yo = __builtin_bit_cast(
+                        bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(tb.o + off)));
+                    const bf16x4 yq = __builtin_bit_cast(
+                        bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(tb.q + off)));
+#pragma unroll
+                    for (int x = 0; x < 4; ++x) {
+                        ao[4 * hh + x] = yo[x];
+                        aq[4 * hh + x] = yq[x];
+                    }
+                }
+                dv[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ao, pb[cc], dv[d], 0, 0, 0);
+                dk[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, db8[cc], dk[d], 0, 0, 0);
+            }
+        }
+    };
+
+    if (ntiles > 0) {
+        Stage<D> st;
+        load(st, 0);
+        store(st, tA);
+        __syncthreads();
+        for (int m = 0; m < ntiles; m += 2) {
+            // tile m in tA; stage m+1 into tB while it is consumed
+            if (m + 1 < ntiles) load(st, m + 1);
+#pragma unroll
+            for (int blk = 0; blk < BPT; ++blk)
+                block(tA, tile_start(m) + 32 * blk, blk, m >= nband, tile_end(m));
+            if (m + 1 >= ntiles) break;
+            store(st, tB);
+            __syncthreads();
+            if (m + 2 < ntiles) load(st, m + 2);
+#pragma unroll
+            for (int blk = 0; blk < BPT; ++blk)
+                block(tB, tile_start(m + 1) + 32 * blk, blk, m + 1 >= nband, tile_end(m + 1));
+            if (m + 2 >= ntiles) break;
+            store(st, tA);
+            __syncthreads();
+        }
+    }
+
+    // ---- store: lane (c, g) holds dims 32db + 8i + 4g + [0, 4) of key c ----
+    if (j_ok) {
+        const int64_t row = rbase + j;
+        float *dkp = bp.dk + row * D, *dvp = bp.dv + row * D;
+#pragma unroll
+        for (int d = 0; d < DB; ++d) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                f32x4 a, v4;
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    a[x] = dk[d][4 * i + x] * p.scale;
+                    v4[x] = dv[d][4 * i + x];
+                }
+                *reinterpret_cast<f32x4 *>(dkp + 32 * d + 8 * i + 4 * g) = a;
+                *reinterpret_cast<f32x4 *>(dvp + 32 * d + 8 * i + 4 * g) = v4;
+            }
+        }
+    }
+}
+
+template <int D, bool CLAMP>
+hipError_t launch_kv(const BwdParams &p, hipStream_t stream) {
+    const int n_kt = (p.f.N + BK - 1) / BK;
+    const int64_t n_logical = (int64_t)p.f.B * p.f.H * n_kt;
+    const int64_t grid = xcd_grid(n_logical);
+    return launch_kernel(backward_kv_bf16_kernel<D, CLAMP>, dim3((unsigned)grid), dim3(NT), stream, p, n_kt,
+                         n_logical);
+}
+
+}  // namespace
+
+hipError_t launch_backward_kv_bf16(const BwdParams &p, hipStream_t stream) {
+    const bool clamp = p.f.clamp > 0.0f;
+    if (p.f.D == 64) return clamp ? launch_kv<64, true>(p, stream) : launch_kv<64, false>(p, stream);
+    return clamp ? launch_kv<128, true>(p, stream) : launch_kv<128, false>(p, stream);
+}
+
+}  // namespace pi_attn

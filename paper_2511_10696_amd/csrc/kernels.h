@@ -74,4 +74,7 @@ hipError_t launch_backward(const BwdParams &p, hipStream_t stream);
 // MFMA query pass (dq, dgate) for bf16 inputs; needs the row terms.
 hipError_t launch_backward_q_bf16(const BwdParams &p, hipStream_t stream);
 
+// MFMA key pass (dk, dv) for bf16 inputs; needs the row terms.
+hipError_t launch_backward_kv_bf16(const BwdParams &p, hipStream_t stream);
+
 }  // namespace pi_attn
