@@ -290,7 +290,7 @@ def bench_backward(cfg, W, pa, torch, dev, stream, steps):
     hbm = t_hbm >= t_mfma
     del q, k, v, out, dout, lse
     torch.cuda.empty_cache()
-    kernels = "rowterm_kernel + backward_q_bf16_kernel<128> + backward_kv_bf16_kernel<128>"
+    kernels = "backward_q_bf16_kernel<128> + backward_kv_bf16_kernel<128>"
     return {"workload": "backward of fwd32k: B1 H32 N32768 D128 k512 pi1024 bf16 in, fp32 gradients",
             "steps": steps, "ms_per_step": round(ms, 4),
             "roofline": {"bound": "hbm" if hbm else "mfma", "kernel": kernels,

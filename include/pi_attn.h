@@ -153,10 +153,12 @@ int pi_attn_decode_step(int32_t dtype, int32_t S, int32_t H, int32_t D, int32_t 
  *                the gate logit as seen by query t (a per-head gate's
  *                gradient is the sum of its entries over b and t).
  *   rowterm      device float32 [B][H][N] contiguous scratch owned by the
- *                caller: receives r_t = <dL/dy_t, y_t>, which equals
- *                sum_j alpha^_tj dL/dalpha^_tj (y_t = sum_j alpha^_tj v_j).
- * Kernels on the stream, in order: the row terms, a query pass (dq, dgate)
- * and a key pass (dk, dv).  Nothing is allocated; buffers must not overlap.
+ *                caller: receives the row terms
+ *                r_t = sum_j alpha^_tj dL/dalpha^_tj = <dL/dy_t, y_t>
+ *                (float32: from out; bf16: as recomputed by the query pass).
+ * Kernels on the stream, in order: (float32) the row terms, then a query
+ * pass (dq, dgate; for bf16 it also writes the row terms) and a key pass
+ * (dk, dv).  Nothing is allocated; buffers must not overlap.
  * Errors: as pi_attn_forward, plus EINVAL for a null or misaligned lse,
  * out, dout, dq, dk, dv, dgate or rowterm.
  */

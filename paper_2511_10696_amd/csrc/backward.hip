@@ -14,7 +14,7 @@
 // d log(1 - alpha~)/dg = -(1 - 2 eps) a (1 - a) / (1 - alpha~) on the partner,
 // a = sigmoid(g).
 //
-// Row terms: r_t from the forward output y (a wavefront per row).  Query
+// Row terms (float32): r_t from the forward output y (a wavefront per row).  Query
 // pass: wavefront per (b, h, t), lane l holding elements l, l+64, ..., one
 // sweep over W_t.  Key pass: wavefront per (b, h, j) over the queries whose
 // working set holds j: t in [j, j + k] and, when pi > k, t = j + pi.  These
@@ -206,13 +206,15 @@ template <int D, typename T>
 hipError_t launch(const BwdParams &p, hipStream_t stream) {
     const int64_t rows = (int64_t)p.f.B * p.f.H * p.f.N;
     const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
-    hipError_t e = launch_kernel(rowterm_kernel<D, T>, grid, block, stream, p);
-    if (e != hipSuccess) return e;
+    hipError_t e;
     if constexpr (sizeof(T) == 2) {
+        // the MFMA query pass computes its row terms and writes the exact ones
         e = launch_backward_q_bf16(p, stream);
         if (e != hipSuccess) return e;
         return launch_backward_kv_bf16(p, stream);
     } else {
+        e = launch_kernel(rowterm_kernel<D, T>, grid, block, stream, p);
+        if (e != hipSuccess) return e;
         e = launch_kernel(backward_q_kernel<D, T>, grid, block, stream, p);
         if (e != hipSuccess) return e;
         return launch_kernel(backward_kv_kernel<D, T>, grid, block, stream, p);

@@ -11,8 +11,9 @@
 // 8i + 4(l/32) + j at slot 4i + j).  The weights come back from the
 // forward's lse, alpha^ = exp(delta - lse), and
 //   dS^T = alpha^ (dP^T - r_t)     (softmax Jacobian, Sec. 3.5 eq. jac)
-// with r_t = <dL/dy_t, y_t> precomputed; dS^T, rounded to bf16, is the B
-// operand of
+// with r_t = <dL/dy_t, y_t> from the forward output (two lanes per query,
+// each with half the dims of dL/dy_t and y_t); dS^T, rounded to bf16, is
+// the B operand of
 //   dQ^T += K^T dS^T    A = K^T by LDS transpose reads of the key tile
 // with the key order permuted inside each 16-key chunk exactly as the
 // forward permutes V^T against P^T.  The gate gradient
@@ -21,7 +22,8 @@
 // row term r* = sum_j alpha^_tj dP_tj accumulated along the way (the r_t
 // used for dS comes from the bf16-rounded forward output): with
 // A = sum alpha^ dP and B = sum alpha^ over the unclamped entries of each
-// prior, dg = sum_prior d(log omega)/dg (A - r* B).  The partner
+// prior, dg = sum_prior d(log omega)/dg (A - r* B).  r* is also written out
+// as the row term of the key pass.  The partner
 // row (Sec. 3.4, eq. Npi) is the diagonal of one 32x32 block per product,
 // read straight from global memory as in the forward.
 //
@@ -200,7 +202,17 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
     }
     const float gl = p.gate[b * p.gsb + h * p.gsh + tq * p.gsn];
     const FusionBias fb = fusion_bias(gl, CLAMP);
-    const float lse = bp.lse[row], r = bp.rowterm[row];
+    // r_t = <dL/dy_t, y_t>: this lane's dims 16s + 8g + [0, 8), then the pair
+    const __bf16 *yp = (const __bf16 *)bp.out + b * bp.osb + h * bp.osh;
+    float rpart = 0.0f;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        const bf16x8 yv = *reinterpret_cast<const bf16x8 *>(yp + tq * bp.osn + 16 * s + 8 * g);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) rpart += (float)of[s][e] * (float)yv[e];
+    }
+    const float r = rpart + other_half(rpart);
+    const float lse = bp.lse[row];
     // alpha^ = exp2(delta * log2e - lse2), delta with the biases of fb
     const float lse2 = (lse - fb.lse_shift) * kLog2e;
     const float c2 = p.scale * kLog2e;
@@ -351,7 +363,10 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
                 *reinterpret_cast<f32x4 *>(dqp + 32 * db + 8 * i + 4 * g) = o;
             }
         }
-        if (g == 0) bp.dgate[row] = dg_tot;
+        if (g == 0) {
+            bp.dgate[row] = dg_tot;
+            bp.rowterm[row] = rs;
+        }
     }
 }
 
