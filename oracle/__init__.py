@@ -1,4 +1,5 @@
-"""fp64 CPU oracle for causal pi-Attention -- TEST INFRASTRUCTURE ONLY.
+"""fp64 CPU oracle for pi-Attention (causal and bidirectional) -- TEST
+INFRASTRUCTURE ONLY.
 
 Nothing in the product path (the HIP library and its Python binding) may
 import, link or call this package.  Its users are the tests, the smoke check
@@ -31,24 +32,25 @@ EPS = 1e-4  # gate clip of Variant 3 (Sec. 3.5)
 
 def build(src: str = _SRC, out: str = _LIB_PATH) -> str:
     """Compile the oracle with gcc (plain -O2, no fast-math)."""
+    tmp = f"{out}.{os.getpid()}.tmp"   # per process: concurrent builds must not collide
     cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
-           "-Wall", "-o", out + ".tmp", src, "-lm"]
+           "-Wall", "-o", tmp, src, "-lm"]
     subprocess.run(cmd, check=True)
-    os.replace(out + ".tmp", out)
+    os.replace(tmp, out)
     return out
 
 
 def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
     i64, dbl, vp = ctypes.c_int64, ctypes.c_double, ctypes.c_void_p
-    lib.oracle_ws_width.argtypes = [ctypes.c_int, ctypes.c_int]
+    lib.oracle_ws_width.argtypes = [ctypes.c_int] * 3
     lib.oracle_ws_width.restype = ctypes.c_int
-    lib.oracle_index_set.argtypes = [ctypes.c_int] * 3 + [vp]
+    lib.oracle_index_set.argtypes = [ctypes.c_int] * 4 + [vp]
     lib.oracle_index_set.restype = None
     lib.oracle_forward_rows.argtypes = (
-        [ctypes.c_int] * 6 + [vp, vp, vp, vp, i64, i64, i64, dbl, dbl, vp, i64, vp, vp, vp])
+        [ctypes.c_int] * 7 + [vp, vp, vp, vp, i64, i64, i64, dbl, dbl, vp, i64, vp, vp, vp])
     lib.oracle_forward_rows.restype = None
     lib.oracle_backward.argtypes = (
-        [ctypes.c_int] * 6 + [vp, vp, vp, vp, i64, i64, i64, dbl, dbl, vp, vp, vp, vp, vp])
+        [ctypes.c_int] * 7 + [vp, vp, vp, vp, i64, i64, i64, dbl, dbl, vp, vp, vp, vp, vp])
     lib.oracle_backward.restype = None
     lib.oracle_decode_step.argtypes = (
         [ctypes.c_int] * 6 + [vp, vp, vp, vp, vp, vp, vp, i64, i64, dbl, dbl, vp, vp])
@@ -101,23 +103,25 @@ def _gate_strides(gate: np.ndarray, B: int, H: int, N: int):
     raise ValueError(f"gate must be [H] or [B,H,N], got {gate.shape}")
 
 
-def ws_width(k: int, pi: int, L=None) -> int:
+def ws_width(k: int, pi: int, L=None, causal: bool = True) -> int:
     L = L or lib()
-    return int(L.oracle_ws_width(k, pi))
+    return int(L.oracle_ws_width(k, pi, int(bool(causal))))
 
 
-def index_set(n: int, k: int, pi: int, L=None) -> np.ndarray:
+def index_set(n: int, k: int, pi: int, L=None, causal: bool = True) -> np.ndarray:
     """W_t for t in [0, n) as an [n, m] int32 array in slot order (see pi_oracle.c)."""
     L = L or lib()
-    m = ws_width(k, pi, L)
+    m = ws_width(k, pi, L, causal)
     idx = np.empty((n, m), dtype=np.int32)
-    L.oracle_index_set(n, k, pi, _ptr(idx))
+    L.oracle_index_set(n, k, pi, int(bool(causal)), _ptr(idx))
     return idx
 
 
 def forward(q, k_, v, gate, k: int, pi: int, scale: float | None = None,
-            clamp: float = 0.0, rows=None, want_lse=False, want_probs=False, L=None):
-    """Oracle forward over q, k, v [B,H,N,D] with gate logits [H] or [B,H,N].
+            clamp: float = 0.0, rows=None, want_lse=False, want_probs=False, L=None,
+            causal: bool = True):
+    """Oracle forward over q, k, v [B,H,N,D] with gate logits [H] or [B,H,N]
+    (``causal=False``: bidirectional window and both partners t -/+ pi).
 
     Returns out [B,H,N,D] float64 (or [len(rows), D] when ``rows`` lists flat
     query rows (b*H+h)*N+t), plus lse and per-slot probabilities on request.
@@ -129,7 +133,7 @@ def forward(q, k_, v, gate, k: int, pi: int, scale: float | None = None,
     gsb, gsh, gsn = _gate_strides(gate, B, H, N)
     if scale is None:
         scale = 1.0 / math.sqrt(D)
-    m = ws_width(k, pi, L)
+    m = ws_width(k, pi, L, causal)
     if rows is None:
         nr, rows_arr = B * H * N, None
         out_shape = (B, H, N, D)
@@ -143,7 +147,7 @@ def forward(q, k_, v, gate, k: int, pi: int, scale: float | None = None,
     lse = np.empty(nr, dtype=np.float64) if want_lse else None
     probs = np.empty((nr, m), dtype=np.float64) if want_probs else None
     if nr:
-        L.oracle_forward_rows(B, H, N, D, k, pi, _ptr(q), _ptr(k_), _ptr(v), _ptr(gate),
+        L.oracle_forward_rows(B, H, N, D, k, pi, int(bool(causal)), _ptr(q), _ptr(k_), _ptr(v), _ptr(gate),
                               gsb, gsh, gsn, float(scale), float(clamp),
                               _ptr(rows_arr), nr, _ptr(out), _ptr(lse), _ptr(probs))
     res = [out.reshape(out_shape)]
@@ -155,7 +159,7 @@ def forward(q, k_, v, gate, k: int, pi: int, scale: float | None = None,
 
 
 def backward(q, k_, v, gate, k: int, pi: int, dout, scale: float | None = None,
-             clamp: float = 0.0, L=None):
+             clamp: float = 0.0, L=None, causal: bool = True):
     """Oracle gradients for a loss L with dL/dy = ``dout`` [B,H,N,D].
 
     Returns (dq, dk, dv) [B,H,N,D] and dgate [B,H,N] (dL/dg of the gate logit
@@ -172,7 +176,7 @@ def backward(q, k_, v, gate, k: int, pi: int, dout, scale: float | None = None,
     dq, dk, dv = (np.empty((B, H, N, D), dtype=np.float64) for _ in range(3))
     dg = np.empty((B, H, N), dtype=np.float64)
     if B * H * N:
-        L.oracle_backward(B, H, N, D, k, pi, _ptr(q), _ptr(k_), _ptr(v), _ptr(gate), gsb, gsh, gsn,
+        L.oracle_backward(B, H, N, D, k, pi, int(bool(causal)), _ptr(q), _ptr(k_), _ptr(v), _ptr(gate), gsb, gsh, gsn,
                           float(scale), float(clamp), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg))
     return dq, dk, dv, dg
 

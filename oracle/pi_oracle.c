@@ -1,6 +1,6 @@
 /*
- * pi_oracle.c -- fp64 CPU oracle for causal pi-Attention (Variant 3,
- * adaptive fusion).  TEST INFRASTRUCTURE ONLY: the product path never links,
+ * pi_oracle.c -- fp64 CPU oracle for pi-Attention (Variant 3, adaptive
+ * fusion), causal and bidirectional.  TEST INFRASTRUCTURE ONLY: the product path never links,
  * loads or calls this file.  It shares no code with the HIP library.
  *
  * Plain, slow, obviously correct.  For every (b, h, t) it enumerates the
@@ -10,16 +10,20 @@
  * Definitions followed (pi-Attention, arXiv 2511.10696):
  *   - score z_tj = <q_t, k_j> * scale, scale = 1/sqrt(d_h)         (Sec. 3.2, eq. z)
  *   - local window N_r(t) = { j : max(0, t-k) <= j <= t }, causal,
- *     self included, so k+1 entries once t >= k                      (Sec. 3.2, eq. Nr)
- *   - long-range partner N_pi(t) = { t - pi }                        (Sec. 3.4, eq. Npi)
+ *     self included, so k+1 entries once t >= k;
+ *     N_r(t) = { j : |j - t| <= k }, bidirectional                   (Sec. 3.2, eq. Nr)
+ *   - long-range partner N_pi(t) = { t - pi } causal; bidirectional
+ *     tasks add t + pi, both priced as partners                      (Sec. 3.4, eq. Npi; App. B,
+ *                                                                      hyper-parameter table)
  *   - union U(t) = N_r(t) u N_pi(t); positions outside [0, T) are
  *     dropped (the appendix masks them to -inf)                      (eq. U; App. A, eqs. app_delta..app_out)
  *   - a partner that already lies in the window is not added twice
- *     (the appendix offset list appends -pi only if absent), so for
- *     pi <= k the set is the window alone                            (App. A, Fig. code)
+ *     (the appendix offset list appends -pi, and +pi when
+ *     bidirectional, only if absent), so for pi <= k the set is the
+ *     window alone                                                    (App. A, Fig. code)
  *   - gate: alpha = sigmoid(g), clipped alpha~ = eps + (1-2 eps) alpha,
  *     eps = 1e-4; g is the pre-sigmoid gate logit                    (Sec. 3.5 Variant 3; eq. app_gate)
- *   - prior omega = alpha~ on local keys, 1 - alpha~ on the partner   (eqs. omega, app_omega)
+ *   - prior omega = alpha~ on local keys, 1 - alpha~ on a partner     (eqs. omega, app_omega)
  *   - fused logit delta = z + log omega                              (eqs. delta_adapt, app_delta)
  *   - optional clamp of delta to [-Lc, Lc] (hyper-parameter table,
  *     App. B; not in the equations, off unless clamp > 0)
@@ -36,7 +40,7 @@
  *     the partner (eq. ddelta_da, written for the clipped gate the forward
  *     uses), dalpha~/dalpha = 1 - 2 eps, dalpha/dg = alpha (1 - alpha); the
  *     clamp cuts these paths too                                      (eqs. ddelta_da, dalpha_da; Sec. 3.5)
- * Decode step (Sec. 3.5, online working set eq. online_ws): query at
+ * Decode step (causal; Sec. 3.5, online working set eq. online_ws): query at
  * position t = len[s] attends to cache rows W_t, where row t is the new
  * key/value, which the step first writes into the cache.
  *
@@ -51,30 +55,40 @@
 
 #define ORACLE_EPS 1e-4
 
-/* Number of index slots per query: k+1 window slots, plus one partner slot
- * when the partner can lie outside the window (pi > k). */
-int oracle_ws_width(int k, int pi) { return k + 1 + (pi > k ? 1 : 0); }
+/* Window slots per query: offsets -k..0 (causal) or -k..k (bidirectional). */
+static int window_slots(int k, int causal) { return causal ? k + 1 : 2 * k + 1; }
 
-/* Working set of query t as an explicit list.  Slot s in [0, k] holds window
- * position t-k+s (window ordered by offset -k..0, as in the appendix offset
- * list); slot k+1 (present iff pi > k) holds t-pi.  Absent entries are -1.
- * Returns the number of valid entries. */
-static int working_set(int t, int n, int k, int pi, int32_t *slot)
+/* Number of index slots per query: the window slots, then one partner slot
+ * per partner (t-pi; t+pi too when bidirectional) when partners can lie
+ * outside the window (pi > k). */
+int oracle_ws_width(int k, int pi, int causal)
 {
-    int m = oracle_ws_width(k, pi), cnt = 0;
+    return window_slots(k, causal) + (pi > k ? (causal ? 1 : 2) : 0);
+}
+
+/* Working set of query t as an explicit list.  Slot s of the window holds
+ * position t-k+s (window ordered by offset, -k first, as in the appendix
+ * offset list); slot nw (present iff pi > k) holds t-pi and, bidirectional,
+ * slot nw+1 holds t+pi.  Absent entries are -1.  Returns the number of valid
+ * entries. */
+static int working_set(int t, int n, int k, int pi, int causal, int32_t *slot)
+{
+    int m = oracle_ws_width(k, pi, causal), nw = window_slots(k, causal), cnt = 0;
     for (int s = 0; s < m; ++s) slot[s] = -1;
     int lo = t - k > 0 ? t - k : 0;
-    for (int j = lo; j <= t; ++j) {
+    int hi = causal ? t : (t + k < n - 1 ? t + k : n - 1);
+    for (int j = lo; j <= hi; ++j) {
         if (j < n) { slot[j - (t - k)] = j; ++cnt; }
     }
-    if (pi > k && t - pi >= 0) { slot[k + 1] = t - pi; ++cnt; }
+    if (pi > k && t - pi >= 0) { slot[nw] = t - pi; ++cnt; }
+    if (!causal && pi > k && t + pi < n) { slot[nw + 1] = t + pi; ++cnt; }
     return cnt;
 }
 
-void oracle_index_set(int n, int k, int pi, int32_t *idx)
+void oracle_index_set(int n, int k, int pi, int causal, int32_t *idx)
 {
-    int m = oracle_ws_width(k, pi);
-    for (int t = 0; t < n; ++t) working_set(t, n, k, pi, idx + (int64_t)t * m);
+    int m = oracle_ws_width(k, pi, causal);
+    for (int t = 0; t < n; ++t) working_set(t, n, k, pi, causal, idx + (int64_t)t * m);
 }
 
 /* alpha~ = eps + (1 - 2 eps) * sigmoid(g) */
@@ -85,10 +99,11 @@ static double clipped_gate(double g)
 }
 
 /* One query against an explicit working set.  Key/value row j lives at
- * krows + j*D / vrows + j*D.  delta[m] is scratch.  Writes y[D], returns
- * lse; fills p[m] (softmax weight per slot) if p is non-null. */
+ * krows + j*D / vrows + j*D; slots below nw are window slots, the rest
+ * partners.  delta[m] is scratch.  Writes y[D], returns lse; fills p[m]
+ * (softmax weight per slot) if p is non-null. */
 static double attend(int D, const float *q, const float *krows, const float *vrows,
-                     const int32_t *slot, int m, int k, double gate_logit,
+                     const int32_t *slot, int m, int nw, double gate_logit,
                      double scale, double clamp, double *delta, double *y, double *p)
 {
     double at = clipped_gate(gate_logit);
@@ -100,7 +115,7 @@ static double attend(int D, const float *q, const float *krows, const float *vro
         double z = 0.0;
         for (int d = 0; d < D; ++d) z += (double)q[d] * (double)kj[d];
         z *= scale;
-        double dl = z + (s <= k ? log_local : log_skip);
+        double dl = z + (s < nw ? log_local : log_skip);
         if (clamp > 0.0) dl = dl < -clamp ? -clamp : (dl > clamp ? clamp : dl);
         delta[s] = dl;
         if (dl > mu) mu = dl;
@@ -123,14 +138,14 @@ static double attend(int D, const float *q, const float *krows, const float *vro
  * flat index r = (b*H + h)*N + t.  rows == NULL means every row, in order.
  * out [nrows][D]; lse [nrows] and probs [nrows][m] (softmax weight per slot,
  * 0 for absent slots) are optional (NULL). */
-void oracle_forward_rows(int B, int H, int N, int D, int k, int pi,
+void oracle_forward_rows(int B, int H, int N, int D, int k, int pi, int causal,
                          const float *q, const float *kk, const float *v,
                          const float *gate, int64_t gsb, int64_t gsh, int64_t gsn,
                          double scale, double clamp,
                          const int64_t *rows, int64_t nrows,
                          double *out, double *lse, double *probs)
 {
-    int m = oracle_ws_width(k, pi);
+    int m = oracle_ws_width(k, pi, causal), nw = window_slots(k, causal);
     if (!rows) nrows = (int64_t)B * H * N;
 #pragma omp parallel
     {
@@ -142,11 +157,11 @@ void oracle_forward_rows(int B, int H, int N, int D, int k, int pi,
             int t = (int)(r % N);
             int64_t bh = r / N;
             int h = (int)(bh % H), b = (int)(bh / H);
-            working_set(t, N, k, pi, slot);
+            working_set(t, N, k, pi, causal, slot);
             const float *kbase = kk + bh * (int64_t)N * D;
             const float *vbase = v + bh * (int64_t)N * D;
             double g = gate[b * gsb + h * gsh + (int64_t)t * gsn];
-            double l = attend(D, q + r * D, kbase, vbase, slot, m, k, g, scale, clamp,
+            double l = attend(D, q + r * D, kbase, vbase, slot, m, nw, g, scale, clamp,
                               delta, out + i * D, probs ? probs + i * m : NULL);
             if (lse) lse[i] = l;
         }
@@ -159,13 +174,13 @@ void oracle_forward_rows(int B, int H, int N, int D, int k, int pi,
  * dv [B][H][N][D] and dgate [B][H][N] (dL/dg for the gate logit as seen by
  * query t; a per-head gate's gradient is the sum over its queries).
  * Every (b, h) is independent; within one, queries are visited in order. */
-void oracle_backward(int B, int H, int N, int D, int k, int pi,
+void oracle_backward(int B, int H, int N, int D, int k, int pi, int causal,
                      const float *q, const float *kk, const float *v,
                      const float *gate, int64_t gsb, int64_t gsh, int64_t gsn,
                      double scale, double clamp, const float *dout,
                      double *dq, double *dk, double *dv, double *dgate)
 {
-    int m = oracle_ws_width(k, pi);
+    int m = oracle_ws_width(k, pi, causal), nw = window_slots(k, causal);
 #pragma omp parallel
     {
         int32_t *slot = (int32_t *)malloc(sizeof(int32_t) * (size_t)m);
@@ -183,9 +198,9 @@ void oracle_backward(int B, int H, int N, int D, int k, int pi,
             for (int64_t i = 0; i < (int64_t)N * D; ++i) dqb[i] = dkb[i] = dvb[i] = 0.0;
             for (int t = 0; t < N; ++t) {
                 const float *qt = qb + (int64_t)t * D, *gt = ob + (int64_t)t * D;
-                working_set(t, N, k, pi, slot);
+                working_set(t, N, k, pi, causal, slot);
                 double g = gate[b * gsb + h * gsh + (int64_t)t * gsn];
-                attend(D, qt, kb, vb, slot, m, k, g, scale, clamp, delta, y, p);
+                attend(D, qt, kb, vb, slot, m, nw, g, scale, clamp, delta, y, p);
                 /* dL/dalpha^ per slot and its weighted mean */
                 double mean = 0.0;
                 for (int s = 0; s < m; ++s) {
@@ -210,7 +225,7 @@ void oracle_backward(int B, int H, int N, int D, int k, int pi,
                         dkb[(int64_t)j * D + d] += scale * dd * (double)qt[d];
                         dvb[(int64_t)j * D + d] += p[s] * (double)gt[d];
                     }
-                    dgt += dd * (s <= k ? dg_local : dg_skip);
+                    dgt += dd * (s < nw ? dg_local : dg_skip);
                 }
                 dgate[bh * (int64_t)N + t] = dgt;
             }
@@ -236,7 +251,7 @@ int oracle_decode_step(int S, int H, int D, int cap, int k, int pi,
 {
     for (int s = 0; s < S; ++s)
         if (len_in[s] < 0 || len_in[s] >= cap) return -1;
-    int m = oracle_ws_width(k, pi);
+    int m = oracle_ws_width(k, pi, 1);
 #pragma omp parallel
     {
         int32_t *slot = (int32_t *)malloc(sizeof(int32_t) * (size_t)m);
@@ -251,9 +266,9 @@ int oracle_decode_step(int S, int H, int D, int cap, int k, int pi,
                 kc[(int64_t)t * D + d] = k_new[r * D + d];
                 vc[(int64_t)t * D + d] = v_new[r * D + d];
             }
-            working_set(t, t + 1, k, pi, slot);
+            working_set(t, t + 1, k, pi, 1, slot);
             double g = gate[s * gss + h * gsh];
-            double l = attend(D, q_new + r * D, kc, vc, slot, m, k, g, scale, clamp,
+            double l = attend(D, q_new + r * D, kc, vc, slot, m, k + 1, g, scale, clamp,
                               delta, out + r * D, NULL);
             if (lse) lse[r] = l;
         }

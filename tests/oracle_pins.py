@@ -24,14 +24,20 @@ EPS = json.load(open(os.path.join(GOLDEN, "defaults.json")))["eps"]
 # ---------------------------------------------------------------------------
 # independent references
 # ---------------------------------------------------------------------------
-def scan_membership(n: int, k: int, pi: int) -> np.ndarray:
+def scan_membership(n: int, k: int, pi: int, causal: bool = True) -> np.ndarray:
     """Brute-force membership scan: M[t, j] for every pair, straight from the
-    set definitions (eq. Nr causal, eq. Npi, eq. U); invalid positions dropped."""
+    set definitions (eq. Nr, eq. Npi, eq. U; bidirectional: |j - t| <= k and
+    the partners t -/+ pi, App. B hyper-parameter table); positions outside
+    the sequence are never visited."""
     M = np.zeros((n, n), dtype=bool)
     for t in range(n):
         for j in range(n):
-            in_window = max(0, t - k) <= j <= t
-            is_partner = j == t - pi
+            if causal:
+                in_window = max(0, t - k) <= j <= t
+                is_partner = j == t - pi
+            else:
+                in_window = abs(j - t) <= k
+                is_partner = j == t - pi or j == t + pi
             M[t, j] = in_window or is_partner
     return M
 
@@ -40,12 +46,14 @@ def rand_qkv(rng, B, H, N, D, dtype=np.float32):
     return [rng.standard_normal((B, H, N, D)).astype(dtype) for _ in range(3)]
 
 
-def textbook_causal(q, k, v, scale):
-    """Dense causal scaled-dot-product attention (eqs. alpha and attn), fp64."""
+def textbook_causal(q, k, v, scale, causal=True):
+    """Dense scaled-dot-product attention (eqs. alpha and attn), causal or
+    over every position, fp64."""
     q, k, v = (np.asarray(x, np.float64) for x in (q, k, v))
     N = q.shape[-2]
     S = (q @ np.swapaxes(k, -1, -2)) * scale
-    S = np.where(np.tril(np.ones((N, N), bool)), S, -np.inf)
+    if causal:
+        S = np.where(np.tril(np.ones((N, N), bool)), S, -np.inf)
     S = S - S.max(-1, keepdims=True)
     P = np.exp(S)
     P /= P.sum(-1, keepdims=True)
@@ -58,16 +66,16 @@ def logsumexp_masked(S, M):
     return (mx + np.log(np.exp(S - mx).sum(-1, keepdims=True)))[..., 0]
 
 
-def multiplicative_fusion(q, k, v, gate, kk, pi, scale):
+def multiplicative_fusion(q, k, v, gate, kk, pi, scale, causal=True):
     """eq. (alphahat_adapt) in its multiplicative form: weights
     omega_tj * exp(z_tj) normalised over U(t), omega = alpha~ on the window and
-    1 - alpha~ on the partner; mask from the brute-force scan.  fp64, dense."""
+    1 - alpha~ on a partner; mask from the brute-force scan.  fp64, dense."""
     q, k, v = (np.asarray(x, np.float64) for x in (q, k, v))
     B, H, N, D = q.shape
-    M = scan_membership(N, kk, pi)
+    M = scan_membership(N, kk, pi, causal)
     window = np.zeros((N, N), bool)
     for t in range(N):
-        window[t, max(0, t - kk):t + 1] = True
+        window[t, max(0, t - kk):(t + 1 if causal else t + kk + 1)] = True
     g = np.asarray(gate, np.float64)
     g = np.broadcast_to(g[None, :, None] if g.shape == (H,) else g, (B, H, N))
     a_t = EPS + (1 - 2 * EPS) / (1 + np.exp(-g))           # [B,H,N]
@@ -337,10 +345,148 @@ def pin_clamp_reading(L):
             assert np.abs(big[0, h, t] - w @ v[0, h, js[js >= 0]].astype(np.float64)).max() <= 1e-12
 
 
+# ---------------------------------------------------------------------------
+# bidirectional mode (eq. Nr bidirectional case; partners t -/+ pi)
+# ---------------------------------------------------------------------------
+BIDIR_IDX_CASES = [(1, 0, 0), (1, 3, 5), (7, 0, 1), (9, 2, 5), (16, 3, 3), (16, 3, 4), (20, 4, 16),
+                   (33, 5, 0), (40, 50, 7), (40, 6, 39), (40, 6, 40), (64, 8, 16), (12, 2, 11)]
+
+
+def pin_bidir_index_set_scan(L):
+    """Bidirectional working sets equal the brute-force scan; slot order is
+    window offsets -k..k, then t - pi, then t + pi (App. A offset list)."""
+    for n, k, pi in BIDIR_IDX_CASES:
+        idx = oracle.index_set(n, k, pi, L, causal=False)
+        m = 2 * k + 1 + (2 if pi > k else 0)
+        assert idx.shape == (n, m), (n, k, pi, idx.shape)
+        M = scan_membership(n, k, pi, causal=False)
+        for t in range(n):
+            got = idx[t][idx[t] >= 0]
+            assert len(set(got.tolist())) == len(got), "duplicate entry"
+            assert sorted(got.tolist()) == np.nonzero(M[t])[0].tolist(), (n, k, pi, t)
+            for s in range(2 * k + 1):
+                j = t - k + s
+                assert idx[t, s] == (j if 0 <= j < n else -1)
+            if pi > k:
+                assert idx[t, 2 * k + 1] == (t - pi if t >= pi else -1)
+                assert idx[t, 2 * k + 2] == (t + pi if t + pi < n else -1)
+
+
+def pin_bidir_working_set_sizes(L):
+    """sum_t |W_t| in closed form: window n(2k+1) - k(k+1) for n > k (n^2
+    otherwise), plus 2 max(0, n - pi) partners when pi > k."""
+    for n, k, pi in [(256, 32, 64), (4096, 128, 256), (1000, 7, 3), (300, 299, 500), (50, 60, 70)]:
+        idx = oracle.index_set(n, k, pi, L, causal=False)
+        total = int((idx >= 0).sum())
+        closed = n * (2 * k + 1) - k * (k + 1) if n > k else n * n
+        closed += 2 * max(0, n - pi) if pi > k else 0
+        assert total == closed, (n, k, pi, total, closed)
+
+
+def pin_bidir_dense_reduction(L):
+    """k >= N-1, bidirectional: every position is in the window, the prior
+    cancels, and the result is dense (unmasked) softmax attention (eqs. alpha,
+    attn) for any gate; lse = log alpha~ + logsumexp(z) over all positions."""
+    rng = np.random.default_rng(31)
+    B, H, N, D = 2, 2, 29, 16
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    gate = rng.uniform(-3, 3, (B, H, N)).astype(np.float32)
+    scale = 1 / math.sqrt(D)
+    ref = textbook_causal(q, k, v, scale, causal=False)
+    S = (q.astype(np.float64) @ np.swapaxes(k, -1, -2).astype(np.float64)) * scale
+    a_t = EPS + (1 - 2 * EPS) / (1 + np.exp(-gate.astype(np.float64)))
+    lse_ref = np.log(a_t) + logsumexp_masked(S, np.ones((N, N), bool))
+    for kk, pi in [(N - 1, 5), (N + 10, 0), (N - 1, N + 3)]:
+        out, lse = oracle.forward(q, k, v, gate, kk, pi, want_lse=True, L=L, causal=False)
+        assert np.abs(out - ref).max() <= 1e-12, (kk, pi, np.abs(out - ref).max())
+        assert np.abs(lse - lse_ref).max() <= 1e-12
+
+
+def pin_bidir_local_reduction(L):
+    """pi <= k, bidirectional: both partners lie in the window, so the result is
+    plain bidirectional sliding-window attention, independent of the gate."""
+    rng = np.random.default_rng(32)
+    B, H, N, D = 1, 2, 40, 8
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    kk = 5
+    M = np.abs(np.arange(N)[:, None] - np.arange(N)[None, :]) <= kk
+    S = (q.astype(np.float64) @ np.swapaxes(k, -1, -2).astype(np.float64)) / math.sqrt(D)
+    S = np.where(M, S, -np.inf)
+    P = np.exp(S - S.max(-1, keepdims=True))
+    P /= P.sum(-1, keepdims=True)
+    ref = P @ v.astype(np.float64)
+    for pi in (0, 1, 3, kk):
+        for g in (-4.0, 0.0, 2.5):
+            out = oracle.forward(q, k, v, np.full(H, g, np.float32), kk, pi, L=L, causal=False)
+            assert np.abs(out - ref).max() <= 1e-12, (pi, g)
+
+
+def pin_bidir_multiplicative_form(L):
+    """Bidirectional adaptive fusion equals the multiplicative form of eq.
+    (alphahat_adapt) with both partners priced 1 - alpha~; g = 0 reduces it to
+    the basic union softmax (eqs. alpha_u, beta)."""
+    rng = np.random.default_rng(33)
+    B, H, N, D = 2, 2, 45, 8
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    for kk, pi in [(3, 9), (6, 7), (2, 20), (4, 44)]:
+        for gate in (rng.uniform(-2, 2, H).astype(np.float32),
+                     rng.uniform(-4, 4, (B, H, N)).astype(np.float32), np.zeros(H, np.float32)):
+            ref, W = multiplicative_fusion(q, k, v, gate, kk, pi, 1 / math.sqrt(D), causal=False)
+            out, P = oracle.forward(q, k, v, gate, kk, pi, want_probs=True, L=L, causal=False)
+            assert np.abs(out - ref).max() <= 1e-12, (kk, pi, np.abs(out - ref).max())
+            idx = oracle.index_set(N, kk, pi, L, causal=False)
+            for t in (0, 1, kk, pi, N - 1 - pi, N - 1):
+                if not 0 <= t < N:
+                    continue
+                for s in range(idx.shape[1]):
+                    j = idx[t, s]
+                    want = W[:, :, t, j] if j >= 0 else 0.0
+                    assert np.abs(P[:, :, t, s] - want).max() <= 1e-12
+
+
+def pin_bidir_time_reversal(L):
+    """Reversing the sequence (q, k, v and a per-query gate) reverses the
+    bidirectional output: the window is symmetric and the partners t -/+ pi
+    trade places."""
+    rng = np.random.default_rng(34)
+    B, H, N, D = 1, 3, 37, 8
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    gate = rng.uniform(-2, 2, (B, H, N)).astype(np.float32)
+    for kk, pi in [(2, 7), (4, 30), (3, 3), (0, 1)]:
+        out = oracle.forward(q, k, v, gate, kk, pi, L=L, causal=False)
+        rev = oracle.forward(q[:, :, ::-1], k[:, :, ::-1], v[:, :, ::-1], gate[:, :, ::-1], kk, pi,
+                             L=L, causal=False)
+        assert np.abs(rev[:, :, ::-1] - out).max() <= 1e-12, (kk, pi)
+
+
+def pin_bidir_gate_limits(L):
+    """g -> +inf: each partner's weight relative to the self entry tends to
+    eps/(1-eps) exp(z_p - z_t); g -> -inf: (1-eps)/eps exp(z_p - z_t)."""
+    rng = np.random.default_rng(35)
+    B, H, N, D = 1, 2, 30, 8
+    q, k, v = rand_qkv(rng, B, H, N, D)
+    kk, pi = 3, 10
+    gate = np.array([60.0, -60.0], np.float32)
+    _, P = oracle.forward(q, k, v, gate, kk, pi, want_probs=True, L=L, causal=False)
+    q64, k64 = q.astype(np.float64), k.astype(np.float64)
+    for t in range(N):
+        for h, ratio in ((0, EPS / (1 - EPS)), (1, (1 - EPS) / EPS)):
+            zs = q64[0, h, t] @ k64[0, h, t] / math.sqrt(D)
+            for slot, j in ((2 * kk + 1, t - pi), (2 * kk + 2, t + pi)):
+                if not 0 <= j < N:
+                    assert P[0, h, t, slot] == 0.0
+                    continue
+                zp = q64[0, h, t] @ k64[0, h, j] / math.sqrt(D)
+                got = P[0, h, t, slot] / P[0, h, t, kk]
+                assert abs(got / (ratio * math.exp(zp - zs)) - 1) <= 1e-9, (t, h, j)
+
+
 ALL_PINS = [pin_index_set_scan, pin_working_set_sizes, pin_dense_reduction, pin_local_reduction,
             pin_basic_union_g0, pin_multiplicative_form, pin_gate_limits, pin_sum_to_one_and_row0,
             pin_causality, pin_head_batch_independence, pin_decode_matches_last_row,
-            pin_clamp_reading]
+            pin_clamp_reading, pin_bidir_index_set_scan, pin_bidir_working_set_sizes,
+            pin_bidir_dense_reduction, pin_bidir_local_reduction, pin_bidir_multiplicative_form,
+            pin_bidir_time_reversal, pin_bidir_gate_limits]
 
 
 def pin_reachability(L):
@@ -368,12 +514,12 @@ ALL_PINS.append(pin_reachability)
 # ---------------------------------------------------------------------------
 # backward pins
 # ---------------------------------------------------------------------------
-def _loss(L, q, k, v, gate, kk, pi, dout, clamp=0.0):
-    y = oracle.forward(q, k, v, gate, kk, pi, clamp=clamp, L=L)
+def _loss(L, q, k, v, gate, kk, pi, dout, clamp=0.0, causal=True):
+    y = oracle.forward(q, k, v, gate, kk, pi, clamp=clamp, L=L, causal=causal)
     return float(np.sum(y * np.asarray(dout, np.float64)))
 
 
-def _central_difference(L, arrays, which, idx, h, kk, pi, dout, clamp=0.0):
+def _central_difference(L, arrays, which, idx, h, kk, pi, dout, clamp=0.0, causal=True):
     """d loss / d arrays[which][idx] by a central difference whose two steps
     are the exact float32 increments actually applied (the oracle takes
     float32 inputs)."""
@@ -383,37 +529,38 @@ def _central_difference(L, arrays, which, idx, h, kk, pi, dout, clamp=0.0):
     a, b = float(up) - float(base), float(base) - float(dn)
     xs = [arr.copy() for arr in arrays]
     xs[which][idx] = up
-    f_up = _loss(L, *xs, kk, pi, dout, clamp)
+    f_up = _loss(L, *xs, kk, pi, dout, clamp, causal)
     xs[which][idx] = dn
-    f_dn = _loss(L, *xs, kk, pi, dout, clamp)
+    f_dn = _loss(L, *xs, kk, pi, dout, clamp, causal)
     return (f_up - f_dn) / (a + b)
 
 
 def pin_backward_finite_differences(L):
     """The oracle gradients (Sec. 3.5 eqs. jac, ddelta_da, dalpha_da) equal
     central differences of the oracle's own forward, for q, k, v and the gate
-    logit, with the partner inside and outside the window and with per-head
-    and per-query gates."""
+    logit, with the partner inside and outside the window, with per-head
+    and per-query gates, causal and bidirectional."""
     rng = np.random.default_rng(11)
-    for (B, H, N, D, kk, pi, per_query) in [(1, 2, 24, 8, 4, 8, False), (2, 1, 20, 8, 3, 3, True),
-                                            (1, 1, 17, 16, 2, 5, True)]:
+    for (B, H, N, D, kk, pi, per_query, causal) in [
+            (1, 2, 24, 8, 4, 8, False, True), (2, 1, 20, 8, 3, 3, True, True), (1, 1, 17, 16, 2, 5, True, True),
+            (1, 2, 22, 8, 3, 7, True, False), (1, 1, 15, 8, 2, 2, False, False)]:
         q, k, v = rand_qkv(rng, B, H, N, D)
         gate = (rng.uniform(-1, 1, (B, H, N)) if per_query else rng.uniform(-1, 1, H)).astype(np.float32)
         dout = rng.standard_normal((B, H, N, D)).astype(np.float32)
-        dq, dk, dv, dg = oracle.backward(q, k, v, gate, kk, pi, dout, L=L)
+        dq, dk, dv, dg = oracle.backward(q, k, v, gate, kk, pi, dout, L=L, causal=causal)
         grads = [dq, dk, dv]
         arrays = [q, k, v, gate]
         for which in range(4):
             for _ in range(6 if which < 3 else 4):
                 idx = tuple(int(rng.integers(0, n)) for n in arrays[which].shape)
-                fd = _central_difference(L, arrays, which, idx, 2.0 ** -8, kk, pi, dout)
+                fd = _central_difference(L, arrays, which, idx, 2.0 ** -8, kk, pi, dout, causal=causal)
                 if which < 3:
                     an = grads[which][idx]
                 elif per_query:
                     an = dg[idx]
                 else:  # a per-head gate collects the gradient of every query of head h
                     an = dg[:, idx[0], :].sum()
-                assert abs(fd - an) <= 5e-5 + 1e-3 * abs(an), (B, H, N, D, kk, pi, which, idx, fd, an)
+                assert abs(fd - an) <= 5e-5 + 1e-3 * abs(an), (B, H, N, D, kk, pi, causal, which, idx, fd, an)
 
 
 def pin_backward_dense_reduction(L):
@@ -428,15 +575,17 @@ def pin_backward_dense_reduction(L):
     gate = rng.uniform(-2, 2, H).astype(np.float32)
     dout = rng.standard_normal((B, H, N, D)).astype(np.float32)
     scale = 1.0 / math.sqrt(D)
-    dq, dk, dv, dg = oracle.backward(q, k, v, gate, N - 1, 0, dout, L=L)
-    tq, tk, tv = (torch.tensor(x, dtype=torch.float64, requires_grad=True) for x in (q, k, v))
-    S = (tq @ tk.transpose(-1, -2)) * scale
-    S = S.masked_fill(~torch.tril(torch.ones(N, N, dtype=torch.bool)), float("-inf"))
-    y = torch.softmax(S, dim=-1) @ tv
-    y.backward(torch.tensor(dout, dtype=torch.float64))
-    for got, ref in ((dq, tq.grad), (dk, tk.grad), (dv, tv.grad)):
-        assert np.allclose(got, ref.numpy(), rtol=1e-10, atol=1e-12)
-    assert np.abs(dg).max() < 1e-12
+    for causal in (True, False):   # bidirectional: no mask at all
+        dq, dk, dv, dg = oracle.backward(q, k, v, gate, N - 1, 0, dout, L=L, causal=causal)
+        tq, tk, tv = (torch.tensor(x, dtype=torch.float64, requires_grad=True) for x in (q, k, v))
+        S = (tq @ tk.transpose(-1, -2)) * scale
+        if causal:
+            S = S.masked_fill(~torch.tril(torch.ones(N, N, dtype=torch.bool)), float("-inf"))
+        y = torch.softmax(S, dim=-1) @ tv
+        y.backward(torch.tensor(dout, dtype=torch.float64))
+        for got, ref in ((dq, tq.grad), (dk, tk.grad), (dv, tv.grad)):
+            assert np.allclose(got, ref.numpy(), rtol=1e-10, atol=1e-12), causal
+        assert np.abs(dg).max() < 1e-12
 
 
 def pin_backward_clamp_limits(L):

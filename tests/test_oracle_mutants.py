@@ -14,18 +14,26 @@ from tests import oracle_pins as P
 SRC = os.path.join(os.path.dirname(oracle.__file__), "pi_oracle.c")
 
 MUTANTS = {
-    "prior_dropped": [("double dl = z + (s <= k ? log_local : log_skip);", "double dl = z;")],
-    "priors_swapped": [("(s <= k ? log_local : log_skip)", "(s <= k ? log_skip : log_local)")],
+    "prior_dropped": [("double dl = z + (s < nw ? log_local : log_skip);", "double dl = z;")],
+    "priors_swapped": [("(s < nw ? log_local : log_skip)", "(s < nw ? log_skip : log_local)")],
     "skip_prior_sign": [("log_skip = log1p(-at);", "log_skip = -log1p(-at);")],
     "eps_clip_dropped": [("return ORACLE_EPS + (1.0 - 2.0 * ORACLE_EPS) * a;", "return a;")],
     "sigmoid_sign": [("double a = 1.0 / (1.0 + exp(-g));", "double a = 1.0 / (1.0 + exp(g));")],
     "scale_dropped": [("z *= scale;", ";")],
     "window_short_by_one": [("int lo = t - k > 0 ? t - k : 0;", "int lo = t - k + 1 > 0 ? t - k + 1 : 0;")],
-    "partner_off_by_one": [("slot[k + 1] = t - pi; ++cnt;", "slot[k + 1] = t - pi + 1; ++cnt;")],
+    "partner_off_by_one": [("slot[nw] = t - pi; ++cnt;", "slot[nw] = t - pi + 1; ++cnt;")],
     "partner_not_deduplicated": [
-        ("int oracle_ws_width(int k, int pi) { return k + 1 + (pi > k ? 1 : 0); }",
-         "int oracle_ws_width(int k, int pi) { return k + 1 + (pi > 0 ? 1 : 0); }"),
-        ("if (pi > k && t - pi >= 0)", "if (pi > 0 && t - pi >= 0)")],
+        ("return window_slots(k, causal) + (pi > k ? (causal ? 1 : 2) : 0);",
+         "return window_slots(k, causal) + (pi > 0 ? (causal ? 1 : 2) : 0);"),
+        ("if (pi > k && t - pi >= 0)", "if (pi > 0 && t - pi >= 0)"),
+        ("if (!causal && pi > k && t + pi < n)", "if (!causal && pi > 0 && t + pi < n)")],
+    # bidirectional mode
+    "bidir_forward_partner_dropped": [("if (!causal && pi > k && t + pi < n) { slot[nw + 1] = t + pi; ++cnt; }", ";")],
+    "bidir_window_left_only": [("int hi = causal ? t : (t + k < n - 1 ? t + k : n - 1);", "int hi = t;")],
+    "bidir_window_right_short": [("int hi = causal ? t : (t + k < n - 1 ? t + k : n - 1);",
+                                  "int hi = causal ? t : (t + k - 1 < n - 1 ? t + k - 1 : n - 1);")],
+    "bidir_forward_partner_local_prior": [("(s < nw ? log_local : log_skip)", "(s < nw || s == nw + 1 ? log_local : log_skip)")],
+    "bidir_forward_partner_mirrored": [("slot[nw + 1] = t + pi;", "slot[nw + 1] = t - pi;")],
     "keys_values_swapped": [("const float *kj = krows + (int64_t)slot[s] * D;",
                              "const float *kj = vrows + (int64_t)slot[s] * D;")],
     "values_from_keys": [("const float *vj = vrows + (int64_t)slot[s] * D;",
@@ -49,7 +57,9 @@ MUTANTS = {
          "double dg_local = (1.0 - 2.0 * ORACLE_EPS) / at;"),
         ("double dg_skip = -(1.0 - 2.0 * ORACLE_EPS) * a * (1.0 - a) / (1.0 - at);",
          "double dg_skip = -(1.0 - 2.0 * ORACLE_EPS) / (1.0 - at);")],
-    "bwd_gate_priors_swapped": [("dgt += dd * (s <= k ? dg_local : dg_skip);", "dgt += dd * (s <= k ? dg_skip : dg_local);")],
+    "bwd_gate_priors_swapped": [("dgt += dd * (s < nw ? dg_local : dg_skip);", "dgt += dd * (s < nw ? dg_skip : dg_local);")],
+    "bwd_bidir_gate_partner_as_local": [("dgt += dd * (s < nw ? dg_local : dg_skip);",
+                                         "dgt += dd * (s < nw || s == nw + 1 ? dg_local : dg_skip);")],
     "bwd_clamp_not_cut": [("if (clamp > 0.0 && fabs(delta[s]) >= clamp) dd = 0.0;", ";")],
 }
 
