@@ -1,18 +1,23 @@
 /*
  * pi_attn.h -- C ABI of the MI355X (gfx950) pi-Attention operator.
  *
- * pi-Attention (arXiv 2511.10696) evaluates causal attention of query t on
- * the online working set W_t = N_r(t) u N_pi(t) (Sec. 3.5, eq. online_ws):
+ * pi-Attention (arXiv 2511.10696) evaluates attention of query t on the
+ * online working set W_t = N_r(t) u N_pi(t) (Sec. 3.5, eq. online_ws).
+ * Causal mode (causal != 0):
  *   - the local window N_r(t) = { j : max(0, t-k) <= j <= t }, radius k,
  *     self included (Sec. 3.2, eq. Nr, causal case);
  *   - the long-range partner N_pi(t) = { t - pi } (Sec. 3.4, eq. Npi), kept
  *     only when it lies in [0, t] and outside the window (pi > k; a partner
  *     inside the window is not counted twice, App. A offset list).
+ * Bidirectional mode (causal == 0; App. B hyper-parameter table):
+ *   - the window N_r(t) = { j : |j - t| <= k } (eq. Nr, bidirectional case);
+ *   - the partners t - pi and t + pi, each kept when it lies in [0, N) and
+ *     pi > k, both priced as partners.
  * Adaptive fusion (Sec. 3.5 Variant 3, eqs. gate..attn_adapt; App. A eqs.
  * app_gate..app_out): with gate logit g (pre-sigmoid),
  *   alpha~ = eps + (1 - 2 eps) * sigmoid(g),  eps = 1e-4,
  *   delta_tj = scale * <q_t, k_j> + log(alpha~)      for j in the window,
- *   delta_tj = scale * <q_t, k_j> + log(1 - alpha~)  for the partner,
+ *   delta_tj = scale * <q_t, k_j> + log(1 - alpha~)  for a partner,
  *   y_t = sum_j softmax_j(delta_t) v_j                 (one shared softmax).
  * scale is 1/sqrt(D) in the paper (Sec. 3.2, eq. z); it is an argument here.
  *
@@ -55,30 +60,36 @@ enum {
 /* Human-readable text for a status code (static storage, never NULL). */
 const char *pi_attn_strerror(int status);
 
-/* Slots per query in the index-set layout: k+1 window slots, plus one
- * partner slot iff pi > k.  Returns -1 for k < 0 or pi < 0. */
-int32_t pi_attn_ws_width(int32_t k, int32_t pi);
+/* Slots per query in the index-set layout: causal, k+1 window slots plus one
+ * partner slot iff pi > k; bidirectional, 2k+1 window slots plus two
+ * partner slots iff pi > k.  Returns -1 for k < 0, pi < 0 or a width beyond
+ * int32. */
+int32_t pi_attn_ws_width(int32_t k, int32_t pi, int32_t causal);
 
 /*
- * pi_attn_index_set -- the working sets W_t of a length-n causal sequence
+ * pi_attn_index_set -- the working sets W_t of a length-n sequence
  * (Sec. 3.2 eq. Nr; Sec. 3.4 eqs. U, Npi; App. A offset list).
- *   idx   device int32 [n][m], m = pi_attn_ws_width(k, pi), written fully:
- *         idx[t*m + s] = t - k + s for s in [0, k] (window offsets -k..0),
- *         idx[t*m + k + 1] = t - pi (only when pi > k),
- *         and -1 wherever that position is < 0.
+ *   causal  non-zero: causal mode; zero: bidirectional mode.
+ *   idx     device int32 [n][m], m = pi_attn_ws_width(k, pi, causal),
+ *           written fully, with w = k+1 (causal) or 2k+1 (bidirectional):
+ *           idx[t*m + s] = t - k + s for s in [0, w) (window offsets from -k),
+ *           idx[t*m + w] = t - pi and, bidirectional, idx[t*m + w + 1] = t + pi
+ *           (only when pi > k), and -1 wherever that position is outside
+ *           [0, n).
  *   Errors: EINVAL for n < 0, k < 0, pi < 0, idx == NULL with n > 0, or
  *   n*m beyond 2^31 entries.
  */
-int pi_attn_index_set(int32_t n, int32_t k, int32_t pi, int32_t *idx, void *stream);
+int pi_attn_index_set(int32_t n, int32_t k, int32_t pi, int32_t causal, int32_t *idx, void *stream);
 
 /*
- * pi_attn_forward -- full-sequence causal pi-Attention with adaptive fusion
+ * pi_attn_forward -- full-sequence pi-Attention with adaptive fusion
  * (Sec. 3.5 Variant 3; App. A eqs. app_gate..app_out).
  *   dtype        PI_ATTN_F32 or PI_ATTN_BF16: element type of q, k, v and out.
  *   B, H, N, D   batch, heads, sequence length, head dimension.
  *   k, pi        window radius (k >= 0) and partner period (pi >= 0; pi <= k
  *                means no separate partner, i.e. sliding-window attention;
- *                k >= N-1 is dense causal attention).
+ *                k >= N-1 is dense attention).
+ *   causal       non-zero: causal mode; zero: bidirectional mode.
  *   q, kk, v     device [B][H][N][D] through element strides (sb, sh, sn)
  *                shared by the three tensors; the D elements are contiguous.
  *   gate         device float32 pre-sigmoid gate logits g, read at
@@ -93,10 +104,11 @@ int pi_attn_index_set(int32_t n, int32_t k, int32_t pi, int32_t *idx, void *stre
  *                sum over W_t of exp(delta), or NULL.
  * Errors: EINVAL (null pointer with non-empty problem, negative size or
  * stride, misalignment), EUNSUPPORTED (D not 64/128, unknown dtype; for
- * bf16, (min(k, N) + 256) * sn * 2 bytes >= 2 GiB), EHIP (launch refused).
+ * bf16, (c * min(k, N) + 256) * sn * 2 bytes >= 2 GiB, c = 1 causal and 2
+ * bidirectional), EHIP (launch refused).
  */
 int pi_attn_forward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D,
-                    int32_t k, int32_t pi,
+                    int32_t k, int32_t pi, int32_t causal,
                     const void *q, const void *kk, const void *v,
                     int64_t sb, int64_t sh, int64_t sn,
                     const float *gate, int64_t gsb, int64_t gsh, int64_t gsn,
@@ -106,7 +118,7 @@ int pi_attn_forward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D,
 
 /*
  * pi_attn_decode_step -- one KV-cached decode step of the online operator
- * (Sec. 3.5, eq. online_ws): for each sequence s and head h, with
+ * (causal mode; Sec. 3.5, eq. online_ws): for each sequence s and head h, with
  * t = len_in[s], first store the new key/value as cache row t, then attend
  * the new query over W_t (window rows max(0,t-k)..t, partner row t-pi when
  * pi > k and t >= pi).
@@ -140,7 +152,8 @@ int pi_attn_decode_step(int32_t dtype, int32_t S, int32_t H, int32_t D, int32_t 
  * given dL/dy (the softmax Jacobian on the fused logits, Sec. 3.5 eq. jac;
  * the prior derivatives for the clipped gate, eqs. ddelta_da and dalpha_da;
  * the same W_t, scale, gate and clamp as pi_attn_forward).
- *   dtype ... logit_clamp   exactly as passed to pi_attn_forward.
+ *   dtype ... logit_clamp   exactly as passed to pi_attn_forward (causal
+ *                included).
  *   lse          device float32 [B][H][N] contiguous: the lse that
  *                pi_attn_forward wrote for these inputs (the weights are
  *                recomputed as exp(delta - lse)).
@@ -163,7 +176,7 @@ int pi_attn_decode_step(int32_t dtype, int32_t S, int32_t H, int32_t D, int32_t 
  * out, dout, dq, dk, dv, dgate or rowterm.
  */
 int pi_attn_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D,
-                     int32_t k, int32_t pi,
+                     int32_t k, int32_t pi, int32_t causal,
                      const void *q, const void *kk, const void *v,
                      int64_t sb, int64_t sh, int64_t sn,
                      const float *gate, int64_t gsb, int64_t gsh, int64_t gsn,

@@ -5,9 +5,11 @@ HIP stream) into the C ABI declared in ``include/pi_attn.h``; every step of
 the operator runs in the library's HIP kernels.  There is no fallback: if the
 library is missing or the tensors are not on the GPU, the calls raise.
 
-Entry points (same names as the C ABI):
-    pi_attn_index_set(n, k, pi)                      -> int32 [n, m] (device)
-    pi_attn_forward(q, k, v, gate, k_window, pi)     -> out [B,H,N,D] (and lse)
+Entry points (same names as the C ABI; ``causal=False`` selects the
+bidirectional mode, window |j - t| <= k and partners t -/+ pi):
+    pi_attn_index_set(n, k, pi, causal=True)                  -> int32 [n, m] (device)
+    pi_attn_forward(q, k, v, gate, k_window, pi, causal=True) -> out [B,H,N,D] (and lse)
+    pi_attn_backward(q, k, v, gate, k_window, pi, out, lse, dout, causal=True)
     pi_attn_decode_step(len_in, q_new, k_new, v_new, k_cache, v_cache, gate, k, pi)
 """
 from __future__ import annotations
@@ -47,17 +49,17 @@ def library() -> ctypes.CDLL:
             i32, i64, f32, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
             lib.pi_attn_strerror.argtypes = [ctypes.c_int]
             lib.pi_attn_strerror.restype = ctypes.c_char_p
-            lib.pi_attn_ws_width.argtypes = [i32, i32]
+            lib.pi_attn_ws_width.argtypes = [i32, i32, i32]
             lib.pi_attn_ws_width.restype = i32
-            lib.pi_attn_index_set.argtypes = [i32, i32, i32, vp, vp]
+            lib.pi_attn_index_set.argtypes = [i32, i32, i32, i32, vp, vp]
             lib.pi_attn_index_set.restype = ctypes.c_int
-            lib.pi_attn_forward.argtypes = ([i32] * 7 + [vp, vp, vp, i64, i64, i64, vp, i64, i64, i64,
+            lib.pi_attn_forward.argtypes = ([i32] * 8 + [vp, vp, vp, i64, i64, i64, vp, i64, i64, i64,
                                                         f32, f32, vp, i64, i64, i64, vp, vp])
             lib.pi_attn_forward.restype = ctypes.c_int
             lib.pi_attn_decode_step.argtypes = ([i32] * 7 + [vp, vp, vp, vp, vp, vp, vp, vp, i64, i64,
                                                             f32, f32, vp, vp, vp])
             lib.pi_attn_decode_step.restype = ctypes.c_int
-            lib.pi_attn_backward.argtypes = ([i32] * 7 + [vp, vp, vp, i64, i64, i64, vp, i64, i64, i64,
+            lib.pi_attn_backward.argtypes = ([i32] * 8 + [vp, vp, vp, i64, i64, i64, vp, i64, i64, i64,
                                                          f32, f32, vp, vp, vp, i64, i64, i64,
                                                          vp, vp, vp, vp, vp, vp])
             lib.pi_attn_backward.restype = ctypes.c_int
@@ -69,8 +71,8 @@ def pi_attn_strerror(status: int) -> str:
     return library().pi_attn_strerror(int(status)).decode()
 
 
-def pi_attn_ws_width(k: int, pi: int) -> int:
-    return int(library().pi_attn_ws_width(int(k), int(pi)))
+def pi_attn_ws_width(k: int, pi: int, causal: bool = True) -> int:
+    return int(library().pi_attn_ws_width(int(k), int(pi), int(bool(causal))))
 
 
 def _torch():
@@ -109,11 +111,12 @@ def _check(status: int, where: str):
         raise PiAttnError(status, where)
 
 
-def pi_attn_index_set(n: int, k: int, pi: int, out=None, device=None, stream=None):
-    """W_t for t in [0, n) as a device int32 tensor [n, m] (m = pi_attn_ws_width(k, pi)):
-    columns 0..k hold t-k..t, column k+1 (present iff pi > k) holds t-pi, -1 where < 0."""
+def pi_attn_index_set(n: int, k: int, pi: int, out=None, device=None, stream=None, causal: bool = True):
+    """W_t for t in [0, n) as a device int32 tensor [n, m] (m = pi_attn_ws_width(k, pi, causal)):
+    window columns hold t-k.. (k+1 causal, 2k+1 bidirectional), then t-pi and
+    (bidirectional) t+pi when pi > k; -1 outside [0, n)."""
     torch = _torch()
-    m = pi_attn_ws_width(k, pi)
+    m = pi_attn_ws_width(k, pi, causal)
     if m < 0:
         raise PiAttnError(-1, "pi_attn_index_set")
     if out is None:
@@ -121,14 +124,15 @@ def pi_attn_index_set(n: int, k: int, pi: int, out=None, device=None, stream=Non
     _require_cuda(out)
     if out.dtype != torch.int32 or tuple(out.shape) != (n, m) or not out.is_contiguous():
         raise ValueError(f"out must be a contiguous int32 tensor of shape {(n, m)}")
-    _check(library().pi_attn_index_set(n, k, pi, _ptr(out), _stream_handle(stream, out.device)),
+    _check(library().pi_attn_index_set(n, k, pi, int(bool(causal)), _ptr(out), _stream_handle(stream, out.device)),
            "pi_attn_index_set")
     return out
 
 
 def pi_attn_forward(q, k, v, gate, k_window: int, pi: int, scale: float | None = None,
-                    logit_clamp: float = 0.0, out=None, return_lse: bool = False, lse=None, stream=None):
-    """Causal pi-Attention forward.
+                    logit_clamp: float = 0.0, out=None, return_lse: bool = False, lse=None, stream=None,
+                    causal: bool = True):
+    """pi-Attention forward (causal, or bidirectional with ``causal=False``).
 
     q, k, v: [B, H, N, D] float32 or bfloat16 on the GPU, identical strides,
     last dimension contiguous.  gate: float32 pre-sigmoid gate logits, [H]
@@ -166,7 +170,7 @@ def pi_attn_forward(q, k, v, gate, k_window: int, pi: int, scale: float | None =
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     st = library().pi_attn_forward(
-        _dtype_code(q.dtype), B, H, N, D, int(k_window), int(pi),
+        _dtype_code(q.dtype), B, H, N, D, int(k_window), int(pi), int(bool(causal)),
         _ptr(q), _ptr(k), _ptr(v), q.stride(0), q.stride(1), q.stride(2),
         _ptr(g), g.stride(0), g.stride(1), g.stride(2), float(scale), float(logit_clamp),
         _ptr(out), out.stride(0), out.stride(1), out.stride(2), _ptr(lse),
@@ -176,10 +180,11 @@ def pi_attn_forward(q, k, v, gate, k_window: int, pi: int, scale: float | None =
 
 
 def pi_attn_backward(q, k, v, gate, k_window: int, pi: int, out, lse, dout, scale: float | None = None,
-                     logit_clamp: float = 0.0, gate_grad_per_query: bool = False, stream=None):
-    """Gradients of the causal pi-Attention forward for dL/dy = ``dout``.
+                     logit_clamp: float = 0.0, gate_grad_per_query: bool = False, stream=None,
+                     causal: bool = True):
+    """Gradients of the pi-Attention forward for dL/dy = ``dout``.
 
-    q, k, v, gate, k_window, pi, scale and logit_clamp as passed to
+    q, k, v, gate, k_window, pi, scale, logit_clamp and causal as passed to
     pi_attn_forward; ``out`` and ``lse`` are what that forward call returned
     ([B, H, N, D] in q's dtype, [B, H, N] float32); ``dout`` has out's shape,
     dtype and strides.  Returns float32
@@ -219,7 +224,7 @@ def pi_attn_backward(q, k, v, gate, k_window: int, pi: int, out, lse, dout, scal
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     st = library().pi_attn_backward(
-        _dtype_code(q.dtype), B, H, N, D, int(k_window), int(pi),
+        _dtype_code(q.dtype), B, H, N, D, int(k_window), int(pi), int(bool(causal)),
         _ptr(q), _ptr(k), _ptr(v), q.stride(0), q.stride(1), q.stride(2),
         _ptr(g), g.stride(0), g.stride(1), g.stride(2), float(scale), float(logit_clamp), _ptr(lse),
         _ptr(out), _ptr(dout), dout.stride(0), dout.stride(1), dout.stride(2),

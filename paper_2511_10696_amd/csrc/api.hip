@@ -23,6 +23,14 @@ bool stride16(int64_t stride_elems, int es) { return stride_elems >= 0 && ((stri
 
 int from_hip(hipError_t e) { return e == hipSuccess ? PI_ATTN_OK : PI_ATTN_EHIP; }
 
+// The bf16 kernels address the key/value rows one tile of 128 queries (or
+// keys) can reach -- at most k + 256 of them, 2k + 256 bidirectional --
+// with 32-bit byte offsets.
+bool tile_span_ok(int32_t k, int32_t N, bool causal, int64_t sn, int es) {
+    const int64_t rows = (causal ? 1 : 2) * (int64_t)std::min(k, N) + 256;
+    return rows * sn * es < ((int64_t)1 << 31);
+}
+
 }  // namespace
 
 extern "C" {
@@ -32,28 +40,29 @@ const char *pi_attn_strerror(int status) {
         case PI_ATTN_OK: return "ok";
         case PI_ATTN_EINVAL: return "invalid argument (null pointer, negative size or stride, misalignment)";
         case PI_ATTN_EUNSUPPORTED:
-            return "unsupported configuration (head dimension must be 64 or 128; dtype f32/bf16; bf16 forward: "
-                   "(k + 256) rows of keys must span under 2 GiB)";
+            return "unsupported configuration (head dimension must be 64 or 128; dtype f32/bf16; bf16: "
+                   "(k + 256) rows of keys, (2k + 256) bidirectional, must span under 2 GiB)";
         case PI_ATTN_EHIP: return "HIP runtime refused the launch";
         default: return "unknown status";
     }
 }
 
-int32_t pi_attn_ws_width(int32_t k, int32_t pi) {
+int32_t pi_attn_ws_width(int32_t k, int32_t pi, int32_t causal) {
     if (k < 0 || pi < 0) return -1;
-    return ws_width(k, pi);
+    const int64_t m = ws_width(k, pi, causal != 0);
+    return m > INT32_MAX ? -1 : (int32_t)m;
 }
 
-int pi_attn_index_set(int32_t n, int32_t k, int32_t pi, int32_t *idx, void *stream) {
+int pi_attn_index_set(int32_t n, int32_t k, int32_t pi, int32_t causal, int32_t *idx, void *stream) {
     if (n < 0 || k < 0 || pi < 0) return PI_ATTN_EINVAL;
-    if ((int64_t)n * ws_width(k, pi) >= kMaxRows) return PI_ATTN_EINVAL;
+    if ((int64_t)n * ws_width(k, pi, causal != 0) >= kMaxRows) return PI_ATTN_EINVAL;
     if (n == 0) return PI_ATTN_OK;
     if (!idx || !aligned4(idx)) return PI_ATTN_EINVAL;
-    return from_hip(launch_index_set(n, k, pi, idx, (hipStream_t)stream));
+    return from_hip(launch_index_set(n, k, pi, causal != 0, idx, (hipStream_t)stream));
 }
 
 int pi_attn_forward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, int32_t k, int32_t pi,
-                    const void *q, const void *kk, const void *v, int64_t sb, int64_t sh, int64_t sn,
+                    int32_t causal, const void *q, const void *kk, const void *v, int64_t sb, int64_t sh, int64_t sn,
                     const float *gate, int64_t gsb, int64_t gsh, int64_t gsn, float scale, float logit_clamp,
                     void *out, int64_t osb, int64_t osh, int64_t osn, float *lse, void *stream) {
     const int es = elem_size(dtype);
@@ -70,13 +79,10 @@ int pi_attn_forward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, i
     if (!stride16(osb, es) || !stride16(osh, es) || !stride16(osn, es)) return PI_ATTN_EINVAL;
     if (!aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
     if (lse && !aligned4(lse)) return PI_ATTN_EINVAL;
-    // The bf16 kernel addresses one query tile's key/value rows (at most
-    // k + 256 of them) with 32-bit byte offsets.
-    if (dtype == PI_ATTN_BF16 && ((int64_t)std::min(k, N) + 256) * sn * es >= ((int64_t)1 << 31))
-        return PI_ATTN_EUNSUPPORTED;
+    if (dtype == PI_ATTN_BF16 && !tile_span_ok(k, N, causal != 0, sn, es)) return PI_ATTN_EUNSUPPORTED;
 
     FwdParams p{};
-    p.B = B; p.H = H; p.N = N; p.D = D; p.k = k; p.pi = pi;
+    p.B = B; p.H = H; p.N = N; p.D = D; p.k = k; p.pi = pi; p.causal = causal != 0;
     p.q = q; p.k_ptr = kk; p.v = v;
     p.sb = sb; p.sh = sh; p.sn = sn;
     p.gate = gate; p.gsb = gsb; p.gsh = gsh; p.gsn = gsn;
@@ -89,7 +95,7 @@ int pi_attn_forward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, i
 }
 
 int pi_attn_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, int32_t k, int32_t pi,
-                     const void *q, const void *kk, const void *v, int64_t sb, int64_t sh, int64_t sn,
+                     int32_t causal, const void *q, const void *kk, const void *v, int64_t sb, int64_t sh, int64_t sn,
                      const float *gate, int64_t gsb, int64_t gsh, int64_t gsn, float scale, float logit_clamp,
                      const float *lse, const void *out, const void *dout, int64_t osb, int64_t osh,
                      int64_t osn, float *dq,
@@ -109,15 +115,14 @@ int pi_attn_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, 
     if (!stride16(sb, es) || !stride16(sh, es) || !stride16(sn, es)) return PI_ATTN_EINVAL;
     if (!stride16(osb, es) || !stride16(osh, es) || !stride16(osn, es)) return PI_ATTN_EINVAL;
     if (!aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
-    if (dtype == PI_ATTN_BF16 && ((int64_t)std::min(k, N) + 256) * sn * es >= ((int64_t)1 << 31))
-        return PI_ATTN_EUNSUPPORTED;
+    if (dtype == PI_ATTN_BF16 && !tile_span_ok(k, N, causal != 0, sn, es)) return PI_ATTN_EUNSUPPORTED;
     if (!aligned4(lse) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv) || !aligned4(dgate) ||
         !aligned4(rowterm))
         return PI_ATTN_EINVAL;
 
     BwdParams p{};
     FwdParams &f = p.f;
-    f.B = B; f.H = H; f.N = N; f.D = D; f.k = k; f.pi = pi;
+    f.B = B; f.H = H; f.N = N; f.D = D; f.k = k; f.pi = pi; f.causal = causal != 0;
     f.q = q; f.k_ptr = kk; f.v = v;
     f.sb = sb; f.sh = sh; f.sn = sn;
     f.gate = gate; f.gsb = gsb; f.gsh = gsh; f.gsn = gsn;
@@ -151,7 +156,7 @@ int pi_attn_decode_step(int32_t dtype, int32_t S, int32_t H, int32_t D, int32_t 
     if (!aligned4(gate) || gss < 0 || gsh < 0) return PI_ATTN_EINVAL;
     if (lse && !aligned4(lse)) return PI_ATTN_EINVAL;
 
-    DecodeParams p{};
+    DecodeParams p{};   // decode is causal
     p.S = S; p.H = H; p.D = D; p.cap = cap; p.k = k; p.pi = pi;
     p.len_in = len_in; p.len_out = len_out;
     p.q_new = q_new; p.k_new = k_new; p.v_new = v_new;

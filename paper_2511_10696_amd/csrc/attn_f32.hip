@@ -1,7 +1,7 @@
 // attn_f32.hip -- float32 forward and decode: one wavefront per query.
 //
 // Lane l holds elements l, l+64, ... of the D-vector.  The working set is
-// visited entry by entry (partner first, then the window oldest to newest);
+// visited entry by entry (partners first, then the window oldest to newest);
 // each score is a wavefront-wide dot product, folded into a running max /
 // running sum (online softmax) in the log2 domain.  This is the plain,
 // correctness-first GPU path; the bf16 kernels are the fast ones.
@@ -67,7 +67,10 @@ __global__ __launch_bounds__(256) void forward_f32_kernel(FwdParams p) {
 
     const int jp = partner_of(t, p.k, p.pi);
     if (jp >= 0) st.visit(kk + base + jp * p.sn, v + base + jp * p.sn, fb.partner, p.scale, p.clamp, lane);
-    for (int j = window_lo(t, p.k); j <= t; ++j)
+    const int jf = p.causal ? -1 : partner_fwd_of(t, p.k, p.pi, p.N);
+    if (jf >= 0) st.visit(kk + base + jf * p.sn, v + base + jf * p.sn, fb.partner, p.scale, p.clamp, lane);
+    const int hi = window_hi(t, p.k, p.N, p.causal);
+    for (int j = window_lo(t, p.k); j <= hi; ++j)
         st.visit(kk + base + j * p.sn, v + base + j * p.sn, fb.local, p.scale, p.clamp, lane);
 
     float *out = (float *)p.out;

@@ -17,7 +17,8 @@
 // Row terms (float32): r_t from the forward output y (a wavefront per row).  Query
 // pass: wavefront per (b, h, t), lane l holding elements l, l+64, ..., one
 // sweep over W_t.  Key pass: wavefront per (b, h, j) over the queries whose
-// working set holds j: t in [j, j + k] and, when pi > k, t = j + pi.  These
+// working set holds j: t in [j, j + k] and, when pi > k, t = j + pi (causal);
+// t in [j - k, j + k] and t = j -/+ pi (bidirectional).  These
 // are the float32 kernels (every dot product a wavefront reduction); bf16
 // inputs run the MFMA passes of backward_bf16.hip and backward_kv_bf16.hip.
 #include "kernels.h"
@@ -110,7 +111,8 @@ __global__ __launch_bounds__(256) void backward_q_kernel(BwdParams p) {
     const GateGrad gg = gate_grad(g);
     const float shift = fb.lse_shift - p.lse[row];   // alpha^ = exp(delta + shift)
     const int jp = partner_of(t, f.k, f.pi);
-    const int lo = window_lo(t, f.k);
+    const int jf = f.causal ? -1 : partner_fwd_of(t, f.k, f.pi, f.N);
+    const int lo = window_lo(t, f.k), hi = window_hi(t, f.k, f.N, f.causal);
 
     // (weight, dp) of one working-set entry
     auto entry = [&](int j, float bias, float &w, float &dp, bool &cut) {
@@ -139,7 +141,8 @@ __global__ __launch_bounds__(256) void backward_q_kernel(BwdParams p) {
         dg += dd * dlogw;
     };
     if (jp >= 0) grad(jp, fb.partner, gg.partner);
-    for (int j = lo; j <= t; ++j) grad(j, fb.local, gg.local);
+    if (jf >= 0) grad(jf, fb.partner, gg.partner);
+    for (int j = lo; j <= hi; ++j) grad(j, fb.local, gg.local);
 
 #pragma unroll
     for (int e = 0; e < E; ++e) p.dq[row * D + lane + 64 * e] = dq[e] * f.scale;
@@ -191,9 +194,16 @@ __global__ __launch_bounds__(256) void backward_kv_kernel(BwdParams p) {
             dv[e] += w * go[e];
         }
     };
-    const int t_hi = min(j + f.k, f.N - 1);
-    for (int t = j; t <= t_hi; ++t) visit(t, false);
-    if (partner_enabled(f.k, f.pi) && (int64_t)j + f.pi < f.N) visit(j + f.pi, true);
+    // The windows holding j are symmetric to j's own: causal t in [j, j + k],
+    // bidirectional t in [j - k, j + k].
+    const int t_lo = f.causal ? j : window_lo(j, f.k);
+    const int t_hi = window_hi(j, f.k, f.N, false);
+    for (int t = t_lo; t <= t_hi; ++t) visit(t, false);
+    // j is the partner t - pi of t = j + pi and, bidirectional, t + pi of t = j - pi.
+    const int tp = partner_fwd_of(j, f.k, f.pi, f.N);
+    if (tp >= 0) visit(tp, true);
+    const int tm = f.causal ? -1 : partner_of(j, f.k, f.pi);
+    if (tm >= 0) visit(tm, true);
 
 #pragma unroll
     for (int e = 0; e < E; ++e) {
@@ -212,13 +222,12 @@ hipError_t launch(const BwdParams &p, hipStream_t stream) {
         e = launch_backward_q_bf16(p, stream);
         if (e != hipSuccess) return e;
         return launch_backward_kv_bf16(p, stream);
-    } else {
-        e = launch_kernel(rowterm_kernel<D, T>, grid, block, stream, p);
-        if (e != hipSuccess) return e;
-        e = launch_kernel(backward_q_kernel<D, T>, grid, block, stream, p);
-        if (e != hipSuccess) return e;
-        return launch_kernel(backward_kv_kernel<D, T>, grid, block, stream, p);
     }
+    e = launch_kernel(rowterm_kernel<D, T>, grid, block, stream, p);
+    if (e != hipSuccess) return e;
+    e = launch_kernel(backward_q_kernel<D, T>, grid, block, stream, p);
+    if (e != hipSuccess) return e;
+    return launch_kernel(backward_kv_kernel<D, T>, grid, block, stream, p);
 }
 
 }  // namespace

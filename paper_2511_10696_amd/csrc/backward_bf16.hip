@@ -25,7 +25,9 @@
 // prior, dg = sum_prior d(log omega)/dg (A - r* B).  r* is also written out
 // as the row term of the key pass.  The partner
 // row (Sec. 3.4, eq. Npi) is the diagonal of one 32x32 block per product,
-// read straight from global memory as in the forward.
+// read straight from global memory as in the forward; the bidirectional mode
+// (window |j - t| <= k, band up to t0 + 127 + k) adds the second partner
+// t + pi the same way.
 //
 // LDS rows are padded (2D + 16 bytes): the row reads are free of bank
 // conflicts and the transpose reads of the key tile cost at most two ways.
@@ -147,7 +149,7 @@ __device__ inline void read_cols(bf16x8 f[2][Tile<D>::DB], const unsigned char *
     }
 }
 
-template <int D, bool CLAMP>
+template <int D, bool CLAMP, bool BIDIR>
 __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, int n_qt, int64_t n_logical) {
     using T = Tile<D>;
     constexpr int KS = T::KS, DB = T::DB;
@@ -179,7 +181,7 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
     const int64_t sn = p.sn;
 
     const int kb0 = window_lo(t0, kw) & ~31;
-    const int kend = min(t0 + BM, N);
+    const int kend = BIDIR ? (int)min((int64_t)t0 + BM + kw, (int64_t)N) : min(t0 + BM, N);
     const int ntiles = (kend - kb0 + TK - 1) / TK;
     const int rowb = (int)(2 * sn);
     const __amdgpu_buffer_rsrc_t rk =
@@ -227,10 +229,10 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
     // exact row term and per-prior sums for the gate gradient
     float r_all = 0.0f, a_loc = 0.0f, b_loc = 0.0f, a_par = 0.0f, b_par = 0.0f;
 
-    // ---- partner: the diagonal of K_p Q^T and V_p dO^T ----------------------
-    const int prow = t - pi;
-    const bool has_p = partner_enabled(kw, pi) && prow >= 0 && t_ok;
-    if (__builtin_amdgcn_ballot_w64(has_p) != 0) {
+    // ---- partners: the diagonal of K_p Q^T and V_p dO^T ----------------------
+    // Partner row prow of this lane's query (has_p: it exists).
+    auto partner = [&](int prow, bool has_p) {
+        if (__builtin_amdgcn_ballot_w64(has_p) == 0) return;
         const int prc = has_p ? prow : 0;
         bf16x8 kpf[KS], vpf[KS];
 #pragma unroll
@@ -257,9 +259,9 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
         const float wgt = has_p ? __builtin_amdgcn_exp2f(delta2 - lse2) : 0.0f;
         const float dd = cut ? 0.0f : wgt * (dpd - r);
         if (g == 0) {   // one lane of the pair counts the partner
-            r_all = wgt * dpd;
-            a_par = cut ? 0.0f : wgt * dpd;
-            b_par = cut ? 0.0f : wgt;
+            r_all += wgt * dpd;
+            a_par += cut ? 0.0f : wgt * dpd;
+            b_par += cut ? 0.0f : wgt;
         }
         // dq += dd * k_p over this lane's dims 32db + 8i + 4g + [0, 4)
 #pragma unroll
@@ -273,16 +275,20 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
                 dq[db][4 * i + 3] += dd * __uint_as_float(raw.y & 0xffff0000u);
             }
         }
-    }
+    };
+    partner(t - pi, partner_enabled(kw, pi) && t - pi >= 0 && t_ok);
+    if constexpr (BIDIR) partner(t + pi, t_ok && partner_fwd_of(t, kw, pi, N) >= 0);
 #pragma unroll
     for (int hf = 0; hf < BPT; ++hf) tile_store<D>(st0[hf], tA, hf, tid);
     __syncthreads();
 
     // ---- window band ---------------------------------------------------------
     auto block = [&](const TileBuf<D> &tb, int j0, int blk) {
-        const bool act = j0 < kend && q0 < N && j0 <= q0 + 31 && j0 + 31 >= q0 - kw;
+        const bool act = BIDIR ? j0 < kend && q0 < N && j0 - (q0 + 31) <= kw && j0 + 31 >= q0 - kw
+                               : j0 < kend && q0 < N && j0 <= q0 + 31 && j0 + 31 >= q0 - kw;
         if (!act) return;
-        const bool edge = !(j0 + 31 <= q0 && j0 >= q0 + 31 - kw) || q0 + 31 >= N;
+        const bool edge = BIDIR ? !(j0 + 31 - q0 <= kw && q0 + 31 - j0 <= kw) || q0 + 31 >= N || j0 + 31 >= N
+                                : !(j0 + 31 <= q0 && j0 >= q0 + 31 - kw) || q0 + 31 >= N;
         bf16x8 f[KS];
         read_rows<D>(f, tb.k, blk, c, g);
         f32x16 sc = {};
@@ -308,7 +314,8 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
             }
             if (edge) {
                 const int j = j0 + 8 * (e >> 2) + 4 * g + (e & 3);
-                if (!(t_ok && j <= t && j >= t - kw)) delta2 = -INFINITY;
+                const bool ok = BIDIR ? t_ok && j < N && j - t <= kw && t - j <= kw : t_ok && j <= t && j >= t - kw;
+                if (!ok) delta2 = -INFINITY;
             }
             const float wgt = __builtin_amdgcn_exp2f(delta2 - lse2);
             const float pd = wgt * dp[e];
@@ -370,21 +377,25 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
     }
 }
 
-template <int D, bool CLAMP>
+template <int D, bool CLAMP, bool BIDIR>
 hipError_t launch_q(const BwdParams &p, hipStream_t stream) {
     const int n_qt = (p.f.N + BM - 1) / BM;
     const int64_t n_logical = (int64_t)p.f.B * p.f.H * n_qt;
     const int64_t grid = xcd_grid(n_logical);
-    return launch_kernel(backward_q_bf16_kernel<D, CLAMP>, dim3((unsigned)grid), dim3(NT), stream, p, n_qt,
+    return launch_kernel(backward_q_bf16_kernel<D, CLAMP, BIDIR>, dim3((unsigned)grid), dim3(NT), stream, p, n_qt,
                          n_logical);
+}
+
+template <int D, bool BIDIR>
+hipError_t launch_qc(const BwdParams &p, hipStream_t stream) {
+    return p.f.clamp > 0.0f ? launch_q<D, true, BIDIR>(p, stream) : launch_q<D, false, BIDIR>(p, stream);
 }
 
 }  // namespace
 
 hipError_t launch_backward_q_bf16(const BwdParams &p, hipStream_t stream) {
-    const bool clamp = p.f.clamp > 0.0f;
-    if (p.f.D == 64) return clamp ? launch_q<64, true>(p, stream) : launch_q<64, false>(p, stream);
-    return clamp ? launch_q<128, true>(p, stream) : launch_q<128, false>(p, stream);
+    if (p.f.D == 64) return p.f.causal ? launch_qc<64, false>(p, stream) : launch_qc<64, true>(p, stream);
+    return p.f.causal ? launch_qc<128, false>(p, stream) : launch_qc<128, true>(p, stream);
 }
 
 }  // namespace pi_attn

@@ -10,7 +10,10 @@
 // j <= t <= j + k, Sec. 3.2 eq. Nr), then the partner run
 // [j0 + pi, j0 + pi + 128) (key j is the partner of query j + pi when
 // pi > k, Sec. 3.4 eq. Npi), in which wavefront w meets its partners on
-// the diagonal of block w.  Per 32-query block, on
+// the diagonal of block w.  The bidirectional mode streams the band
+// [j0 - k, j0 + 127 + k] (|t - j| <= k) and a second partner run
+// [j0 - pi, j0 - pi + 128) (key j is the partner t + pi of query j - pi);
+// rows of a run outside [0, N) are zero and masked.  Per 32-query block, on
 // v_mfma_f32_32x32x16_bf16:
 //   S   = Q K^T      A = Q rows (LDS), B = K^T (registers)
 //   dP  = dO V^T     A = dO rows (LDS), B = V^T (registers)
@@ -76,7 +79,7 @@ __device__ inline float other_half(float x) {
     return __uint_as_float(__lane_id() < 32 ? p[1] : p[0]);
 }
 
-template <int D, bool CLAMP>
+template <int D, bool CLAMP, bool BIDIR>
 __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, int n_kt, int64_t n_logical) {
     using T = Tile<D>;
     constexpr int KS = T::KS, DB = T::DB;
@@ -125,34 +128,48 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
         dv[db] = f32x16{};
     }
 
-    // Query streams: the window band, then (pi > k) the partner run.
-    const int band_lo = j0, band_hi = min(N, j0 + BK + kw);   // queries [band_lo, band_hi)
+    // Query streams (kind 0 band, 1 the run of queries whose partner t - pi
+    // is one of these keys, 2 (bidirectional) the run whose partner t + pi
+    // is): tiles [0, nband), [nband, nband + npar), then the rest.  Query
+    // rows [lo, hi) of a stream; rows outside [0, N) are zero and masked.
+    const int band_lo = BIDIR ? window_lo(j0, kw) & ~31 : j0;
+    const int band_hi = (int)min((int64_t)j0 + BK + kw, (int64_t)N);
     const int nband = band_hi > band_lo ? (band_hi - band_lo + TQ - 1) / TQ : 0;
     const bool has_par = partner_enabled(kw, pi) && (int64_t)j0 + pi < N;
     const int par_lo = j0 + pi;
     const int par_hi = has_par ? min(N, j0 + pi + BK) : par_lo;
     const int npar = has_par ? (par_hi - par_lo + TQ - 1) / TQ : 0;
-    const int ntiles = nband + npar;
+    const bool has_par2 = BIDIR && partner_enabled(kw, pi) && j0 + BK > pi;
+    const int par2_lo = j0 - pi;   // may be negative
+    const int par2_hi = has_par2 ? min(N, j0 + BK - pi) : par2_lo;
+    const int npar2 = has_par2 ? (par2_hi - par2_lo + TQ - 1) / TQ : 0;
+    const int ntiles = nband + npar + npar2;
 
     // Stage tile m of the combined stream: 64 query rows starting at q0m.
-    auto tile_start = [&](int m) { return m < nband ? band_lo + TQ * m : par_lo + TQ * (m - nband); };
-    auto tile_end = [&](int m) { return m < nband ? band_hi : par_hi; };
+    auto tile_kind = [&](int m) { return m < nband ? 0 : m < nband + npar ? 1 : 2; };
+    auto tile_start = [&](int m) {
+        return m < nband ? band_lo + TQ * m : m < nband + npar ? par_lo + TQ * (m - nband)
+                                                               : par2_lo + TQ * (m - nband - npar);
+    };
+    auto tile_end = [&](int m) { return m < nband ? band_hi : m < nband + npar ? par_hi : par2_hi; };
     auto load = [&](Stage<D> &st, int m) {
         const int q0m = tile_start(m), lim = tile_end(m);
+        const int tfirst = q0m > 0 ? q0m : 0;   // an always-valid row of the stream
 #pragma unroll
         for (int u = 0; u < T::CH; ++u) {
             const int cid = tid + NT * u;
             const int row = cid / T::CPR, pc = cid % T::CPR;
             const int t = q0m + row;
-            const int tc = t < lim ? t : q0m;
+            const bool ok = t >= 0 && t < lim;
+            const int tc = ok ? t : tfirst;
             const uint4 qv = *reinterpret_cast<const uint4 *>(qp + tc * sn + 8 * pc);
             const uint4 ov = *reinterpret_cast<const uint4 *>(op + tc * osn + 8 * pc);
-            st.q[u] = t < lim ? qv : make_uint4(0, 0, 0, 0);
-            st.o[u] = t < lim ? ov : make_uint4(0, 0, 0, 0);
+            st.q[u] = ok ? qv : make_uint4(0, 0, 0, 0);
+            st.o[u] = ok ? ov : make_uint4(0, 0, 0, 0);
         }
         if (tid < TQ) {
             const int t = q0m + tid;
-            const int tc = t < lim ? t : q0m;
+            const int tc = (t >= 0 && t < lim) ? t : tfirst;
             const FusionBias fb = fusion_bias(p.gate[b * p.gsb + h * p.gsh + tc * p.gsn], exact);
             st.lse2 = (bp.lse[rbase + tc] - fb.lse_shift) * kLog2e;
             st.r = bp.rowterm[rbase + tc];
@@ -174,16 +191,24 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
         }
     };
 
-    // One 32-query block (rows 32 blk.. of tile tb, first query t0b).
-    auto block = [&](const QTile<D> &tb, int t0b, int blk, bool partner, int lim) {
-        bool act;
-        if (partner) {
+    // One 32-query block (rows 32 blk.. of tile tb, first query t0b) of a
+    // stream of the given kind.
+    auto block = [&](const QTile<D> &tb, int t0b, int blk, int kind, int lim) {
+        bool act, edge;
+        if (kind == 1) {
             act = blk == (w & 1) && t0b == kq0 + pi;
+            edge = true;
+        } else if (kind == 2) {
+            act = blk == (w & 1) && t0b == kq0 - pi;
+            edge = true;
+        } else if (BIDIR) {
+            act = t0b < lim && kq0 < N && t0b - (kq0 + 31) <= kw && t0b + 31 >= kq0 - kw;
+            edge = !(t0b + 31 - kq0 <= kw && kq0 + 31 - t0b <= kw) || t0b + 31 >= N || kq0 + 31 >= N;
         } else {
             act = t0b < lim && kq0 < N && t0b <= kq0 + 31 + kw && t0b + 31 >= kq0;
+            edge = !(t0b >= kq0 + 31 && t0b + 31 <= kq0 + kw) || t0b + 31 >= N || kq0 + 31 >= N;
         }
         if (!act) return;
-        const bool edge = partner || !(t0b >= kq0 + 31 && t0b + 31 <= kq0 + kw) || t0b + 31 >= N || kq0 + 31 >= N;
         // rows of this block (A operands: query l%32, dims 16s + 8g)
         const unsigned char *qrow = tb.q + (32 * blk + c) * T::ROW + 16 * g;
         const unsigned char *orow = tb.o + (32 * blk + c) * T::ROW + 16 * g;
@@ -218,8 +243,16 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
                 }
                 if (edge) {
                     const int t = t0b + 8 * i + 4 * g + jj;
-                    const bool ok = partner ? (t - j == pi && t < N && j_ok)
-                                            : (t >= j && t - j <= kw && t < N && j_ok);
+                    bool ok;
+                    if (kind == 1) {
+                        ok = t - j == pi && t < N && j_ok;
+                    } else if (kind == 2) {
+                        ok = j - t == pi && t >= 0 && j_ok;
+                    } else if (BIDIR) {
+                        ok = t - j <= kw && j - t <= kw && t < N && j_ok;
+                    } else {
+                        ok = t >= j && t - j <= kw && t < N && j_ok;
+                    }
                     if (!ok) delta2 = -INFINITY;
                 }
                 const float wgt = __builtin_amdgcn_exp2f(delta2 - l4[jj]);
@@ -273,14 +306,14 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
             if (m + 1 < ntiles) load(st, m + 1);
 #pragma unroll
             for (int blk = 0; blk < BPT; ++blk)
-                block(tA, tile_start(m) + 32 * blk, blk, m >= nband, tile_end(m));
+                block(tA, tile_start(m) + 32 * blk, blk, tile_kind(m), tile_end(m));
             if (m + 1 >= ntiles) break;
             store(st, tB);
             __syncthreads();
             if (m + 2 < ntiles) load(st, m + 2);
 #pragma unroll
             for (int blk = 0; blk < BPT; ++blk)
-                block(tB, tile_start(m + 1) + 32 * blk, blk, m + 1 >= nband, tile_end(m + 1));
+                block(tB, tile_start(m + 1) + 32 * blk, blk, tile_kind(m + 1), tile_end(m + 1));
             if (m + 2 >= ntiles) break;
             store(st, tA);
             __syncthreads();
@@ -308,21 +341,25 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
     }
 }
 
-template <int D, bool CLAMP>
+template <int D, bool CLAMP, bool BIDIR>
 hipError_t launch_kv(const BwdParams &p, hipStream_t stream) {
     const int n_kt = (p.f.N + BK - 1) / BK;
     const int64_t n_logical = (int64_t)p.f.B * p.f.H * n_kt;
     const int64_t grid = xcd_grid(n_logical);
-    return launch_kernel(backward_kv_bf16_kernel<D, CLAMP>, dim3((unsigned)grid), dim3(NT), stream, p, n_kt,
+    return launch_kernel(backward_kv_bf16_kernel<D, CLAMP, BIDIR>, dim3((unsigned)grid), dim3(NT), stream, p, n_kt,
                          n_logical);
+}
+
+template <int D, bool BIDIR>
+hipError_t launch_kvc(const BwdParams &p, hipStream_t stream) {
+    return p.f.clamp > 0.0f ? launch_kv<D, true, BIDIR>(p, stream) : launch_kv<D, false, BIDIR>(p, stream);
 }
 
 }  // namespace
 
 hipError_t launch_backward_kv_bf16(const BwdParams &p, hipStream_t stream) {
-    const bool clamp = p.f.clamp > 0.0f;
-    if (p.f.D == 64) return clamp ? launch_kv<64, true>(p, stream) : launch_kv<64, false>(p, stream);
-    return clamp ? launch_kv<128, true>(p, stream) : launch_kv<128, false>(p, stream);
+    if (p.f.D == 64) return p.f.causal ? launch_kvc<64, false>(p, stream) : launch_kvc<64, true>(p, stream);
+    return p.f.causal ? launch_kvc<128, false>(p, stream) : launch_kvc<128, true>(p, stream);
 }
 
 }  // namespace pi_attn

@@ -1,12 +1,13 @@
-// forward_bf16.hip -- banded MFMA forward of causal pi-Attention, bf16 in,
-// fp32 accumulate, for head dimension D = 64 or 128.
+// forward_bf16.hip -- banded MFMA forward of pi-Attention, bf16 in, fp32
+// accumulate, for head dimension D = 64 or 128, causal or bidirectional.
 //
 // Work decomposition.  One work-group (4 wavefronts) owns a query tile of
 // BM = 128 consecutive positions [t0, t0+128) of one (b, h); wavefront w owns
 // the 32 queries q0 = t0 + 32w + [0, 32).  The window keys of the tile,
-// [max(0, t0-k), t0+127], form a band that is streamed through LDS in 64-row
-// tiles (two 32-key blocks, aligned to multiples of 32); each wavefront works
-// on the blocks that meet its own band [q0 - k, q0 + 31].  Two work-groups
+// [max(0, t0-k), t0+127] (bidirectional: up to t0+127+k), form a band that is
+// streamed through LDS in 64-row tiles (two 32-key blocks, aligned to
+// multiples of 32); each wavefront works on the blocks that meet its own band
+// [q0 - k, q0 + 31] (bidirectional: [q0 - k, q0 + 31 + k]).  Two work-groups
 // share a CU, so each SIMD interleaves two wavefronts.
 //
 // MFMA layout (v_mfma_f32_32x32x16_bf16).  Scores are computed transposed,
@@ -34,6 +35,8 @@
 // pi, read straight from global memory into the MFMA operand layout.  Its
 // score (the diagonal of one 32x32 MFMA block) seeds the online softmax:
 // running max = partner logit, running sum = 1, accumulator = partner value.
+// The bidirectional mode scores the second partner t + pi the same way and
+// seeds the state with both.
 //
 // Online softmax with a lazily updated maximum: a lane raises its reference
 // maximum m only when a block's maximum exceeds it by more than 2^8 (exp2
@@ -41,6 +44,15 @@
 // the stale m, which changes nothing in exact arithmetic (numerator and
 // denominator share the reference) and keeps the rescale of the accumulators
 // out of the common path.
+//
+// Normalisation.  The value product takes the probabilities rounded to bf16,
+// so the output is divided by the sum of those rounded values (accumulated
+// with v_dot2c_f32_bf16, two per instruction): the weights actually applied
+// to V sum to one, and a query whose attention sits on one key returns that
+// key's value row exactly, whatever the rounding of its stale-maximum
+// probability.  The lse, when requested, is taken from a second, fp32 sum of
+// the unrounded values (a separate instantiation keeps it off the common
+// path).
 #include "kernels.h"
 #include "pi_common.h"
 
@@ -49,6 +61,7 @@ namespace pi_attn {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -144,14 +157,25 @@ struct Wave {
     bf16x8 qf[KS];                      // B operand: Q[t][16s + 8g .. +8]
     f32x16 o[DB];                       // O^T accumulators: dims 32db + 8i + 4g + j
     float m;                            // reference (lazy) maximum, log2 units
-    float l;                            // this lane's part of the running sum
+    float l;                            // this lane's part of the running sum (kept for the lse)
+    float lb;                           // the same sum over the bf16-rounded probabilities
 };
+
+// s + the sum of the eight bf16 values of p.
+__device__ inline float sum_bf16x8(const bf16x8 &p, float s) {
+    const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 0, 1), one, s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 2, 3), one, s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 4, 5), one, s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 6, 7), one, s, false);
+    return s;
+}
 
 // Scores of one 32-key block -> log2-unit logits (masked to -inf on edge
 // blocks), running state update, and bf16 probabilities for the value product.
-template <int D, bool CLAMP>
-__device__ inline void softmax_block(Wave<D> &ws, f32x16 &s, bool edge, int j0, int t, int kw, bool t_ok, float c2,
-                                     float scale, float bias, float clampv, int g, bf16x8 pb[2]) {
+template <int D, bool CLAMP, bool BIDIR, bool LSE>
+__device__ inline void softmax_block(Wave<D> &ws, f32x16 &s, bool edge, int j0, int t, int kw, int N, bool t_ok,
+                                     float c2, float scale, float bias, float clampv, int g, bf16x8 pb[2]) {
     if constexpr (CLAMP) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) s[e] = fminf(fmaxf(s[e] * scale + bias, -clampv), clampv) * kLog2e;
@@ -160,7 +184,12 @@ __device__ inline void softmax_block(Wave<D> &ws, f32x16 &s, bool edge, int j0, 
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
             const int j = j0 + 8 * (e >> 2) + 4 * g + (e & 3);
-            const bool ok = t_ok && j <= t && j >= t - kw;
+            bool ok;
+            if constexpr (BIDIR) {
+                ok = t_ok && j < N && j - t <= kw && t - j <= kw;
+            } else {
+                ok = t_ok && j <= t && j >= t - kw;
+            }
             s[e] = ok ? s[e] : -INFINITY;
         }
     }
@@ -175,7 +204,8 @@ __device__ inline void softmax_block(Wave<D> &ws, f32x16 &s, bool edge, int j0, 
         const float m_new = need ? mx : ws.m;
         const float alpha = need ? __builtin_amdgcn_exp2f(ws.m - m_new) : 1.0f;
         ws.m = m_new;
-        ws.l *= alpha;
+        if constexpr (LSE) ws.l *= alpha;
+        ws.lb *= alpha;
 #pragma unroll
         for (int db = 0; db < Wave<D>::DB; ++db) ws.o[db] *= alpha;
     }
@@ -192,14 +222,15 @@ __device__ inline void softmax_block(Wave<D> &ws, f32x16 &s, bool edge, int j0, 
                 v = __builtin_fmaf(s[8 * c + e], c2, -mu);
             }
             const float p = __builtin_amdgcn_exp2f(v);
-            lsum += p;
+            if constexpr (LSE) lsum += p;
             pb[c][e] = (__bf16)p;
         }
     }
-    ws.l += lsum;
+    if constexpr (LSE) ws.l += lsum;
+    ws.lb = sum_bf16x8(pb[1], sum_bf16x8(pb[0], ws.lb));
 }
 
-template <int D, bool CLAMP>
+template <int D, bool CLAMP, bool BIDIR, bool LSE>
 __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdParams p, int n_qt, int64_t n_logical) {
     using T = Tile<D>;
     using W = Wave<D>;
@@ -228,7 +259,7 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
 
     // Window tiles: rows [kb0, kend) in 64-row steps, blocks aligned to 32.
     const int kb0 = window_lo(t0, kw) & ~31;
-    const int kend = min(t0 + BM, N);
+    const int kend = BIDIR ? (int)min((int64_t)t0 + BM + kw, (int64_t)N) : min(t0 + BM, N);
     const int ntiles = (kend - kb0 + TK - 1) / TK;
     // ---- prologue: every load is issued before any is waited for ----------
     // (the first tile, the query fragments, the gate logit and the partner
@@ -272,19 +303,34 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
             for (int i = 0; i < 4; ++i)
                 vraw[db][i] = *reinterpret_cast<const uint2 *>(vp + prc * sn + 32 * db + 8 * i + 4 * g);
     }
+    // Bidirectional: the second partner t + pi, loaded the same way.
+    const bool has_f = BIDIR && t_ok && partner_fwd_of(t, kw, pi, N) >= 0;
+    const bool any_f = BIDIR && __builtin_amdgcn_ballot_w64(has_f) != 0;
+    const int frc = has_f ? t + pi : 0;
+    bf16x8 kff[W::KS];
+    uint2 vfraw[W::DB][4];
+    if (any_f) {
+#pragma unroll
+        for (int s = 0; s < W::KS; ++s) kff[s] = *reinterpret_cast<const bf16x8 *>(kp + frc * sn + 16 * s + 8 * g);
+#pragma unroll
+        for (int db = 0; db < W::DB; ++db)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                vfraw[db][i] = *reinterpret_cast<const uint2 *>(vp + frc * sn + 32 * db + 8 * i + 4 * g);
+    }
 #pragma unroll
     for (int s = 0; s < W::KS; ++s) ws.qf[s] = t_ok ? qraw[s] : bf16x8{};
 
     const FusionBias fb = fusion_bias(gl, CLAMP);
     const float c2 = p.scale * kLog2e;
-    ws.m = -INFINITY;
-    if (any_p) {
+    // Partner logit (log2 units) of this lane's query from the partner rows
+    // kf: the diagonal of one 32x32 score block, whose entry (row c, column
+    // c) sits in half (c/4)%2 at slot 4(c/8) + c%4.
+    auto partner_logit = [&](const bf16x8 (&kf)[W::KS], bool has) {
         f32x16 acc = {};
 #pragma unroll
         for (int s = 0; s < W::KS; ++s)
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(has_p ? kpf[s] : bf16x8{}, ws.qf[s], acc, 0, 0, 0);
-        // The diagonal entry (row c, column c) sits in half (c/4)%2 at slot
-        // 4(c/8) + c%4.
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(has ? kf[s] : bf16x8{}, ws.qf[s], acc, 0, 0, 0);
         const int slot = 4 * (c >> 3) + (c & 3);
         float mine = 0.0f;
 #pragma unroll
@@ -297,20 +343,37 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
         } else {
             sp = diag * c2 + fb.partner * kLog2e;
         }
-        ws.m = has_p ? sp : -INFINITY;
-    }
-    ws.l = (has_p && g == 0) ? 1.0f : 0.0f;
+        return has ? sp : -INFINITY;
+    };
+    // Seed: running max = the larger partner logit, running sum and
+    // accumulator = the partners' weights and weighted values.
+    const float sp = any_p ? partner_logit(kpf, has_p) : -INFINITY;
+    const float sf = any_f ? partner_logit(kff, has_f) : -INFINITY;
+    ws.m = fmaxf(sp, sf);
+    const float wp = has_p ? (BIDIR ? __builtin_amdgcn_exp2f(sp - ws.m) : 1.0f) : 0.0f;
+    const float wf = has_f ? __builtin_amdgcn_exp2f(sf - ws.m) : 0.0f;
+    ws.l = g == 0 ? wp + wf : 0.0f;
+    ws.lb = ws.l;   // the partner weights enter the accumulator unrounded
+    // Lanes without that partner contribute exactly 0 (their loads read a
+    // clamped row whose data is not used, not even multiplied by 0).
+    auto seed = [&](uint2 (&vr)[W::DB][4], float wt, bool has, bool add) {
 #pragma unroll
-    for (int db = 0; db < W::DB; ++db) {
+        for (int db = 0; db < W::DB; ++db) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            if (!has_p) vraw[db][i] = make_uint2(0, 0);
-            ws.o[db][4 * i + 0] = __uint_as_float(vraw[db][i].x << 16);
-            ws.o[db][4 * i + 1] = __uint_as_float(vraw[db][i].x & 0xffff0000u);
-            ws.o[db][4 * i + 2] = __uint_as_float(vraw[db][i].y << 16);
-            ws.o[db][4 * i + 3] = __uint_as_float(vraw[db][i].y & 0xffff0000u);
+            for (int i = 0; i < 4; ++i) {
+                if (!has) vr[db][i] = make_uint2(0, 0);
+                const float e[4] = {__uint_as_float(vr[db][i].x << 16), __uint_as_float(vr[db][i].x & 0xffff0000u),
+                                    __uint_as_float(vr[db][i].y << 16), __uint_as_float(vr[db][i].y & 0xffff0000u)};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float x = BIDIR ? wt * e[j] : e[j];   // causal: the one partner has weight 1
+                    ws.o[db][4 * i + j] = add ? ws.o[db][4 * i + j] + x : x;
+                }
+            }
         }
-    }
+    };
+    seed(vraw, wp, has_p, false);
+    if constexpr (BIDIR) seed(vfraw, wf, has_f, true);
 #pragma unroll
     for (int hf = 0; hf < BPT; ++hf) tile_store<D>(st0[hf], tA, hf, tid);
     __syncthreads();
@@ -320,9 +383,11 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
     // keys [j0, j0 + 32).
     auto block = [&](const unsigned char *kt, const unsigned char *vt, int j0, int blk) {
         // Wave-uniform: does the block meet the band, is it wholly inside it?
-        const bool act = j0 < kend && q0 < N && j0 <= q0 + 31 && j0 + 31 >= q0 - kw;
+        const bool act = BIDIR ? j0 < kend && q0 < N && j0 - (q0 + 31) <= kw && j0 + 31 >= q0 - kw
+                               : j0 < kend && q0 < N && j0 <= q0 + 31 && j0 + 31 >= q0 - kw;
         if (!act) return;
-        const bool edge = !(j0 + 31 <= q0 && j0 >= q0 + 31 - kw) || q0 + 31 >= N;
+        const bool edge = BIDIR ? !(j0 + 31 - q0 <= kw && q0 + 31 - j0 <= kw) || q0 + 31 >= N || j0 + 31 >= N
+                                : !(j0 + 31 <= q0 && j0 >= q0 + 31 - kw) || q0 + 31 >= N;
 
         // Fragment reads: the K rows (A operand of the scores) are issued
         // together ahead of the score MFMAs; the V^T reads (A operand of
@@ -359,7 +424,7 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
             }
         }
         bf16x8 pb[2];
-        softmax_block<D, CLAMP>(ws, sc, edge, j0, t, kw, t_ok, c2, p.scale, fb.local, p.clamp, g, pb);
+        softmax_block<D, CLAMP, BIDIR, LSE>(ws, sc, edge, j0, t, kw, N, t_ok, c2, p.scale, fb.local, p.clamp, g, pb);
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc) {
 #pragma unroll
@@ -391,9 +456,9 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
     }
 
     // ---- normalise and store -----------------------------------------------
-    const float l_tot = ws.l + other_half(ws.l);
+    const float lb_tot = ws.lb + other_half(ws.lb);
     if (t_ok) {
-        const float inv = 1.0f / l_tot;
+        const float inv = 1.0f / lb_tot;
         __bf16 *op = (__bf16 *)p.out + b * p.osb + h * p.osh + t * p.osn;
 #pragma unroll
         for (int db = 0; db < W::DB; ++db) {
@@ -405,25 +470,38 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
                 *reinterpret_cast<bf16x4 *>(op + 32 * db + 8 * i + 4 * g) = o4;
             }
         }
-        if (p.lse && g == 0) p.lse[bh * N + t] = (ws.m + __log2f(l_tot)) * kLn2 + fb.lse_shift;
+        if constexpr (LSE) {
+            const float l_tot = ws.l + other_half(ws.l);
+            if (g == 0) p.lse[bh * N + t] = (ws.m + __log2f(l_tot)) * kLn2 + fb.lse_shift;
+        }
     }
 }
 
-template <int D, bool CLAMP>
+template <int D, bool CLAMP, bool BIDIR, bool LSE>
 hipError_t launch(const FwdParams &p, hipStream_t stream) {
     const int n_qt = (p.N + BM - 1) / BM;
     const int64_t n_logical = (int64_t)p.B * p.H * n_qt;
     if (n_logical == 0) return hipSuccess;
     const int64_t grid = xcd_grid(n_logical);
-    return launch_kernel(forward_bf16_kernel<D, CLAMP>, dim3((unsigned)grid), dim3(NT), stream, p, n_qt, n_logical);
+    return launch_kernel(forward_bf16_kernel<D, CLAMP, BIDIR, LSE>, dim3((unsigned)grid), dim3(NT), stream, p, n_qt,
+                         n_logical);
+}
+
+template <int D, bool BIDIR, bool LSE>
+hipError_t launch_l(const FwdParams &p, hipStream_t stream) {
+    return p.clamp > 0.0f ? launch<D, true, BIDIR, LSE>(p, stream) : launch<D, false, BIDIR, LSE>(p, stream);
+}
+
+template <int D, bool BIDIR>
+hipError_t launch_d(const FwdParams &p, hipStream_t stream) {
+    return p.lse ? launch_l<D, BIDIR, true>(p, stream) : launch_l<D, BIDIR, false>(p, stream);
 }
 
 }  // namespace
 
 hipError_t launch_forward_bf16(const FwdParams &p, hipStream_t stream) {
-    const bool clamp = p.clamp > 0.0f;
-    if (p.D == 64) return clamp ? launch<64, true>(p, stream) : launch<64, false>(p, stream);
-    return clamp ? launch<128, true>(p, stream) : launch<128, false>(p, stream);
+    if (p.D == 64) return p.causal ? launch_d<64, false>(p, stream) : launch_d<64, true>(p, stream);
+    return p.causal ? launch_d<128, false>(p, stream) : launch_d<128, true>(p, stream);
 }
 
 }  // namespace pi_attn

@@ -21,6 +21,7 @@ inline hipError_t launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block,
 
 struct FwdParams {
     int B, H, N, D, k, pi;
+    int causal;                     // 1: causal window and t - pi; 0: bidirectional, t -/+ pi
     const void *q, *k_ptr, *v;
     int64_t sb, sh, sn;             // element strides shared by q, k, v
     const float *gate;
@@ -54,7 +55,7 @@ struct BwdParams {
     float *dgate, *rowterm;         // [B][H][N] contiguous
 };
 
-hipError_t launch_index_set(int n, int k, int pi, int32_t *idx, hipStream_t stream);
+hipError_t launch_index_set(int n, int k, int pi, bool causal, int32_t *idx, hipStream_t stream);
 
 // Reference-style fp32 kernels: one wavefront per query, W_t visited entry by
 // entry with an online softmax.  Correctness path for float32 data.

@@ -13,12 +13,16 @@ constexpr float kGateEps = 1e-4f;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-// Window N_r(t) (Sec. 3.2, eq. Nr, causal): j in [window_lo(t,k), t].
+// Window N_r(t) (Sec. 3.2, eq. Nr): j in [window_lo, window_hi], where the
+// causal window ends at t and the bidirectional one at min(t + k, n - 1).
 __host__ __device__ inline int window_lo(int t, int k) { return t - k > 0 ? t - k : 0; }
 
-__host__ __device__ inline bool in_window(int j, int t, int k) { return j <= t && j >= t - k && j >= 0; }
+__host__ __device__ inline int window_hi(int t, int k, int n, bool causal) {
+    if (causal) return t;
+    return k >= n - 1 - t ? n - 1 : t + k;
+}
 
-// A partner slot exists only when t - pi can lie outside the window.
+// Partner slots exist only when t -/+ pi can lie outside the window.
 __host__ __device__ inline bool partner_enabled(int k, int pi) { return pi > k; }
 
 // Partner N_pi(t) = {t - pi} (Sec. 3.4, eq. Npi); -1 when absent.
@@ -26,16 +30,32 @@ __host__ __device__ inline int partner_of(int t, int k, int pi) {
     return (partner_enabled(k, pi) && t >= pi) ? t - pi : -1;
 }
 
-// Slots per query: k+1 window slots (offsets -k..0) then the partner slot.
-__host__ __device__ inline int ws_width(int k, int pi) { return k + 1 + (partner_enabled(k, pi) ? 1 : 0); }
+// The second partner t + pi of the bidirectional mode (App. B,
+// hyper-parameter table); -1 when absent.
+__host__ __device__ inline int partner_fwd_of(int t, int k, int pi, int n) {
+    return (partner_enabled(k, pi) && pi < n - t) ? t + pi : -1;
+}
 
-// Slot s of W_t in the exported layout; -1 for an absent entry.
-__host__ __device__ inline int ws_slot(int t, int s, int k, int pi) {
-    if (s <= k) {
-        int j = t - k + s;
-        return j >= 0 ? j : -1;
+// Window slots per query: offsets -k..0 (causal) or -k..k (bidirectional).
+__host__ __device__ inline int64_t window_slots(int k, bool causal) {
+    return causal ? (int64_t)k + 1 : 2 * (int64_t)k + 1;
+}
+
+// Slots per query: the window slots, then t - pi, then (bidirectional) t + pi.
+__host__ __device__ inline int64_t ws_width(int k, int pi, bool causal) {
+    return window_slots(k, causal) + (partner_enabled(k, pi) ? (causal ? 1 : 2) : 0);
+}
+
+// Slot s of W_t (sequence length n) in the exported layout; -1 for an
+// absent entry.  Requires ws_width(k, pi, causal) to fit in int.
+__host__ __device__ inline int ws_slot(int t, int s, int k, int pi, int n, bool causal) {
+    const int nw = (int)window_slots(k, causal);
+    if (s < nw) {
+        const int j = t - k + s;
+        return (j >= 0 && j < n) ? j : -1;
     }
-    return partner_of(t, k, pi);
+    if (s == nw) return partner_of(t, k, pi);
+    return partner_fwd_of(t, k, pi, n);
 }
 
 // Per-query fusion biases, natural-log units.

@@ -50,13 +50,20 @@ def test_ws_width(lib, k, pi, m):
     assert pa.pi_attn_ws_width(k, pi) == m
 
 
+@pytest.mark.parametrize("k,pi,m", [(0, 0, 1), (4, 16, 11), (4, 4, 9), (4, 3, 9), (512, 1024, 1027),
+                                    (0, 1, 3), (-1, 2, -1), (2, -1, -1), (1 << 30, (1 << 30) + 1, -1)])
+def test_ws_width_bidirectional(lib, k, pi, m):
+    assert pa.pi_attn_ws_width(k, pi, causal=False) == m
+
+
 def fwd(lib, **kw):
-    a = dict(dtype=1, B=1, H=2, N=256, D=64, k=32, pi=64, q=16, kk=16, v=16, sb=32768, sh=16384, sn=64,
-             gate=16, gsb=0, gsh=1, gsn=0, scale=0.125, clamp=0.0, out=16, osb=32768, osh=16384, osn=64,
+    a = dict(dtype=1, B=1, H=2, N=256, D=64, k=32, pi=64, causal=1, q=16, kk=16, v=16, sb=32768, sh=16384,
+             sn=64, gate=16, gsb=0, gsh=1, gsn=0, scale=0.125, clamp=0.0, out=16, osb=32768, osh=16384, osn=64,
              lse=None, stream=None)
     a.update(kw)
     vp = lambda x: None if x is None else ctypes.c_void_p(x)
-    return lib.pi_attn_forward(a["dtype"], a["B"], a["H"], a["N"], a["D"], a["k"], a["pi"], vp(a["q"]),
+    return lib.pi_attn_forward(a["dtype"], a["B"], a["H"], a["N"], a["D"], a["k"], a["pi"], a["causal"],
+                               vp(a["q"]),
                                vp(a["kk"]), vp(a["v"]), a["sb"], a["sh"], a["sn"], vp(a["gate"]), a["gsb"],
                                a["gsh"], a["gsn"], a["scale"], a["clamp"], vp(a["out"]), a["osb"], a["osh"],
                                a["osn"], vp(a["lse"]), vp(a["stream"]))
@@ -74,6 +81,8 @@ def fwd(lib, **kw):
     # bf16: one query tile's (min(k, N) + 256) key rows must span < 2 GiB
     (dict(sn=1 << 22, sh=1 << 32, sb=1 << 33, k=32), EUNSUP),
     (dict(N=1 << 16, k=1 << 16, sn=1 << 14, sh=1 << 30, sb=1 << 31), EUNSUP),
+    # bidirectional: (2 min(k, N) + 256) rows
+    (dict(causal=0, N=1 << 16, k=40000, sn=1 << 14, sh=1 << 30, sb=1 << 31), EUNSUP),
 ])
 def test_forward_rejects(lib, kw, code):
     assert fwd(lib, **kw) == code
@@ -85,12 +94,13 @@ def test_forward_empty_is_noop(lib, kw):
 
 
 def bwd(lib, **kw):
-    a = dict(dtype=1, B=1, H=2, N=256, D=64, k=32, pi=64, q=16, kk=16, v=16, sb=32768, sh=16384, sn=64,
-             gate=16, gsb=0, gsh=1, gsn=0, scale=0.125, clamp=0.0, lse=16, out=16, dout=16, osb=32768, osh=16384,
-             osn=64, dq=16, dk=16, dv=16, dg=16, rt=16, stream=None)
+    a = dict(dtype=1, B=1, H=2, N=256, D=64, k=32, pi=64, causal=1, q=16, kk=16, v=16, sb=32768, sh=16384,
+             sn=64, gate=16, gsb=0, gsh=1, gsn=0, scale=0.125, clamp=0.0, lse=16, out=16, dout=16, osb=32768,
+             osh=16384, osn=64, dq=16, dk=16, dv=16, dg=16, rt=16, stream=None)
     a.update(kw)
     vp = lambda x: None if x is None else ctypes.c_void_p(x)
-    return lib.pi_attn_backward(a["dtype"], a["B"], a["H"], a["N"], a["D"], a["k"], a["pi"], vp(a["q"]),
+    return lib.pi_attn_backward(a["dtype"], a["B"], a["H"], a["N"], a["D"], a["k"], a["pi"], a["causal"],
+                                vp(a["q"]),
                                 vp(a["kk"]), vp(a["v"]), a["sb"], a["sh"], a["sn"], vp(a["gate"]), a["gsb"],
                                 a["gsh"], a["gsn"], a["scale"], a["clamp"], vp(a["lse"]), vp(a["out"]), vp(a["dout"]),
                                 a["osb"], a["osh"], a["osn"], vp(a["dq"]), vp(a["dk"]), vp(a["dv"]),
@@ -104,6 +114,7 @@ def bwd(lib, **kw):
     (dict(dv=None), EINVAL), (dict(dg=None), EINVAL), (dict(rt=None), EINVAL), (dict(q=None), EINVAL),
     (dict(lse=18), EINVAL), (dict(dq=20), EINVAL), (dict(dout=24), EINVAL), (dict(osn=4), EINVAL),
     (dict(scale=0.0), EINVAL), (dict(clamp=float("nan")), EINVAL), (dict(gsh=-1), EINVAL),
+    (dict(causal=0, N=1 << 16, k=40000, sn=1 << 14, sh=1 << 30, sb=1 << 31), EUNSUP),
 ])
 def test_backward_rejects(lib, kw, code):
     assert bwd(lib, **kw) == code
@@ -140,14 +151,17 @@ def test_decode_empty_is_noop(lib, kw):
     assert dec(lib, **kw) == 0
 
 
-def test_index_set_rejects(lib):
-    assert lib.pi_attn_index_set(-1, 2, 3, ctypes.c_void_p(16), None) == EINVAL
-    assert lib.pi_attn_index_set(5, -2, 3, ctypes.c_void_p(16), None) == EINVAL
-    assert lib.pi_attn_index_set(5, 2, -3, ctypes.c_void_p(16), None) == EINVAL
-    assert lib.pi_attn_index_set(5, 2, 3, None, None) == EINVAL
-    assert lib.pi_attn_index_set(5, 2, 3, ctypes.c_void_p(2), None) == EINVAL
-    assert lib.pi_attn_index_set(1 << 30, 8, 16, ctypes.c_void_p(16), None) == EINVAL
-    assert lib.pi_attn_index_set(0, 2, 3, None, None) == 0
+@pytest.mark.parametrize("causal", [1, 0])
+def test_index_set_rejects(lib, causal):
+    assert lib.pi_attn_index_set(-1, 2, 3, causal, ctypes.c_void_p(16), None) == EINVAL
+    assert lib.pi_attn_index_set(5, -2, 3, causal, ctypes.c_void_p(16), None) == EINVAL
+    assert lib.pi_attn_index_set(5, 2, -3, causal, ctypes.c_void_p(16), None) == EINVAL
+    assert lib.pi_attn_index_set(5, 2, 3, causal, None, None) == EINVAL
+    assert lib.pi_attn_index_set(5, 2, 3, causal, ctypes.c_void_p(2), None) == EINVAL
+    assert lib.pi_attn_index_set(1 << 30, 8, 16, causal, ctypes.c_void_p(16), None) == EINVAL
+    if not causal:   # n * (2k + 3) entries pass 2^31 where n * (k + 2) does not
+        assert lib.pi_attn_index_set(1 << 27, 8, 16, causal, ctypes.c_void_p(16), None) == EINVAL
+    assert lib.pi_attn_index_set(0, 2, 3, causal, None, None) == 0
 
 
 def test_binding_refuses_cpu_tensors(lib):

@@ -1,0 +1,241 @@
+"""GPU parity of the bidirectional mode (window |j - t| <= k, partners t - pi
+and t + pi; eq. Nr bidirectional case, App. B hyper-parameter table) against
+the fp64 oracle, through the C ABI, with the bars of the causal tests:
+index sets bit-exact, float32 max-abs <= 1e-4, bfloat16 max-abs <= 2e-2 and
+relative L2 <= 5e-3, gradients as in the causal backward tests.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2511_10696_amd as pa
+from paper_2511_10696_amd import workloads as W
+from tests.oracle_pins import BIDIR_IDX_CASES
+from tests.test_gpu_backward import assert_grad
+from tests.test_gpu_parity import LSE_TOL, assert_close, np32
+
+pytestmark = pytest.mark.gpu
+
+
+def run_forward(q, k, v, gate, kw, pi, **kw2):
+    out, lse = pa.pi_attn_forward(q, k, v, gate, kw, pi, return_lse=True, causal=False, **kw2)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+def rand_inputs(B, H, N, D, dtype, seed, per_query_gate=False):
+    cfg = W.ForwardConfig("custom", B, H, N, D, 0, 0, dtype)
+    return W.forward_inputs(cfg, seed, "cuda", per_query_gate)
+
+
+@pytest.mark.parametrize("n,k,pi", BIDIR_IDX_CASES + [(256, 32, 64), (4096, 128, 256), (32768, 512, 1024),
+                                                      (1000, 0, 0), (70, 70, 3), (33, 16, 17)])
+def test_index_set_bit_exact(device, n, k, pi):
+    got = pa.pi_attn_index_set(n, k, pi, causal=False).cpu().numpy()
+    ref = oracle.index_set(n, k, pi, causal=False)
+    assert got.dtype == np.int32 and np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_forward_f32_tiny(device, seed):
+    cfg = W.FORWARD["tiny"]
+    q, k, v, gate = W.forward_inputs(cfg, seed, device)
+    out, lse = run_forward(q, k, v, gate, cfg.k, cfg.pi)
+    ref, lref = oracle.forward(q, k, v, gate, cfg.k, cfg.pi, want_lse=True, causal=False)
+    assert_close(np32(out), ref, torch.float32, "tiny")
+    assert np.abs(np32(lse) - lref).max() <= LSE_TOL
+
+
+@pytest.mark.parametrize("B,H,N,D,k,pi", [(1, 2, 70, 128, 5, 13), (2, 1, 33, 64, 0, 0), (1, 1, 40, 64, 7, 3),
+                                          (1, 2, 50, 128, 60, 7), (1, 1, 1, 64, 4, 16), (1, 1, 30, 64, 2, 29)])
+def test_forward_f32_shapes(device, B, H, N, D, k, pi):
+    q, k_, v, gate = rand_inputs(B, H, N, D, torch.float32, 5, per_query_gate=True)
+    out, lse = run_forward(q, k_, v, gate, k, pi)
+    ref, lref = oracle.forward(q, k_, v, gate, k, pi, want_lse=True, causal=False)
+    assert_close(np32(out), ref, torch.float32)
+    assert np.abs(np32(lse) - lref).max() <= LSE_TOL
+
+
+BF16_SHAPES = [
+    (1, 2, 300, 64, 37, 100),       # several query tiles, ragged tail
+    (2, 3, 517, 128, 64, 129),
+    (1, 2, 640, 128, 130, 260),     # band wider than one tile on each side
+    (1, 1, 1, 64, 4, 16),           # single position
+    (1, 1, 127, 128, 4, 16),        # less than one tile, small k (paper default)
+    (1, 2, 200, 64, 0, 0),          # self only
+    (1, 2, 333, 128, 40, 40),       # pi == k: no partner slots
+    (1, 1, 300, 64, 299, 17),       # k >= N-1: dense
+    (1, 1, 257, 128, 5, 256),       # t - pi only for the last row, t + pi only for the first
+    (2, 2, 1100, 64, 100, 1000),    # partner period beyond several tiles
+    (1, 2, 160, 128, 3, 80),        # every row has exactly one partner
+]
+
+
+@pytest.mark.parametrize("B,H,N,D,k,pi", BF16_SHAPES)
+@pytest.mark.parametrize("per_query_gate", [False, True])
+def test_forward_bf16_shapes(device, B, H, N, D, k, pi, per_query_gate):
+    q, k_, v, gate = rand_inputs(B, H, N, D, torch.bfloat16, 7, per_query_gate)
+    out, lse = run_forward(q, k_, v, gate, k, pi)
+    ref, lref = oracle.forward(q, k_, v, gate, k, pi, want_lse=True, causal=False)
+    assert_close(np32(out), ref, torch.bfloat16, f"{(B, H, N, D, k, pi)}")
+    assert np.abs(np32(lse) - lref).max() <= LSE_TOL
+
+
+def test_forward_bf16_self_only_is_exact(device):
+    q, k, v, gate = rand_inputs(1, 2, 300, 128, torch.bfloat16, 3)
+    out, _ = run_forward(q, k, v, gate, 0, 0)
+    assert torch.equal(out, v)
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_forward_bf16_config_4k(device, seed):
+    cfg = W.FORWARD["fwd4k"]
+    q, k, v, gate = W.forward_inputs(cfg, seed, device)
+    out, lse = run_forward(q, k, v, gate, cfg.k, cfg.pi)
+    ref, lref = oracle.forward(q, k, v, gate, cfg.k, cfg.pi, want_lse=True, causal=False)
+    assert_close(np32(out), ref, torch.bfloat16, "fwd4k bidirectional")
+    assert np.abs(np32(lse) - lref).max() <= LSE_TOL
+
+
+def sampled_rows(cfg, rng):
+    """Every query of two seeded (b, h) pairs; in every head the first and
+    the last pi + 256 rows (where a partner or the window is cut off) and
+    256 rows at query-tile boundaries."""
+    B, H, N = cfg.B, cfg.H, cfg.N
+    bh = rng.choice(B * H, size=2, replace=False)
+    rows = [np.arange(N) + x * N for x in bh]
+    ends = np.concatenate([np.arange(min(N, cfg.pi + 256)), np.arange(max(0, N - cfg.pi - 256), N)])
+    bounds = np.unique(np.concatenate([np.arange(0, N, 128), np.arange(127, N, 128),
+                                       np.arange(63, N, 128), np.arange(64, N, 128)]))
+    bounds = rng.choice(bounds, size=min(256, bounds.size), replace=False)
+    for x in range(B * H):
+        rows.append(ends + x * N)
+        rows.append(bounds + x * N)
+    return np.unique(np.concatenate(rows))
+
+
+@pytest.mark.parametrize("name", ["fwd16k", "fwd32k"])
+def test_forward_bf16_config_sampled(device, name):
+    cfg = W.FORWARD[name]
+    q, k, v, gate = W.forward_inputs(cfg, 0, device)
+    out, lse = run_forward(q, k, v, gate, cfg.k, cfg.pi)
+    rows = sampled_rows(cfg, np.random.default_rng(0))
+    ref, lref = oracle.forward(q, k, v, gate, cfg.k, cfg.pi, rows=rows, want_lse=True, causal=False)
+    assert_close(np32(out).reshape(-1, cfg.D)[rows], ref, torch.bfloat16, name)
+    assert np.abs(np32(lse).reshape(-1)[rows] - lref).max() <= LSE_TOL
+
+
+@pytest.mark.parametrize("kw", [dict(k=32767, pi=1024), dict(k=512, pi=0)])
+def test_forward_bf16_dense_and_local_only(device, kw):
+    """Dense bidirectional attention (k = N-1) and window-only (pi = 0) at the 32K shape."""
+    cfg = W.FORWARD["fwd32k"]
+    q, k, v, gate = W.forward_inputs(cfg, 1, device)
+    out, lse = run_forward(q, k, v, gate, kw["k"], kw["pi"])
+    rng = np.random.default_rng(1)
+    rows = np.unique(np.concatenate([rng.choice(cfg.B * cfg.H * cfg.N, 256, replace=False),
+                                     np.arange(130), cfg.N - 1 - np.arange(130)]))
+    ref, lref = oracle.forward(q, k, v, gate, kw["k"], kw["pi"], rows=rows, want_lse=True, causal=False)
+    assert_close(np32(out).reshape(-1, cfg.D)[rows], ref, torch.bfloat16)
+    assert np.abs(np32(lse).reshape(-1)[rows] - lref).max() <= LSE_TOL
+
+
+def test_forward_bf16_logit_clamp(device):
+    cfg = W.ForwardConfig("hh", 1, 2, 700, 128, 50, 120, torch.bfloat16, heavy_frac=0.05, heavy_mult=8.0)
+    q, k, v, gate = W.forward_inputs(cfg, 2, device, per_query_gate=True)
+    for clamp in (20.0, 3.0):
+        out, lse = run_forward(q, k, v, gate, cfg.k, cfg.pi, logit_clamp=clamp, scale=0.5)
+        ref, lref = oracle.forward(q, k, v, gate, cfg.k, cfg.pi, scale=0.5, clamp=clamp, want_lse=True,
+                                   causal=False)
+        assert_close(np32(out), ref, torch.bfloat16, f"clamp {clamp}")
+        assert np.abs(np32(lse) - lref).max() <= LSE_TOL * 10
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_forward_locality(device, dtype):
+    """Rows t whose working set ends before `cut` (t + max(k, pi) < cut) are
+    bit-identical when every row from `cut` on is replaced by large finite
+    values: the kernels may read such rows, but their weights are exactly 0."""
+    B, H, N, D, k, pi = 1, 2, 700, 128, 40, 150
+    q, kk, v, gate = rand_inputs(B, H, N, D, dtype, 11)
+    base, _ = run_forward(q, kk, v, gate, k, pi)
+    for cut in (200, 383, 600):
+        q2, k2, v2 = q.clone(), kk.clone(), v.clone()
+        for x in (q2, k2, v2):
+            x[:, :, cut:] = 1e4
+        out, _ = run_forward(q2, k2, v2, gate, k, pi)
+        keep = cut - max(k, pi)
+        assert torch.equal(out[:, :, :keep], base[:, :, :keep]), cut
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_forward_deterministic(device, dtype):
+    q, k, v, gate = rand_inputs(2, 4, 1000, 128, dtype, 12)
+    a, la = run_forward(q, k, v, gate, 100, 300)
+    b, lb = run_forward(q, k, v, gate, 100, 300)
+    assert torch.equal(a, b) and torch.equal(la, lb)
+
+
+# ---------------------------------------------------------------------------
+# backward
+# ---------------------------------------------------------------------------
+def run_backward_case(q, k, v, gate, kw, pi, seed, clamp=0.0, scale=None):
+    out, lse = pa.pi_attn_forward(q, k, v, gate, kw, pi, return_lse=True, logit_clamp=clamp, scale=scale,
+                                  causal=False)
+    dout = W.cotangent(q.shape, q.dtype, seed, q.device)
+    dq, dk, dv, dg = pa.pi_attn_backward(q, k, v, gate, kw, pi, out, lse, dout, logit_clamp=clamp, scale=scale,
+                                         gate_grad_per_query=True, causal=False)
+    torch.cuda.synchronize()
+    rq, rk, rv, rg = oracle.backward(q, k, v, gate, kw, pi, dout, scale=scale, clamp=clamp, causal=False)
+    for name, got, ref in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv), ("dgate", dg, rg)):
+        assert_grad(np32(got), ref, name, q.dtype)
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_backward_f32_tiny(device, seed):
+    cfg = W.FORWARD["tiny"]
+    q, k, v, gate = W.forward_inputs(cfg, seed, device)
+    run_backward_case(q, k, v, gate, cfg.k, cfg.pi, seed)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("B,H,N,D,k,pi,pq", [
+    (1, 2, 300, 64, 32, 64, False),      # several tiles, ragged tail
+    (1, 2, 200, 128, 16, 40, True),      # D = 128, per-query gate
+    (2, 1, 130, 64, 5, 3, False),        # pi <= k: no partner slots
+    (1, 2, 70, 128, 100, 7, True),       # k >= N: dense
+    (1, 1, 1, 64, 4, 16, False),         # a single position
+    (1, 1, 40, 64, 0, 0, False),         # k = 0: self only
+    (1, 1, 45, 64, 3, 44, True),         # partners only for the first and last positions
+    (1, 2, 400, 128, 20, 170, True),     # partner tiles on both sides of a key tile
+])
+def test_backward_shapes(device, dtype, B, H, N, D, k, pi, pq):
+    q, kk, v, gate = rand_inputs(B, H, N, D, dtype, 7, pq)
+    run_backward_case(q, kk, v, gate, k, pi, 7)
+
+
+def test_backward_bf16_mid(device):
+    """One D = 128 head pair at the 32K workload's window and period."""
+    q, kk, v, gate = rand_inputs(1, 2, 4096, 128, torch.bfloat16, 3)
+    run_backward_case(q, kk, v, gate, 512, 1024, 3)
+
+
+def test_backward_bf16_fwd4k(device):
+    cfg = W.FORWARD["fwd4k"]
+    q, kk, v, gate = W.forward_inputs(cfg, 0, device)
+    run_backward_case(q, kk, v, gate, cfg.k, cfg.pi, 0)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_backward_clamp(device, dtype):
+    """Clamp on, with the causal test's placement of gate and clamp (no fused
+    logit within 1e-3 of +-clamp on the 1/128 score grid)."""
+    from tests.test_gpu_backward import _clamp_placement
+    B, H, N, D, kw, pi = 1, 2, 150, 64, 20, 33
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    q, kk, v = (torch.randint(-8, 9, (B, H, N, D), generator=gen, device="cuda").float().div(4).to(dtype)
+                for _ in range(3))
+    margin, g, clamp = _clamp_placement()
+    assert margin > 1e-3
+    gate = torch.full((H,), g, device="cuda")
+    run_backward_case(q, kk, v, gate, kw, pi, 5, clamp=clamp, scale=0.125)
