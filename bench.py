@@ -6,9 +6,15 @@ Workload (the metric's configuration): full-sequence causal forward, B=1,
 H=32, N=32768, D=128, k=512, pi=1024, bf16 q/k/v ~ N(0,1), per-head gate
 logits ~ U(-1,1).  One step = one pi_attn_forward over the whole sequence.
 Also timed in the same run: the KV-cached decode step (64 sequences, 32
-heads, 32768 cached rows, k=512, pi=1024, 1000 consecutive steps), and the
-fp64 CPU oracle on a bounded sample of the forward workload, and the
-backward (pi_attn_backward) on the forward workload with a seeded dL/dy.
+heads, 32768 cached rows, k=512, pi=1024, 1000 consecutive steps), the
+bidirectional forward on the same shape, the backward (pi_attn_backward,
+causal and bidirectional) on that shape with a seeded dL/dy, and the fp64
+CPU oracle on a bounded sample of the forward workload.
+
+Every timed loop is preceded by a settling phase (the same launches, untimed,
+for at least SETTLE_S seconds, so the GPU clocks have left their idle state)
+and by the warm-up launches; the timed region is exactly the stated number
+of launches between two HIP events on the launch stream.
 
 Prints ONE JSON line.  value = query positions per second (B*N per step) of
 the forward, inputs resident in HBM.
@@ -29,35 +35,48 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "forward_bf16_fwd32k_hbm_traffic.txt")
 DECODE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_bf16_s64_hbm_traffic.txt")
+BIDIR_TRAFFIC = os.path.join(ROOT, "profiles", "forward_bf16_bidir_fwd32k_hbm_traffic.txt")
+BACKWARD_TRAFFIC = {True: os.path.join(ROOT, "profiles", "backward_bf16_fwd32k_hbm_traffic.txt"),
+                    False: os.path.join(ROOT, "profiles", "backward_bf16_bidir_fwd32k_hbm_traffic.txt")}
+FORWARD_SOURCES = ("forward_bf16.hip", "pi_common.h", "kernels.h")
+BACKWARD_SOURCES = ("backward_bf16.hip", "backward_kv_bf16.hip", "backward.hip", "pi_common.h", "kernels.h")
+
+
+def csrc_digest(names):
+    return source_digest([os.path.join(ROOT, "paper_2511_10696_amd", "csrc", f) for f in names])
 COPY_PROBE_BYTES = 1 << 30      # plain device copy used to calibrate the HBM byte counters
+SETTLE_S = 0.3                  # untimed run-in before each timed loop (clock ramp)
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--decode-steps", type=int, default=1000)
     ap.add_argument("--no-decode", action="store_true")
-    ap.add_argument("--backward-steps", type=int, default=3)
+    ap.add_argument("--backward-steps", type=int, default=20)
     ap.add_argument("--no-backward", action="store_true")
+    ap.add_argument("--no-bidirectional", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pmc-probe", action="store_true",
-                    help="run 3 forward launches, 3 decode steps and 3 plain 1 GiB device copies, "
-                         "then exit (for hardware-counter runs)")
+                    help="run 3 launches of each timed kernel (forward, bidirectional forward, backward "
+                         "both ways, decode step) and 3 plain 1 GiB device copies, then exit (for "
+                         "hardware-counter runs)")
     return ap.parse_args()
 
 
-def forward_algorithmic(cfg):
-    """Algorithmic work of one forward: attended keys, FLOPs (QK + PV, 2 FLOP
-    per MAC), bytes (q, k, v read once, out written once)."""
+def forward_algorithmic(cfg, causal=True):
+    """Algorithmic work of one forward: attended keys (sum of |W_t|, closed
+    form), FLOPs (QK + PV, 2 FLOP per MAC), bytes (q, k, v read once, out
+    written once)."""
     n, k, pi = cfg.N, cfg.k, cfg.pi
-    if n > k:
-        keys = (k + 1) * (k + 2) // 2 + (n - k - 1) * (k + 1)
+    if causal:
+        keys = (k + 1) * (k + 2) // 2 + (n - k - 1) * (k + 1) if n > k else n * (n + 1) // 2
+        keys += max(0, n - pi) if pi > k else 0
     else:
-        keys = n * (n + 1) // 2
-    if pi > k:
-        keys += max(0, n - pi)
+        keys = n * (2 * k + 1) - k * (k + 1) if n > k else n * n
+        keys += 2 * max(0, n - pi) if pi > k else 0
     keys *= cfg.B * cfg.H
     flops = 4 * cfg.D * keys
     es = 2
@@ -65,12 +84,53 @@ def forward_algorithmic(cfg):
     return keys, flops, nbytes
 
 
-def backward_algorithmic(cfg):
+def time_launches(torch, fn, steps, warmup, stream):
+    """Settle (>= SETTLE_S s of fn, untimed), `warmup` more launches, then
+    exactly `steps` launches between two HIP events on `stream`.  Returns
+    (ms per launch, wall seconds of the timed region, settle seconds)."""
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < SETTLE_S:
+        for _ in range(4):
+            fn()
+        torch.cuda.synchronize()
+    settle = time.perf_counter() - t0
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    return e0.elapsed_time(e1) / steps, t_wall, settle
+
+
+def roofline_of(flops, nbytes, sec, kernel, traffic=None):
+    """Roofline record of one launch: the bound is whichever of the HBM and
+    MFMA times of its algorithmic work is larger."""
+    tflops, gbs = flops / sec / 1e12, nbytes / sec / 1e9
+    hbm = nbytes / (HBM_PEAK_GBS * 1e9) >= flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
+    r = {"bound": "hbm" if hbm else "mfma", "kernel": kernel,
+         "achieved": round(gbs if hbm else tflops, 2),
+         "peak": HBM_PEAK_GBS if hbm else MFMA_BF16_PEAK_TFLOPS,
+         "unit": "GB/s" if hbm else "TFLOP/s",
+         "frac": round((gbs / HBM_PEAK_GBS) if hbm else (tflops / MFMA_BF16_PEAK_TFLOPS), 4),
+         "traffic": traffic}
+    mf = {"achieved": round(tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+          "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "flops_per_launch": flops,
+          "bytes_per_launch": nbytes}
+    return r, mf
+
+
+def backward_algorithmic(cfg, causal=True):
     """Algorithmic work of one backward: per attended key 10*D FLOPs (the
     scores recomputed, dP = dO V^T, dV, dQ and dK: five D-long products,
     2 FLOP per MAC); bytes: q, k, v, dO read once (input dtype), lse read,
     dq, dk, dv (float32) and the per-query gate gradient written."""
-    keys, _, _ = forward_algorithmic(cfg)
+    keys, _, _ = forward_algorithmic(cfg, causal)
     rows = cfg.B * cfg.H * cfg.N
     nbytes = rows * (4 * cfg.D * 2 + 3 * cfg.D * 4 + 4 + 4)
     return keys, 10 * cfg.D * keys, nbytes
@@ -119,7 +179,19 @@ def pmc_probe(W, pa, torch, dev):
         pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi, out=out)
     torch.cuda.synchronize()
     print(f"probe: 3 x forward fwd32k", flush=True)
-    del q, k, v, out
+    for _ in range(3):
+        pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi, out=out, causal=False)
+    torch.cuda.synchronize()
+    print(f"probe: 3 x bidirectional forward fwd32k", flush=True)
+    dout = W.cotangent(q.shape, q.dtype, 0, dev)
+    for causal in (True, False):
+        y, lse = pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi, return_lse=True, causal=causal)
+        for _ in range(3):
+            pa.pi_attn_backward(q, k, v, gate, cfg.k, cfg.pi, y, lse, dout, causal=causal)
+        torch.cuda.synchronize()
+        print(f"probe: 3 x backward fwd32k causal={causal}", flush=True)
+        del y, lse
+    del q, k, v, out, dout
     dcfg = W.DECODE["decode"]
     kc, vc, lens, dgate = W.decode_state(dcfg, 0, dev)
     qs, ks, vs = W.decode_tokens(dcfg, 3, 1, dev)
@@ -155,51 +227,40 @@ def main():
     if args.pmc_probe:
         pmc_probe(W, pa, torch, dev)
         return
+    stream = torch.cuda.current_stream(dev)
     cfg = W.FORWARD["fwd32k"]
     q, k, v, gate = W.forward_inputs(cfg, 0, dev)
     out = torch.empty_like(q)
-    keys, flops, nbytes = forward_algorithmic(cfg)
 
-    def step():
-        pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi, out=out)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    stream = torch.cuda.current_stream(dev)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t_wall = time.perf_counter()
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    ms = e0.elapsed_time(e1) / args.steps
+    # ---- causal forward (the metric) ---------------------------------------
+    ms, t_wall, settle = time_launches(
+        torch, lambda: pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi, out=out), args.steps, args.warmup, stream)
     sec = ms / 1e3
     value = cfg.B * cfg.N / sec
+    keys, flops, nbytes = forward_algorithmic(cfg)
+    digest = csrc_digest(FORWARD_SOURCES)
+    roofline, roofline_mfma = roofline_of(flops, nbytes, sec, "forward_bf16_kernel<128,false,false,false>",
+                                          measured_traffic(digest))
 
-    src = [os.path.join(ROOT, "paper_2511_10696_amd", "csrc", f)
-           for f in ("forward_bf16.hip", "pi_common.h", "kernels.h")]
-    digest = source_digest(src)
-    traffic = measured_traffic(digest)
-    hbm_gbs = nbytes / sec / 1e9
-    tflops = flops / sec / 1e12
-    t_hbm = nbytes / (HBM_PEAK_GBS * 1e9)
-    t_mfma = flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
-    roofline = {"bound": "hbm" if t_hbm >= t_mfma else "mfma",
-                "kernel": "forward_bf16_kernel<128>",
-                "achieved": round(hbm_gbs if t_hbm >= t_mfma else tflops, 2),
-                "peak": HBM_PEAK_GBS if t_hbm >= t_mfma else MFMA_BF16_PEAK_TFLOPS,
-                "unit": "GB/s" if t_hbm >= t_mfma else "TFLOP/s",
-                "traffic": traffic}
-    roofline["frac"] = round(roofline["achieved"] / roofline["peak"], 4)
-    roofline_mfma = {"achieved": round(tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
-                     "flops_per_launch": flops, "bytes_per_launch": nbytes}
+    # ---- bidirectional forward, same shape ----------------------------------
+    bidir = None
+    if not args.no_bidirectional:
+        bms, _, _ = time_launches(
+            torch, lambda: pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi, out=out, causal=False),
+            args.steps, args.warmup, stream)
+        bkeys, bflops, bbytes = forward_algorithmic(cfg, causal=False)
+        brl, bmf = roofline_of(bflops, bbytes, bms / 1e3, "forward_bf16_kernel<128,false,true,false>",
+                               measured_traffic(digest, BIDIR_TRAFFIC))
+        bidir = {"workload": "fwd32k bidirectional: B1 H32 N32768 D128 k512 pi1024 bf16 (window |j-t|<=k, "
+                             "partners t-pi and t+pi)",
+                 "steps": args.steps, "ms_per_step": round(bms, 5),
+                 "query_positions_per_s": round(cfg.B * cfg.N / (bms / 1e3), 1),
+                 "attended_keys_per_s": round(bkeys / (bms / 1e3), 1),
+                 "roofline": brl, "roofline_mfma": bmf}
     del q, k, v, out
     torch.cuda.empty_cache()
 
+    # ---- decode step --------------------------------------------------------
     decode = None
     if not args.no_decode:
         dcfg = W.DECODE["decode"]
@@ -208,17 +269,22 @@ def main():
         qs, ks, vs = W.decode_tokens(dcfg, nsteps, 1, dev)
         lbuf = [lens, torch.empty_like(lens)]
         dout = torch.empty((dcfg.S, dcfg.H, dcfg.D), dtype=dcfg.dtype, device=dev)
-        # warm-up on a scratch copy of the lengths: the timed loop starts from cache_len
+        # settle and warm up on a scratch copy of the lengths (row cache_len is
+        # rewritten by every such step); the timed loop starts from cache_len
         warm_len = [lens.clone(), torch.empty_like(lens)]
-        for i in range(3):
-            pa.pi_attn_decode_step(warm_len[i % 2], qs[i], ks[i], vs[i], kc, vc, dgate, dcfg.k, dcfg.pi,
-                                   len_out=warm_len[(i + 1) % 2], out=dout)
-        torch.cuda.synchronize()
-        d0, d1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        d0.record(stream)
-        for i in range(nsteps):
+        time_launches(torch, lambda: pa.pi_attn_decode_step(warm_len[0], qs[0], ks[0], vs[0], kc, vc, dgate, dcfg.k,
+                                                            dcfg.pi, len_out=warm_len[1], out=dout), 1, 3, stream)
+        si = [0]
+
+        def step():
+            i = si[0]
             pa.pi_attn_decode_step(lbuf[i % 2], qs[i], ks[i], vs[i], kc, vc, dgate, dcfg.k, dcfg.pi,
                                    len_out=lbuf[(i + 1) % 2], out=dout)
+            si[0] += 1
+        d0, d1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        d0.record(stream)
+        for _ in range(nsteps):
+            step()
         d1.record(stream)
         torch.cuda.synchronize()
         dms = d0.elapsed_time(d1) / nsteps
@@ -237,9 +303,12 @@ def main():
         del kc, vc, qs, ks, vs
         torch.cuda.empty_cache()
 
-    backward = None
+    # ---- backward -----------------------------------------------------------
+    backward = backward_bidir = None
     if not args.no_backward:
-        backward = bench_backward(cfg, W, pa, torch, dev, stream, args.backward_steps)
+        backward = bench_backward(cfg, W, pa, torch, dev, stream, args.backward_steps, True)
+        if not args.no_bidirectional:
+            backward_bidir = bench_backward(cfg, W, pa, torch, dev, stream, args.backward_steps, False)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -260,71 +329,53 @@ def main():
         "attended_keys_per_s": round(keys / sec, 1),
         "roofline": roofline,
         "roofline_mfma": roofline_mfma,
+        "settle_s": round(settle, 3),
+        "bidirectional": bidir,
         "decode": decode,
         "backward": backward,
+        "backward_bidirectional": backward_bidir,
         "cpu_baseline": cpu,
         "wall_s_timed": round(t_wall, 3),
     }
     print(json.dumps(rec))
 
 
-def bench_backward(cfg, W, pa, torch, dev, stream, steps):
+def bench_backward(cfg, W, pa, torch, dev, stream, steps, causal):
     """pi_attn_backward on the forward workload (lse from one forward call,
-    a seeded dL/dy); inputs resident, one warm-up call, then ``steps``."""
+    a seeded dL/dy); inputs resident, settled and warmed up, then ``steps``."""
     q, k, v, gate = W.forward_inputs(cfg, 0, dev)
-    out, lse = pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi, return_lse=True)
+    out, lse = pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi, return_lse=True, causal=causal)
     dout = W.cotangent(q.shape, q.dtype, 0, dev)
-    pa.pi_attn_backward(q, k, v, gate, cfg.k, cfg.pi, out, lse, dout)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(steps):
-        pa.pi_attn_backward(q, k, v, gate, cfg.k, cfg.pi, out, lse, dout)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / steps
-    keys, flops, nbytes = backward_algorithmic(cfg)
-    sec = ms / 1e3
-    tflops, gbs = flops / sec / 1e12, nbytes / sec / 1e9
-    t_hbm, t_mfma = nbytes / (HBM_PEAK_GBS * 1e9), flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
-    hbm = t_hbm >= t_mfma
+    ms, _, _ = time_launches(
+        torch, lambda: pa.pi_attn_backward(q, k, v, gate, cfg.k, cfg.pi, out, lse, dout, causal=causal),
+        steps, 2, stream)
+    keys, flops, nbytes = backward_algorithmic(cfg, causal)
     del q, k, v, out, dout, lse
     torch.cuda.empty_cache()
-    kernels = "backward_q_bf16_kernel<128> + backward_kv_bf16_kernel<128>"
-    return {"workload": "backward of fwd32k: B1 H32 N32768 D128 k512 pi1024 bf16 in, fp32 gradients",
-            "steps": steps, "ms_per_step": round(ms, 4),
-            "roofline": {"bound": "hbm" if hbm else "mfma", "kernel": kernels,
-                         "achieved": round(gbs if hbm else tflops, 2),
-                         "peak": HBM_PEAK_GBS if hbm else MFMA_BF16_PEAK_TFLOPS,
-                         "unit": "GB/s" if hbm else "TFLOP/s",
-                         "frac": round((gbs / HBM_PEAK_GBS) if hbm else (tflops / MFMA_BF16_PEAK_TFLOPS), 4),
-                         "traffic": None},
-            "roofline_mfma": {"achieved": round(tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                              "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "flops_per_step": flops,
-                              "bytes_per_step": nbytes}}
+    mode = "false" if causal else "true"
+    kernels = f"backward_q_bf16_kernel<128,false,{mode}> + backward_kv_bf16_kernel<128,false,{mode}>"
+    rl, mf = roofline_of(flops, nbytes, ms / 1e3, kernels,
+                         measured_traffic(csrc_digest(BACKWARD_SOURCES), BACKWARD_TRAFFIC[causal]))
+    return {"workload": ("backward of fwd32k" + ("" if causal else " bidirectional")
+                         + ": B1 H32 N32768 D128 k512 pi1024 bf16 in, fp32 gradients"),
+            "steps": steps, "ms_per_step": round(ms, 4), "roofline": rl, "roofline_mfma": mf}
 
 
 def cpu_baseline(cfg, W):
-    """The fp64 oracle, as it stands, on a bounded sample of the same
-    workload: every query of the first few heads (fresh CPU inputs of the
-    same shape and distribution), converted to query positions/s of the
-    full problem."""
-    import numpy as np
+    """The fp64 oracle, as it stands, on the forward workload (fresh CPU
+    inputs of the same shape and distribution, every head and query; a few
+    seconds on the host's cores), in query positions/s of the full problem."""
     import torch
 
     import oracle
-    heads = 16
-    sub = W.ForwardConfig("sample", 1, heads, cfg.N, cfg.D, cfg.k, cfg.pi, cfg.dtype)
-    q, k, v, gate = W.forward_inputs(sub, 0, "cpu")
+    q, k, v, gate = W.forward_inputs(cfg, 0, "cpu")
     t = time.perf_counter()
     oracle.forward(q, k, v, gate, cfg.k, cfg.pi)
     dt = time.perf_counter() - t
-    head_rows_per_s = heads * cfg.N / dt
-    return {"value": round(head_rows_per_s / cfg.H, 1), "unit": "query positions/s",
+    return {"value": round(cfg.B * cfg.N / dt, 1), "unit": "query positions/s",
             "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"{heads} of {cfg.H} heads x {cfg.N} queries (B=1), fp64, {dt:.2f} s; "
-                      f"value = head-rows/s divided by H={cfg.H}",
-            "head_rows_per_s": round(head_rows_per_s, 1)}
+            "sample": f"the whole fwd32k forward ({cfg.B * cfg.H} heads x {cfg.N} queries), fp64, {dt:.2f} s",
+            "head_rows_per_s": round(cfg.B * cfg.H * cfg.N / dt, 1)}
 
 
 if __name__ == "__main__":

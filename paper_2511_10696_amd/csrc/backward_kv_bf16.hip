@@ -133,7 +133,7 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
     // is): tiles [0, nband), [nband, nband + npar), then the rest.  Query
     // rows [lo, hi) of a stream; rows outside [0, N) are zero and masked.
     const int band_lo = BIDIR ? window_lo(j0, kw) & ~31 : j0;
-    const int band_hi = (int)min((int64_t)j0 + BK + kw, (int64_t)N);
+    const int band_hi = BIDIR ? (int)min((int64_t)j0 + BK + kw, (int64_t)N) : min(N, j0 + BK + kw);
     const int nband = band_hi > band_lo ? (band_hi - band_lo + TQ - 1) / TQ : 0;
     const bool has_par = partner_enabled(kw, pi) && (int64_t)j0 + pi < N;
     const int par_lo = j0 + pi;
@@ -146,21 +146,21 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
     const int ntiles = nband + npar + npar2;
 
     // Stage tile m of the combined stream: 64 query rows starting at q0m.
-    auto tile_kind = [&](int m) { return m < nband ? 0 : m < nband + npar ? 1 : 2; };
+    auto tile_kind = [&](int m) { return m < nband ? 0 : (!BIDIR || m < nband + npar) ? 1 : 2; };
     auto tile_start = [&](int m) {
-        return m < nband ? band_lo + TQ * m : m < nband + npar ? par_lo + TQ * (m - nband)
-                                                               : par2_lo + TQ * (m - nband - npar);
+        return m < nband ? band_lo + TQ * m : (!BIDIR || m < nband + npar) ? par_lo + TQ * (m - nband)
+                                                                           : par2_lo + TQ * (m - nband - npar);
     };
-    auto tile_end = [&](int m) { return m < nband ? band_hi : m < nband + npar ? par_hi : par2_hi; };
+    auto tile_end = [&](int m) { return m < nband ? band_hi : (!BIDIR || m < nband + npar) ? par_hi : par2_hi; };
     auto load = [&](Stage<D> &st, int m) {
         const int q0m = tile_start(m), lim = tile_end(m);
-        const int tfirst = q0m > 0 ? q0m : 0;   // an always-valid row of the stream
+        const int tfirst = BIDIR && q0m < 0 ? 0 : q0m;   // an always-valid row of the stream
 #pragma unroll
         for (int u = 0; u < T::CH; ++u) {
             const int cid = tid + NT * u;
             const int row = cid / T::CPR, pc = cid % T::CPR;
             const int t = q0m + row;
-            const bool ok = t >= 0 && t < lim;
+            const bool ok = BIDIR ? t >= 0 && t < lim : t < lim;   // causal streams start at row >= 0
             const int tc = ok ? t : tfirst;
             const uint4 qv = *reinterpret_cast<const uint4 *>(qp + tc * sn + 8 * pc);
             const uint4 ov = *reinterpret_cast<const uint4 *>(op + tc * osn + 8 * pc);
@@ -169,7 +169,7 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
         }
         if (tid < TQ) {
             const int t = q0m + tid;
-            const int tc = (t >= 0 && t < lim) ? t : tfirst;
+            const int tc = (BIDIR ? t >= 0 && t < lim : t < lim) ? t : tfirst;
             const FusionBias fb = fusion_bias(p.gate[b * p.gsb + h * p.gsh + tc * p.gsn], exact);
             st.lse2 = (bp.lse[rbase + tc] - fb.lse_shift) * kLog2e;
             st.r = bp.rowterm[rbase + tc];
@@ -194,21 +194,19 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
     // One 32-query block (rows 32 blk.. of tile tb, first query t0b) of a
     // stream of the given kind.
     auto block = [&](const QTile<D> &tb, int t0b, int blk, int kind, int lim) {
-        bool act, edge;
-        if (kind == 1) {
-            act = blk == (w & 1) && t0b == kq0 + pi;
-            edge = true;
-        } else if (kind == 2) {
-            act = blk == (w & 1) && t0b == kq0 - pi;
-            edge = true;
-        } else if (BIDIR) {
+        const bool partner = kind != 0;
+        bool act;
+        if (partner) {
+            act = blk == (w & 1) && t0b == (BIDIR && kind == 2 ? kq0 - pi : kq0 + pi);
+        } else if constexpr (BIDIR) {
             act = t0b < lim && kq0 < N && t0b - (kq0 + 31) <= kw && t0b + 31 >= kq0 - kw;
-            edge = !(t0b + 31 - kq0 <= kw && kq0 + 31 - t0b <= kw) || t0b + 31 >= N || kq0 + 31 >= N;
         } else {
             act = t0b < lim && kq0 < N && t0b <= kq0 + 31 + kw && t0b + 31 >= kq0;
-            edge = !(t0b >= kq0 + 31 && t0b + 31 <= kq0 + kw) || t0b + 31 >= N || kq0 + 31 >= N;
         }
         if (!act) return;
+        const bool edge = BIDIR ? partner || !(t0b + 31 - kq0 <= kw && kq0 + 31 - t0b <= kw) || t0b + 31 >= N ||
+                                      kq0 + 31 >= N
+                                : partner || !(t0b >= kq0 + 31 && t0b + 31 <= kq0 + kw) || t0b + 31 >= N || kq0 + 31 >= N;
         // rows of this block (A operands: query l%32, dims 16s + 8g)
         const unsigned char *qrow = tb.q + (32 * blk + c) * T::ROW + 16 * g;
         const unsigned char *orow = tb.o + (32 * blk + c) * T::ROW + 16 * g;
@@ -244,14 +242,11 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
                 if (edge) {
                     const int t = t0b + 8 * i + 4 * g + jj;
                     bool ok;
-                    if (kind == 1) {
-                        ok = t - j == pi && t < N && j_ok;
-                    } else if (kind == 2) {
-                        ok = j - t == pi && t >= 0 && j_ok;
-                    } else if (BIDIR) {
-                        ok = t - j <= kw && j - t <= kw && t < N && j_ok;
+                    if constexpr (BIDIR) {
+                        const bool is_par = kind == 2 ? j - t == pi : t - j == pi;
+                        ok = (partner ? is_par : t - j <= kw && j - t <= kw) && t >= 0 && t < N && j_ok;
                     } else {
-                        ok = t >= j && t - j <= kw && t < N && j_ok;
+                        ok = partner ? (t - j == pi && t < N && j_ok) : (t >= j && t - j <= kw && t < N && j_ok);
                     }
                     if (!ok) delta2 = -INFINITY;
                 }

@@ -28,3 +28,13 @@ def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, "bench.py", "--gpus", "2"], capture_output=True, text=True,
                        cwd=bench.ROOT)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_bidirectional_attended_keys_match_the_index_sets():
+    import oracle
+    for name in ("tiny", "fwd4k"):
+        cfg = W.FORWARD[name]
+        keys, flops, _ = bench.forward_algorithmic(cfg, causal=False)
+        idx = oracle.index_set(cfg.N, cfg.k, cfg.pi, causal=False)
+        assert keys == int((idx >= 0).sum()) * cfg.B * cfg.H
+        assert flops == 4 * cfg.D * keys

@@ -139,11 +139,11 @@ def test_forward_bf16_config_4k(device, seed):
 
 def sampled_rows(cfg, rng):
     """Every query of two seeded (b, h) pairs, plus in every head the rows
-    t < pi + 256 and the rows at query-tile boundaries."""
+    t < pi + 256, the last 512 rows and the rows at query-tile boundaries."""
     B, H, N = cfg.B, cfg.H, cfg.N
     bh = rng.choice(B * H, size=2, replace=False)
     rows = [np.arange(N) + x * N for x in bh]
-    early = np.arange(min(N, cfg.pi + 256))
+    early = np.concatenate([np.arange(min(N, cfg.pi + 256)), np.arange(max(0, N - 512), N)])
     bounds = np.unique(np.concatenate([np.arange(0, N, 128), np.arange(127, N, 128),
                                        np.arange(63, N, 128), np.arange(64, N, 128)]))
     bounds = rng.choice(bounds, size=min(256, bounds.size), replace=False)
