@@ -94,6 +94,13 @@ def _f32(a) -> np.ndarray:
     return a
 
 
+def _f64(a) -> np.ndarray:
+    """Contiguous float64 numpy array (gate logits)."""
+    if hasattr(a, "detach"):
+        a = a.detach().cpu().double().numpy()
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
 def _gate_strides(gate: np.ndarray, B: int, H: int, N: int):
     """Element strides (gsb, gsh, gsn) for a per-head [H] or per-query [B,H,N] gate."""
     if gate.shape == (H,):
@@ -127,7 +134,7 @@ def forward(q, k_, v, gate, k: int, pi: int, scale: float | None = None,
     query rows (b*H+h)*N+t), plus lse and per-slot probabilities on request.
     """
     L = L or lib()
-    q, k_, v, gate = _f32(q), _f32(k_), _f32(v), _f32(gate)
+    q, k_, v, gate = _f32(q), _f32(k_), _f32(v), _f64(gate)
     B, H, N, D = q.shape
     assert k_.shape == q.shape and v.shape == q.shape
     gsb, gsh, gsn = _gate_strides(gate, B, H, N)
@@ -167,7 +174,7 @@ def backward(q, k_, v, gate, k: int, pi: int, dout, scale: float | None = None,
     queries), all float64.  See the backward block of pi_oracle.c's header.
     """
     L = L or lib()
-    q, k_, v, gate, dout = _f32(q), _f32(k_), _f32(v), _f32(gate), _f32(dout)
+    q, k_, v, gate, dout = _f32(q), _f32(k_), _f32(v), _f64(gate), _f32(dout)
     B, H, N, D = q.shape
     assert k_.shape == q.shape and v.shape == q.shape and dout.shape == q.shape
     gsb, gsh, gsn = _gate_strides(gate, B, H, N)
@@ -191,7 +198,7 @@ def decode_step(len_in, q_new, k_new, v_new, k_cache, v_cache, gate, k: int, pi:
         if not (isinstance(c, np.ndarray) and c.dtype == np.float32 and c.flags.c_contiguous):
             raise TypeError("caches must be contiguous float32 numpy arrays (updated in place)")
     S, H, cap, D = k_cache.shape
-    q_new, k_new, v_new, gate = _f32(q_new), _f32(k_new), _f32(v_new), _f32(gate)
+    q_new, k_new, v_new, gate = _f32(q_new), _f32(k_new), _f32(v_new), _f64(gate)
     len_in = np.ascontiguousarray(np.asarray(len_in, dtype=np.int32))
     if gate.shape == (H,):
         gss, gsh = 0, 1
@@ -209,6 +216,17 @@ def decode_step(len_in, q_new, k_new, v_new, k_cache, v_cache, gate, k: int, pi:
     if rc != 0:
         raise ValueError("len_in out of range [0, cap)")
     return (out, lse) if want_lse else out
+
+
+def gate_logits(u, w2, b2) -> np.ndarray:
+    """Variant-3 gate logits from the gate MLP's hidden activations (the App. A
+    gate module is Linear(d, d/2), GELU, Linear(d/2, h), Sigmoid; ``u`` is the
+    GELU output [B, N, dh], ``w2`` [dh, H] and ``b2`` [H] the last Linear layer,
+    whose output is the pre-sigmoid logit g of R1):
+    g[b, h, t] = sum_c u[b, t, c] w2[c, h] + b2[h], in fp64.  Returns [B, H, N]."""
+    u, w2, b2 = (np.asarray(_f32(x), np.float64) for x in (u, w2, b2))
+    g = u @ w2 + b2            # [B, N, H]
+    return np.ascontiguousarray(np.transpose(g, (0, 2, 1)))
 
 
 def num_threads() -> int:

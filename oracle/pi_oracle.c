@@ -44,8 +44,10 @@
  * position t = len[s] attends to cache rows W_t, where row t is the new
  * key/value, which the step first writes into the cache.
  *
- * Inputs are float32 (bf16 data is widened exactly by the caller); every
- * arithmetic operation is double precision.  Layouts are dense row-major:
+ * Inputs are float32 (bf16 data is widened exactly by the caller) except the
+ * gate logits, which are double (so logits computed in fp64 from the gate
+ * MLP's last layer enter unrounded); every arithmetic operation is double
+ * precision.  Layouts are dense row-major:
  * q, k, v [B][H][N][D]; gate logits addressed as g[b*gsb + h*gsh + t*gsn]
  * (element strides; zeros broadcast a per-head gate).
  */
@@ -140,7 +142,7 @@ static double attend(int D, const float *q, const float *krows, const float *vro
  * 0 for absent slots) are optional (NULL). */
 void oracle_forward_rows(int B, int H, int N, int D, int k, int pi, int causal,
                          const float *q, const float *kk, const float *v,
-                         const float *gate, int64_t gsb, int64_t gsh, int64_t gsn,
+                         const double *gate, int64_t gsb, int64_t gsh, int64_t gsn,
                          double scale, double clamp,
                          const int64_t *rows, int64_t nrows,
                          double *out, double *lse, double *probs)
@@ -176,7 +178,7 @@ void oracle_forward_rows(int B, int H, int N, int D, int k, int pi, int causal,
  * Every (b, h) is independent; within one, queries are visited in order. */
 void oracle_backward(int B, int H, int N, int D, int k, int pi, int causal,
                      const float *q, const float *kk, const float *v,
-                     const float *gate, int64_t gsb, int64_t gsh, int64_t gsn,
+                     const double *gate, int64_t gsb, int64_t gsh, int64_t gsn,
                      double scale, double clamp, const float *dout,
                      double *dq, double *dk, double *dv, double *dgate)
 {
@@ -246,7 +248,7 @@ int oracle_decode_step(int S, int H, int D, int cap, int k, int pi,
                        const int32_t *len_in,
                        const float *q_new, const float *k_new, const float *v_new,
                        float *k_cache, float *v_cache,
-                       const float *gate, int64_t gss, int64_t gsh,
+                       const double *gate, int64_t gss, int64_t gsh,
                        double scale, double clamp, double *out, double *lse)
 {
     for (int s = 0; s < S; ++s)

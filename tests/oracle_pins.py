@@ -66,19 +66,24 @@ def logsumexp_masked(S, M):
     return (mx + np.log(np.exp(S - mx).sum(-1, keepdims=True)))[..., 0]
 
 
-def multiplicative_fusion(q, k, v, gate, kk, pi, scale, causal=True):
+def multiplicative_fusion(q, k, v, gate, kk, pi, scale, causal=True, alpha_t=None):
     """eq. (alphahat_adapt) in its multiplicative form: weights
     omega_tj * exp(z_tj) normalised over U(t), omega = alpha~ on the window and
-    1 - alpha~ on a partner; mask from the brute-force scan.  fp64, dense."""
+    1 - alpha~ on a partner; mask from the brute-force scan.  fp64, dense.
+    ``alpha_t`` [B, H, N], when given, is used as alpha~ directly (``gate``
+    is then ignored)."""
     q, k, v = (np.asarray(x, np.float64) for x in (q, k, v))
     B, H, N, D = q.shape
     M = scan_membership(N, kk, pi, causal)
     window = np.zeros((N, N), bool)
     for t in range(N):
         window[t, max(0, t - kk):(t + 1 if causal else t + kk + 1)] = True
-    g = np.asarray(gate, np.float64)
-    g = np.broadcast_to(g[None, :, None] if g.shape == (H,) else g, (B, H, N))
-    a_t = EPS + (1 - 2 * EPS) / (1 + np.exp(-g))           # [B,H,N]
+    if alpha_t is None:
+        g = np.asarray(gate, np.float64)
+        g = np.broadcast_to(g[None, :, None] if g.shape == (H,) else g, (B, H, N))
+        a_t = EPS + (1 - 2 * EPS) / (1 + np.exp(-g))           # [B,H,N]
+    else:
+        a_t = np.asarray(alpha_t, np.float64)
     omega = np.where(window[None, None], a_t[..., None], (1 - a_t)[..., None])
     Z = (q @ np.swapaxes(k, -1, -2)) * scale
     W = np.where(M[None, None], omega * np.exp(Z), 0.0)
@@ -481,12 +486,41 @@ def pin_bidir_gate_limits(L):
                 assert abs(got / (ratio * math.exp(zp - zs)) - 1) <= 1e-9, (t, h, j)
 
 
+def pin_gate_mlp_composition(L):
+    """App. A module, written with torch fp64 layers: gate = Sigmoid(Linear(
+    GELU(Linear(x)))), alpha~ = alpha (1 - 2 eps) + eps, union attention in
+    its multiplicative form.  Equals oracle.forward on the logits
+    oracle.gate_logits(u, W2^T, b2), u = GELU(Linear(x)) (rounded to float32,
+    the operator's input), for causal and bidirectional windows."""
+    import torch
+    import torch.nn.functional as F
+    rng = np.random.default_rng(40)
+    B, T, d, h = 2, 37, 32, 4
+    dh, D = d // 2, d // h
+    f32 = lambda a: np.asarray(a, np.float32)
+    x = torch.tensor(rng.standard_normal((B, T, d)))
+    W1, b1 = torch.tensor(rng.standard_normal((dh, d)) / math.sqrt(d)), torch.tensor(rng.standard_normal(dh) * 0.1)
+    W2 = torch.tensor(f32(rng.standard_normal((h, dh)) / math.sqrt(dh)), dtype=torch.float64)
+    b2 = torch.tensor(f32(rng.standard_normal(h)), dtype=torch.float64)
+    u = F.gelu(F.linear(x, W1, b1)).float().double()           # the operator's input u
+    a = torch.sigmoid(F.linear(u, W2, b2))                     # [B, T, h]
+    a_t = (a * (1 - 2 * EPS) + EPS).permute(0, 2, 1).numpy()   # [B, h, T]
+    g = oracle.gate_logits(u.float().numpy(), W2.T.float().numpy(), b2.float().numpy())
+    assert g.shape == (B, h, T)
+    q, k, v = rand_qkv(rng, B, h, T, D)
+    for causal in (True, False):
+        for kk, pi in [(2, 5), (3, 3), (1, 9)]:
+            ref, _ = multiplicative_fusion(q, k, v, None, kk, pi, 1 / math.sqrt(D), causal, alpha_t=a_t)
+            out = oracle.forward(q, k, v, g, kk, pi, L=L, causal=causal)
+            assert np.abs(out - ref).max() <= 1e-12, (causal, kk, pi, np.abs(out - ref).max())
+
+
 ALL_PINS = [pin_index_set_scan, pin_working_set_sizes, pin_dense_reduction, pin_local_reduction,
             pin_basic_union_g0, pin_multiplicative_form, pin_gate_limits, pin_sum_to_one_and_row0,
             pin_causality, pin_head_batch_independence, pin_decode_matches_last_row,
             pin_clamp_reading, pin_bidir_index_set_scan, pin_bidir_working_set_sizes,
             pin_bidir_dense_reduction, pin_bidir_local_reduction, pin_bidir_multiplicative_form,
-            pin_bidir_time_reversal, pin_bidir_gate_limits]
+            pin_bidir_time_reversal, pin_bidir_gate_limits, pin_gate_mlp_composition]
 
 
 def pin_reachability(L):
