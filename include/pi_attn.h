@@ -102,6 +102,8 @@ int pi_attn_index_set(int32_t n, int32_t k, int32_t pi, int32_t causal, int32_t 
  *   out          device [B][H][N][D] through (osb, osh, osn), same dtype.
  *   lse          optional device float32 [B][H][N] contiguous: natural-log
  *                sum over W_t of exp(delta), or NULL.
+ * bf16 with k <= 16 runs a gather kernel (the window band staged in LDS per
+ * head); larger windows the banded MFMA kernel.
  * Errors: EINVAL (null pointer with non-empty problem, negative size or
  * stride, misalignment), EUNSUPPORTED (D not 64/128, unknown dtype; for
  * bf16, (c * min(k, N) + 256) * sn * 2 bytes >= 2 GiB, c = 1 causal and 2
@@ -115,6 +117,42 @@ int pi_attn_forward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D,
                     float scale, float logit_clamp,
                     void *out, int64_t osb, int64_t osh, int64_t osn,
                     float *lse, void *stream);
+
+/*
+ * pi_attn_forward_gated -- pi_attn_forward with the Variant-3 gate logits
+ * computed from the gate MLP (App. A gate module: Linear(d, d/2), GELU,
+ * Linear(d/2, h), Sigmoid; Sec. 3.5 eq. gate): the caller passes the GELU
+ * output u and the last Linear layer, and the operator forms
+ *   g[b, h, t] = sum_c u[b, t, c] * w2[h, c] + b2[h]
+ * (fp32 accumulation) before the sigmoid, the eps clip and the fusion.
+ *   dtype ... k, pi, causal, q, kk, v, strides, scale, logit_clamp, out,
+ *                lse  as in pi_attn_forward.
+ *   u            device [B][N][dh] in dtype through element strides (usb,
+ *                usn), the dh elements contiguous, rows 16-byte aligned.
+ *   dh           hidden width (the paper uses d/2); dh * sizeof(dtype) must
+ *                be a multiple of 16.
+ *   w2           device [H][dh] in dtype, contiguous (the Linear weight as
+ *                stored, output-major), 16-byte aligned.
+ *   b2           device float32 [H], or NULL for no bias.
+ *   gate_out     device float32 [B][H][N] contiguous, overwritten with g (the
+ *                gate argument that pi_attn_backward takes, strides
+ *                (H*N, N, 1); dL/dg from there flows back into u, w2, b2).
+ * For bf16 with k <= 16 the logits are computed inside the attention kernel
+ * (u read once per token for a group of up to 32 heads); otherwise a gate
+ * kernel writes gate_out first and the forward reads it.
+ * Errors: as pi_attn_forward, plus EINVAL for a null u, w2 or gate_out, a
+ * misaligned u, w2, b2 or gate_out, dh < 1 or dh not a multiple of
+ * 16 bytes.
+ */
+int pi_attn_forward_gated(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D,
+                          int32_t k, int32_t pi, int32_t causal,
+                          const void *q, const void *kk, const void *v,
+                          int64_t sb, int64_t sh, int64_t sn,
+                          const void *u, int64_t usb, int64_t usn, int32_t dh,
+                          const void *w2, const float *b2,
+                          float scale, float logit_clamp,
+                          void *out, int64_t osb, int64_t osh, int64_t osn,
+                          float *lse, float *gate_out, void *stream);
 
 /*
  * pi_attn_decode_step -- one KV-cached decode step of the online operator

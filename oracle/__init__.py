@@ -221,11 +221,12 @@ def decode_step(len_in, q_new, k_new, v_new, k_cache, v_cache, gate, k: int, pi:
 def gate_logits(u, w2, b2) -> np.ndarray:
     """Variant-3 gate logits from the gate MLP's hidden activations (the App. A
     gate module is Linear(d, d/2), GELU, Linear(d/2, h), Sigmoid; ``u`` is the
-    GELU output [B, N, dh], ``w2`` [dh, H] and ``b2`` [H] the last Linear layer,
-    whose output is the pre-sigmoid logit g of R1):
-    g[b, h, t] = sum_c u[b, t, c] w2[c, h] + b2[h], in fp64.  Returns [B, H, N]."""
+    GELU output [B, N, dh], ``w2`` [H, dh] (the Linear weight as stored) and
+    ``b2`` [H] the last Linear layer, whose output is the pre-sigmoid gate
+    logit): g[b, h, t] = sum_c u[b, t, c] w2[h, c] + b2[h], in fp64.
+    Returns [B, H, N]."""
     u, w2, b2 = (np.asarray(_f32(x), np.float64) for x in (u, w2, b2))
-    g = u @ w2 + b2            # [B, N, H]
+    g = u @ w2.T + b2          # [B, N, H]
     return np.ascontiguousarray(np.transpose(g, (0, 2, 1)))
 
 

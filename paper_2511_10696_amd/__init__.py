@@ -9,6 +9,7 @@ Entry points (same names as the C ABI; ``causal=False`` selects the
 bidirectional mode, window |j - t| <= k and partners t -/+ pi):
     pi_attn_index_set(n, k, pi, causal=True)                  -> int32 [n, m] (device)
     pi_attn_forward(q, k, v, gate, k_window, pi, causal=True) -> out [B,H,N,D] (and lse)
+    pi_attn_forward_gated(q, k, v, u, w2, b2, k_window, pi)   -> out, gate logits [B,H,N]
     pi_attn_backward(q, k, v, gate, k_window, pi, out, lse, dout, causal=True)
     pi_attn_decode_step(len_in, q_new, k_new, v_new, k_cache, v_cache, gate, k, pi)
 """
@@ -19,12 +20,13 @@ import math
 import os
 import threading
 
-__all__ = ["pi_attn_index_set", "pi_attn_forward", "pi_attn_backward", "pi_attn_decode_step", "pi_attn_ws_width",
+__all__ = ["pi_attn_index_set", "pi_attn_forward", "pi_attn_forward_gated", "pi_attn_backward",
+           "pi_attn_decode_step", "pi_attn_ws_width",
            "pi_attn_strerror", "library", "LIB_PATH", "EXPORTED_SYMBOLS", "PiAttnError"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpi_attn.so")
 EXPORTED_SYMBOLS = ("pi_attn_strerror", "pi_attn_ws_width", "pi_attn_index_set",
-                    "pi_attn_forward", "pi_attn_decode_step", "pi_attn_backward")
+                    "pi_attn_forward", "pi_attn_forward_gated", "pi_attn_decode_step", "pi_attn_backward")
 
 PI_ATTN_F32, PI_ATTN_BF16 = 0, 1
 
@@ -56,6 +58,9 @@ def library() -> ctypes.CDLL:
             lib.pi_attn_forward.argtypes = ([i32] * 8 + [vp, vp, vp, i64, i64, i64, vp, i64, i64, i64,
                                                         f32, f32, vp, i64, i64, i64, vp, vp])
             lib.pi_attn_forward.restype = ctypes.c_int
+            lib.pi_attn_forward_gated.argtypes = ([i32] * 8 + [vp, vp, vp, i64, i64, i64, vp, i64, i64, i32, vp, vp,
+                                                              f32, f32, vp, i64, i64, i64, vp, vp, vp])
+            lib.pi_attn_forward_gated.restype = ctypes.c_int
             lib.pi_attn_decode_step.argtypes = ([i32] * 7 + [vp, vp, vp, vp, vp, vp, vp, vp, i64, i64,
                                                             f32, f32, vp, vp, vp])
             lib.pi_attn_decode_step.restype = ctypes.c_int
@@ -177,6 +182,61 @@ def pi_attn_forward(q, k, v, gate, k_window: int, pi: int, scale: float | None =
         _stream_handle(stream, q.device))
     _check(st, "pi_attn_forward")
     return (out, lse) if (return_lse or lse is not None) else out
+
+
+def pi_attn_forward_gated(q, k, v, u, w2, b2, k_window: int, pi: int, scale: float | None = None,
+                          logit_clamp: float = 0.0, out=None, return_lse: bool = False, lse=None,
+                          gate_out=None, stream=None, causal: bool = True):
+    """pi-Attention forward with the gate logits computed from the gate MLP's
+    last layer: g[b, h, t] = <u[b, t], w2[h]> + b2[h] (App. A gate module).
+
+    q, k, v as in pi_attn_forward; u [B, N, dh] (the GELU output, q's dtype,
+    last dimension contiguous), w2 [H, dh] (q's dtype, contiguous: a Linear
+    weight as stored), b2 [H] float32 or None.  Returns (out, gate_logits
+    [B, H, N] float32) and lse on request; gate_logits is the ``gate`` that
+    pi_attn_backward takes.
+    """
+    torch = _torch()
+    _require_cuda(q, k, v, u, w2, b2, out, lse, gate_out)
+    if q.dim() != 4 or k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k, v must share one [B, H, N, D] shape")
+    if k.dtype != q.dtype or v.dtype != q.dtype or u.dtype != q.dtype or w2.dtype != q.dtype:
+        raise TypeError("q, k, v, u and w2 must share one dtype")
+    if k.stride() != q.stride() or v.stride() != q.stride():
+        raise ValueError("q, k, v must share strides (use .contiguous())")
+    if q.stride(3) != 1:
+        raise ValueError("the head dimension must be contiguous")
+    B, H, N, D = q.shape
+    if u.dim() != 3 or u.shape[0] != B or u.shape[1] != N or u.stride(2) != 1:
+        raise ValueError("u must be [B, N, dh] with a contiguous last dimension")
+    dh = u.shape[2]
+    if tuple(w2.shape) != (H, dh) or not w2.is_contiguous():
+        raise ValueError(f"w2 must be a contiguous [H, dh] = {(H, dh)} tensor")
+    if b2 is not None and (b2.dtype != torch.float32 or tuple(b2.shape) != (H,) or not b2.is_contiguous()):
+        raise ValueError("b2 must be a contiguous float32 [H] tensor or None")
+    if out is None:
+        out = torch.empty_like(q, memory_format=torch.contiguous_format)
+    if out.shape != q.shape or out.dtype != q.dtype or out.stride(3) != 1:
+        raise ValueError("out must match q's shape and dtype with a contiguous last dimension")
+    if gate_out is None:
+        gate_out = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    if gate_out.dtype != torch.float32 or tuple(gate_out.shape) != (B, H, N) or not gate_out.is_contiguous():
+        raise ValueError("gate_out must be a contiguous float32 [B, H, N] tensor")
+    if return_lse and lse is None:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, N)
+                            or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous float32 [B, H, N] tensor")
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    st = library().pi_attn_forward_gated(
+        _dtype_code(q.dtype), B, H, N, D, int(k_window), int(pi), int(bool(causal)),
+        _ptr(q), _ptr(k), _ptr(v), q.stride(0), q.stride(1), q.stride(2),
+        _ptr(u), u.stride(0), u.stride(1), dh, _ptr(w2), _ptr(b2), float(scale), float(logit_clamp),
+        _ptr(out), out.stride(0), out.stride(1), out.stride(2), _ptr(lse), _ptr(gate_out),
+        _stream_handle(stream, q.device))
+    _check(st, "pi_attn_forward_gated")
+    return (out, gate_out, lse) if (return_lse or lse is not None) else (out, gate_out)
 
 
 def pi_attn_backward(q, k, v, gate, k_window: int, pi: int, out, lse, dout, scale: float | None = None,

@@ -7,6 +7,7 @@
 #include "../../include/pi_attn.h"
 #include "kernels.h"
 #include "pi_common.h"
+#include "smallk.h"
 
 using namespace pi_attn;
 
@@ -91,6 +92,49 @@ int pi_attn_forward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, i
     p.out = out; p.osb = osb; p.osh = osh; p.osn = osn;
     p.lse = lse;
     const hipStream_t st = (hipStream_t)stream;
+    if (dtype != PI_ATTN_BF16) return from_hip(launch_forward_f32(p, st));
+    // a window of a few keys: the gather path; otherwise the banded MFMA path
+    return from_hip(k <= kSmallK ? launch_forward_smallk(p, nullptr, st) : launch_forward_bf16(p, st));
+}
+
+int pi_attn_forward_gated(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, int32_t k, int32_t pi,
+                          int32_t causal, const void *q, const void *kk, const void *v, int64_t sb, int64_t sh,
+                          int64_t sn, const void *u, int64_t usb, int64_t usn, int32_t dh, const void *w2,
+                          const float *b2, float scale, float logit_clamp, void *out, int64_t osb, int64_t osh,
+                          int64_t osn, float *lse, float *gate_out, void *stream) {
+    const int es = elem_size(dtype);
+    if (es == 0) return PI_ATTN_EUNSUPPORTED;
+    if (B < 0 || H < 0 || N < 0 || k < 0 || pi < 0 || dh < 1) return PI_ATTN_EINVAL;
+    if (D != 64 && D != 128) return PI_ATTN_EUNSUPPORTED;
+    if (!isfinite(scale) || scale <= 0.0f || isnan(logit_clamp)) return PI_ATTN_EINVAL;
+    const int64_t rows = (int64_t)B * H * N;
+    if (rows >= kMaxRows) return PI_ATTN_EINVAL;
+    if (rows == 0) return PI_ATTN_OK;
+    if (!q || !kk || !v || !u || !w2 || !out || !gate_out) return PI_ATTN_EINVAL;
+    if (!aligned16(q) || !aligned16(kk) || !aligned16(v) || !aligned16(out) || !aligned16(u) || !aligned16(w2))
+        return PI_ATTN_EINVAL;
+    if (!stride16(sb, es) || !stride16(sh, es) || !stride16(sn, es)) return PI_ATTN_EINVAL;
+    if (!stride16(osb, es) || !stride16(osh, es) || !stride16(osn, es)) return PI_ATTN_EINVAL;
+    if (!stride16(usb, es) || !stride16(usn, es) || ((int64_t)dh * es) % 16 != 0) return PI_ATTN_EINVAL;
+    if ((b2 && !aligned4(b2)) || !aligned4(gate_out) || (lse && !aligned4(lse))) return PI_ATTN_EINVAL;
+    if (dtype == PI_ATTN_BF16 && !tile_span_ok(k, N, causal != 0, sn, es)) return PI_ATTN_EUNSUPPORTED;
+
+    FwdParams p{};
+    p.B = B; p.H = H; p.N = N; p.D = D; p.k = k; p.pi = pi; p.causal = causal != 0;
+    p.q = q; p.k_ptr = kk; p.v = v;
+    p.sb = sb; p.sh = sh; p.sn = sn;
+    p.gate = gate_out; p.gsb = (int64_t)H * N; p.gsh = N; p.gsn = 1;   // the logits this call computes
+    p.scale = scale;
+    p.clamp = logit_clamp > 0.0f ? logit_clamp : 0.0f;
+    p.out = out; p.osb = osb; p.osh = osh; p.osn = osn;
+    p.lse = lse;
+    GateMlp m{};
+    m.u = u; m.usb = usb; m.usn = usn; m.dh = dh; m.w2 = w2; m.b2 = b2; m.gate_out = gate_out;
+    const hipStream_t st = (hipStream_t)stream;
+    if (dtype == PI_ATTN_BF16 && k <= kSmallK) return from_hip(launch_forward_smallk(p, &m, st));
+    // otherwise: the logits first, then the forward that reads them
+    const hipError_t e = launch_gate_logits(p, m, dtype == PI_ATTN_BF16 ? 1 : 0, st);
+    if (e != hipSuccess) return PI_ATTN_EHIP;
     return from_hip(dtype == PI_ATTN_BF16 ? launch_forward_bf16(p, st) : launch_forward_f32(p, st));
 }
 

@@ -10,6 +10,9 @@ Workloads (one GPU):
   fwd4k   B4  H16 N4096  D64  k128 pi256  bf16, q scaled by 1/sqrt(D)
   fwd16k  B2  H32 N16384 D128 k256 pi512  bf16, 1% of key rows x8 (heavy hitters)
   fwd32k  B1  H32 N32768 D128 k512 pi1024 bf16
+  smallk8k B8 H16 N8192  D64  k4   pi16   bf16, the paper's default window and period
+          (Sec. 4, App. B) at its 8K efficiency context; gate from the gate MLP's
+          last layer (hidden width d/2 = 512)
   decode  S64 H32 D128 k512 pi1024, bf16 KV cache of 32768 rows, 1000 appended steps
 q, k, v ~ N(0, 1) drawn in float32 then rounded to the dtype; per-head gate
 logits ~ U(-1, 1) in float32.  The paper's own efficiency runs use trained
@@ -65,6 +68,7 @@ FORWARD = {
     "fwd16k": ForwardConfig("fwd16k", 2, 32, 16384, 128, 256, 512, torch.bfloat16,
                             heavy_frac=0.01, heavy_mult=8.0),
     "fwd32k": ForwardConfig("fwd32k", 1, 32, 32768, 128, 512, 1024, torch.bfloat16),
+    "smallk8k": ForwardConfig("smallk8k", 8, 16, 8192, 64, EFF_K, EFF_PI, torch.bfloat16),
 }
 DECODE = {
     "decode": DecodeConfig("decode", 64, 32, 128, 512, 1024, 32768, 1000),
@@ -98,6 +102,20 @@ def forward_inputs(cfg: ForwardConfig, seed: int = 0, device="cuda", per_query_g
     gshape = (cfg.B, cfg.H, cfg.N) if per_query_gate else (cfg.H,)
     gate = torch.rand(gshape, generator=g, device=device, dtype=torch.float32) * 2.0 - 1.0
     return out[0], out[1], out[2], gate
+
+
+def gate_mlp_inputs(cfg: ForwardConfig, seed: int = 0, device="cuda", dh: int | None = None):
+    """Operands of the gate MLP's last layer: u [B, N, dh] (GELU of N(0, 1),
+    the hidden activations), w2 [H, dh] ~ N(0, 1/dh) (both cfg.dtype) and
+    b2 [H] ~ U(-0.1, 0.1) float32; dh defaults to d/2 = H*D/2."""
+    dh = dh or cfg.H * cfg.D // 2
+    g = _gen(device, seed + 2000003)
+    x = torch.randn((cfg.B, cfg.N, dh), generator=g, device=device, dtype=torch.float32)
+    u = torch.nn.functional.gelu(x).to(cfg.dtype)
+    del x
+    w2 = (torch.randn((cfg.H, dh), generator=g, device=device, dtype=torch.float32) / math.sqrt(dh)).to(cfg.dtype)
+    b2 = torch.rand((cfg.H,), generator=g, device=device, dtype=torch.float32) * 0.2 - 0.1
+    return u, w2, b2
 
 
 def cotangent(shape, dtype, seed: int = 0, device="cuda"):

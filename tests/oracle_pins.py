@@ -490,7 +490,7 @@ def pin_gate_mlp_composition(L):
     """App. A module, written with torch fp64 layers: gate = Sigmoid(Linear(
     GELU(Linear(x)))), alpha~ = alpha (1 - 2 eps) + eps, union attention in
     its multiplicative form.  Equals oracle.forward on the logits
-    oracle.gate_logits(u, W2^T, b2), u = GELU(Linear(x)) (rounded to float32,
+    oracle.gate_logits(u, W2, b2), u = GELU(Linear(x)) (rounded to float32,
     the operator's input), for causal and bidirectional windows."""
     import torch
     import torch.nn.functional as F
@@ -505,7 +505,7 @@ def pin_gate_mlp_composition(L):
     u = F.gelu(F.linear(x, W1, b1)).float().double()           # the operator's input u
     a = torch.sigmoid(F.linear(u, W2, b2))                     # [B, T, h]
     a_t = (a * (1 - 2 * EPS) + EPS).permute(0, 2, 1).numpy()   # [B, h, T]
-    g = oracle.gate_logits(u.float().numpy(), W2.T.float().numpy(), b2.float().numpy())
+    g = oracle.gate_logits(u.float().numpy(), W2.float().numpy(), b2.float().numpy())
     assert g.shape == (B, h, T)
     q, k, v = rand_qkv(rng, B, h, T, D)
     for causal in (True, False):

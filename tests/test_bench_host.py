@@ -9,7 +9,7 @@ from paper_2511_10696_amd import workloads as W
 
 def test_attended_keys_match_closed_form():
     # sum over t of |W_t| per (b, h): window min(t,k)+1 plus the partner for t >= pi
-    per_bh = {"tiny": 8112, "fwd4k": 523968, "fwd16k": 4193664, "fwd32k": 16710400}
+    per_bh = {"tiny": 8112, "fwd4k": 523968, "fwd16k": 4193664, "fwd32k": 16710400, "smallk8k": 49126}
     for name, cfg in W.FORWARD.items():
         keys, flops, nbytes = bench.forward_algorithmic(cfg)
         assert keys == per_bh[name] * cfg.B * cfg.H
