@@ -38,7 +38,12 @@ DECODE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_bf16_s64_hbm_traffic.txt
 BIDIR_TRAFFIC = os.path.join(ROOT, "profiles", "forward_bf16_bidir_fwd32k_hbm_traffic.txt")
 BACKWARD_TRAFFIC = {True: os.path.join(ROOT, "profiles", "backward_bf16_fwd32k_hbm_traffic.txt"),
                     False: os.path.join(ROOT, "profiles", "backward_bf16_bidir_fwd32k_hbm_traffic.txt")}
+SMALLK_TRAFFIC = {"gated": os.path.join(ROOT, "profiles", "smallk_bf16_gated_smallk8k_hbm_traffic.txt"),
+                  "gated_bidirectional": os.path.join(ROOT, "profiles",
+                                                      "smallk_bf16_gated_bidir_smallk8k_hbm_traffic.txt"),
+                  "per_head_gate": os.path.join(ROOT, "profiles", "smallk_bf16_smallk8k_hbm_traffic.txt")}
 FORWARD_SOURCES = ("forward_bf16.hip", "pi_common.h", "kernels.h")
+SMALLK_SOURCES = ("smallk_bf16.hip", "smallk.h", "pi_common.h", "kernels.h")
 BACKWARD_SOURCES = ("backward_bf16.hip", "backward_kv_bf16.hip", "backward.hip", "pi_common.h", "kernels.h")
 
 
@@ -58,6 +63,7 @@ def parse():
     ap.add_argument("--backward-steps", type=int, default=20)
     ap.add_argument("--no-backward", action="store_true")
     ap.add_argument("--no-bidirectional", action="store_true")
+    ap.add_argument("--no-smallk", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pmc-probe", action="store_true",
                     help="run 3 launches of each timed kernel (forward, bidirectional forward, backward "
@@ -81,6 +87,19 @@ def forward_algorithmic(cfg, causal=True):
     flops = 4 * cfg.D * keys
     es = 2
     nbytes = 4 * cfg.B * cfg.H * cfg.N * cfg.D * es
+    return keys, flops, nbytes
+
+
+def smallk_algorithmic(cfg, causal=True, gated=True):
+    """Algorithmic work of one small-window forward: the attention's keys,
+    FLOPs and bytes, plus (gated) the gate MLP's last layer: u [B, N, dh] and
+    w2 [H, dh] read once, the logits [B, H, N] float32 written, 2 dh FLOPs
+    per (b, h, t)."""
+    keys, flops, nbytes = forward_algorithmic(cfg, causal)
+    if gated:
+        dh = cfg.H * cfg.D // 2
+        flops += 2 * dh * cfg.B * cfg.H * cfg.N
+        nbytes += 2 * (cfg.B * cfg.N * dh + cfg.H * dh) + 4 * cfg.B * cfg.H * cfg.N
     return keys, flops, nbytes
 
 
@@ -192,6 +211,18 @@ def pmc_probe(W, pa, torch, dev):
         print(f"probe: 3 x backward fwd32k causal={causal}", flush=True)
         del y, lse
     del q, k, v, out, dout
+    scfg = W.FORWARD["smallk8k"]
+    q, k, v, gate = W.forward_inputs(scfg, 0, dev)
+    u, w2, b2 = W.gate_mlp_inputs(scfg, 0, dev)
+    out = torch.empty_like(q)
+    for _ in range(3):
+        pa.pi_attn_forward(q, k, v, gate, scfg.k, scfg.pi, out=out)
+    for causal in (True, False):
+        for _ in range(3):
+            pa.pi_attn_forward_gated(q, k, v, u, w2, b2, scfg.k, scfg.pi, out=out, causal=causal)
+    torch.cuda.synchronize()
+    print("probe: 3 x small-window forward, 3 x gated (causal, bidirectional) smallk8k", flush=True)
+    del q, k, v, u, w2, out
     dcfg = W.DECODE["decode"]
     kc, vc, lens, dgate = W.decode_state(dcfg, 0, dev)
     qs, ks, vs = W.decode_tokens(dcfg, 3, 1, dev)
@@ -259,6 +290,11 @@ def main():
                  "roofline": brl, "roofline_mfma": bmf}
     del q, k, v, out
     torch.cuda.empty_cache()
+
+    # ---- small window (the paper's default k = 4, pi = 16) -------------------
+    smallk = None
+    if not args.no_smallk:
+        smallk = bench_smallk(W, pa, torch, dev, stream, args.steps, args.warmup)
 
     # ---- decode step --------------------------------------------------------
     decode = None
@@ -331,6 +367,7 @@ def main():
         "roofline_mfma": roofline_mfma,
         "settle_s": round(settle, 3),
         "bidirectional": bidir,
+        "smallk": smallk,
         "decode": decode,
         "backward": backward,
         "backward_bidirectional": backward_bidir,
@@ -338,6 +375,39 @@ def main():
         "wall_s_timed": round(t_wall, 3),
     }
     print(json.dumps(rec))
+
+
+def bench_smallk(W, pa, torch, dev, stream, steps, warmup):
+    """The small-window gather path on smallk8k: the gated forward (gate MLP's
+    last layer fused), causal and bidirectional, and the forward with given
+    per-head gate logits."""
+    cfg = W.FORWARD["smallk8k"]
+    q, k, v, gate = W.forward_inputs(cfg, 0, dev)
+    u, w2, b2 = W.gate_mlp_inputs(cfg, 0, dev)
+    out = torch.empty_like(q)
+    g = torch.empty((cfg.B, cfg.H, cfg.N), dtype=torch.float32, device=dev)
+    res = {"workload": "smallk8k: B8 H16 N8192 D64 k4 pi16 bf16, gate MLP hidden width 512",
+           "steps": steps}
+    for name, causal, gated in (("gated", True, True), ("gated_bidirectional", False, True),
+                                ("per_head_gate", True, False)):
+        if gated:
+            fn = lambda c=causal: pa.pi_attn_forward_gated(q, k, v, u, w2, b2, cfg.k, cfg.pi, out=out, gate_out=g,
+                                                           causal=c)
+        else:
+            fn = lambda c=causal: pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi, out=out, causal=c)
+        ms, _, _ = time_launches(torch, fn, steps, warmup, stream)
+        keys, flops, nbytes = smallk_algorithmic(cfg, causal, gated)
+        mode = "false" if causal else "true"
+        rl, mf = roofline_of(flops, nbytes, ms / 1e3,
+                             f"smallk_bf16_kernel<64,{mode},{'true' if gated else 'false'},4>",
+                             measured_traffic(csrc_digest(SMALLK_SOURCES), SMALLK_TRAFFIC[name]))
+        res[name] = {"us_per_step": round(ms * 1e3, 2),
+                     "query_positions_per_s": round(cfg.B * cfg.N / (ms / 1e3), 1),
+                     "attended_keys_per_s": round(keys / (ms / 1e3), 1),
+                     "bytes_per_step": nbytes, "roofline": rl}
+    del q, k, v, u, w2, out, g
+    torch.cuda.empty_cache()
+    return res
 
 
 def bench_backward(cfg, W, pa, torch, dev, stream, steps, causal):

@@ -15,11 +15,13 @@
 //     is 4 (D = 64) or 8 packed-bf16 dot products per lane
 //     (v_dot2c_f32_bf16) and a 3-step DPP reduction inside the 8 lanes, which
 //     leaves the same sum in each of them;
-//   - the working set is visited entry by entry with an online softmax in
-//     fp32 (maximum raised only when an entry exceeds it by more than 2^8):
-//     the partners t - pi (and t + pi), read straight from global memory,
-//     then the window from LDS.  Absent entries read a clamped row of the
-//     band and get weight exactly 0.
+//   - the kernel is instantiated for a window bound KMAX (4, 8 or 16, the
+//     smallest that holds k); the working set is unrolled to its KMAX-bound
+//     size: every score first (independent chains: the partners t - pi and
+//     t + pi read straight from global memory, the window from LDS), then
+//     one exact maximum, the fp32 softmax and the weighted sum of V.
+//     Absent entries (and slots beyond k) read a clamped row of the band and
+//     get weight exactly 0.
 // Gate MLP epilogue: the logits g[t, h] = <u_t, w2_h> + b2_h of the work-group's
 // 32 tokens and heads are one 32x32 block of v_mfma_f32_32x32x16_bf16 products
 // (A = the tokens' hidden activations u, B = the heads' rows of w2), the K
@@ -40,11 +42,11 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int NT = 256;    // threads per work-group
 constexpr int TT = 32;     // tokens per work-group
 constexpr int HG = 32;     // heads per work-group at most
-constexpr float kTau = 8.0f;
+constexpr int kGateScratch = 4 * 32 * 33;
 
-template <int D, bool BIDIR>
+template <int D, bool BIDIR, int KMAX>
 struct Band {
-    static constexpr int ROWS = TT + (BIDIR ? 2 : 1) * kSmallK;   // staged rows at most
+    static constexpr int ROWS = TT + (BIDIR ? 2 : 1) * KMAX;      // staged rows at most
     static constexpr int ROWB = 2 * D;                            // LDS bytes per row
     static constexpr int CPR = D / 8;                             // 16-byte chunks per row
     static constexpr int CH = (ROWS * CPR + NT - 1) / NT;         // staged chunks per thread and tensor
@@ -92,7 +94,8 @@ __device__ inline void axpy8(float *acc, float p, const uint4 &v) {
 
 // The gate logits of tokens [t0, t0 + 32) and heads [h0, h0 + nh) (nh <= 32)
 // into glds[h - h0][t - t0] (fp32, plus b2) and, when `out` is set, into
-// gate_out.  `scratch` holds 4 x 32 x 32 floats.  Called by all threads.
+// gate_out.  `scratch` holds kGateScratch floats (per wavefront a [head]
+// [token] block, rows padded to 33).  Called by all threads.
 __device__ void gate_tile(const FwdParams &p, const GateMlp &m, int b, int t0, int h0, int nh, float *scratch,
                           float *glds, bool out) {
     const int tid = threadIdx.x, lane = __lane_id(), w = tid >> 6;
@@ -112,12 +115,12 @@ __device__ void gate_tile(const FwdParams &p, const GateMlp &m, int b, int t0, i
     }
     // C[token r][head i]: lane (i, g) holds rows r = 8(e/4) + 4g + e%4
 #pragma unroll
-    for (int e = 0; e < 16; ++e) scratch[(w * 32 + 8 * (e >> 2) + 4 * g + (e & 3)) * 32 + i] = acc[e];
+    for (int e = 0; e < 16; ++e) scratch[(w * 32 + i) * 33 + 8 * (e >> 2) + 4 * g + (e & 3)] = acc[e];
     __syncthreads();
     for (int x = tid; x < 32 * 32; x += NT) {
         const int hh = x >> 5, r = x & 31;   // consecutive threads: consecutive tokens of one head
-        float v = scratch[(0 * 32 + r) * 32 + hh] + scratch[(1 * 32 + r) * 32 + hh] + scratch[(2 * 32 + r) * 32 + hh] +
-                  scratch[(3 * 32 + r) * 32 + hh];
+        float v = scratch[(0 * 32 + hh) * 33 + r] + scratch[(1 * 32 + hh) * 33 + r] + scratch[(2 * 32 + hh) * 33 + r] +
+                  scratch[(3 * 32 + hh) * 33 + r];
         if (hh < nh) {
             if (m.b2) v += m.b2[h0 + hh];
             glds[hh * TT + r] = v;
@@ -127,14 +130,14 @@ __device__ void gate_tile(const FwdParams &p, const GateMlp &m, int b, int t0, i
     __syncthreads();
 }
 
-template <int D, bool BIDIR, bool GATED>
+template <int D, bool BIDIR, bool GATED, int KMAX>
 __global__ __launch_bounds__(NT) void smallk_bf16_kernel(FwdParams p, GateMlp m, int n_tt, int n_hg,
                                                          int64_t n_logical) {
-    using BD = Band<D, BIDIR>;
+    using BD = Band<D, BIDIR, KMAX>;
     constexpr int E = BD::E, CPR = BD::CPR, ROWB = BD::ROWB;
     __shared__ alignas(16) unsigned char band[2][2][BD::ROWS * ROWB];   // [buffer][K, V]
     __shared__ float glds[HG * TT];
-    static_assert(sizeof(band) >= 4 * 32 * 32 * sizeof(float), "the gate prologue borrows the band buffers");
+    static_assert(sizeof(band) >= kGateScratch * sizeof(float), "the gate prologue borrows the band buffers");
     const int64_t logical = xcd_remap(blockIdx.x, n_logical);
     if (logical < 0) return;
     const int hg = (int)(logical % n_hg);
@@ -161,9 +164,6 @@ __global__ __launch_bounds__(NT) void smallk_bf16_kernel(FwdParams p, GateMlp m,
     const bool has_p = t_ok && partner_enabled(kw, pi) && jp_raw >= 0;
     const bool has_f = BIDIR && t_ok && partner_fwd_of(t, kw, pi, N) >= 0;
 
-    if constexpr (GATED) {
-        gate_tile(p, m, b, t0, h0, h1 - h0, reinterpret_cast<float *>(&band[0][0][0]), glds, true);
-    }
 
     // staged state of one head: band chunks, the query chunk, partner chunks, gate logit
     struct Next {
@@ -204,7 +204,7 @@ __global__ __launch_bounds__(NT) void smallk_bf16_kernel(FwdParams p, GateMlp m,
             }
         }
         if constexpr (GATED) {
-            nx.gl = glds[(h - h0) * TT + qi];
+            if (h > h0) nx.gl = glds[(h - h0) * TT + qi];   // head h0: after the gate prologue
         } else {
             nx.gl = p.gate[b * p.gsb + h * p.gsh + tq * p.gsn];
         }
@@ -224,7 +224,11 @@ __global__ __launch_bounds__(NT) void smallk_bf16_kernel(FwdParams p, GateMlp m,
     const bool clamp_on = p.clamp > 0.0f;
     const float c2 = p.scale * kLog2e;
     Next cur, nxt;
-    fetch(cur, h0);
+    fetch(cur, h0);   // head h0's loads fly during the gate prologue
+    if constexpr (GATED) {
+        gate_tile(p, m, b, t0, h0, h1 - h0, reinterpret_cast<float *>(&band[0][0][0]), glds, true);
+        cur.gl = glds[qi];
+    }
     stage(cur, 0);
     __syncthreads();
     for (int h = h0; h < h1; ++h) {
@@ -237,53 +241,71 @@ __global__ __launch_bounds__(NT) void smallk_bf16_kernel(FwdParams p, GateMlp m,
             return clamp_on ? fminf(fmaxf(dot * p.scale + bias, -p.clamp), p.clamp) * kLog2e
                             : __builtin_fmaf(dot, c2, bias * kLog2e);
         };
-        float mref = -INFINITY, l = 0.0f, acc[E];
-#pragma unroll
-        for (int e = 0; e < E; ++e) acc[e] = 0.0f;
-        auto visit = [&](float s, bool ok, const uint4 *vv) {
-            s = ok ? s : -INFINITY;
-            if (s > mref + kTau) {   // raise the reference maximum (lanes of a row agree)
-                const float a = __builtin_amdgcn_exp2f(mref - s);
-                l *= a;
-#pragma unroll
-                for (int e = 0; e < E; ++e) acc[e] *= a;
-                mref = s;
-            }
-            const float pr = ok ? __builtin_amdgcn_exp2f(s - mref) : 0.0f;   // (mref may still be -inf)
-            l += pr;
-#pragma unroll
-            for (int x = 0; x < E / 8; ++x) axpy8(acc + 8 * x, pr, vv[x]);
-        };
-        {   // partners
+        constexpr int NW = BIDIR ? 2 * KMAX + 1 : KMAX + 1;   // window slots at most
+        constexpr int NP = BIDIR ? 2 : 1;                     // partner slots
+        const unsigned char *kb = band[buf][0];
+        const unsigned char *vb = band[buf][1];
+        // ---- scores: partners, then window slot s (row t - k + s, LDS row qi + s)
+        float sc[NP + NW];
+        int row[NW];
+        {
             float part = 0.0f;
 #pragma unroll
             for (int x = 0; x < E / 8; ++x) part = dot8(cur.q[x], cur.kp[x], part);
-            visit(logit(part, fb.partner), has_p, cur.vp);
+            sc[0] = has_p ? logit(part, fb.partner) : -INFINITY;
             if constexpr (BIDIR) {
                 part = 0.0f;
 #pragma unroll
                 for (int x = 0; x < E / 8; ++x) part = dot8(cur.q[x], cur.kf[x], part);
-                visit(logit(part, fb.partner), has_f, cur.vf);
+                sc[1] = has_f ? logit(part, fb.partner) : -INFINITY;
             }
         }
-        // window slots s: row j = t - k + s, LDS row qi + s
-        const unsigned char *kb = band[buf][0];
-        const unsigned char *vb = band[buf][1];
-        for (int s = 0; s < nw; ++s) {
+#pragma unroll
+        for (int s = 0; s < NW; ++s) {
             const int j = t - kw + s;
-            const bool ok = t_ok && j >= 0 && j < N;
-            const int r = ok ? qi + s : tq - rlo;   // a clamped row of the band otherwise
-            uint4 kk[E / 8], vv[E / 8];
+            const bool ok = s < nw && t_ok && j >= 0 && j < N;
+            row[s] = ok ? qi + s : tq - rlo;   // a clamped row of the band otherwise
+            float part = 0.0f;
 #pragma unroll
             for (int x = 0; x < E / 8; ++x) {
                 const int c = (E / 8) * sl + x;
-                kk[x] = *reinterpret_cast<const uint4 *>(kb + r * ROWB + 16 * chunk_pos<D>(r, c));
-                vv[x] = *reinterpret_cast<const uint4 *>(vb + r * ROWB + 16 * chunk_pos<D>(r, c));
+                const uint4 kk =
+                    *reinterpret_cast<const uint4 *>(kb + row[s] * ROWB + 16 * chunk_pos<D>(row[s], c));
+                part = dot8(cur.q[x], kk, part);
             }
-            float part = 0.0f;
+            sc[NP + s] = ok ? logit(part, fb.local) : -INFINITY;
+        }
+        // ---- softmax (the 8 lanes of a row hold identical scores)
+        float mx = sc[0];
 #pragma unroll
-            for (int x = 0; x < E / 8; ++x) part = dot8(cur.q[x], kk[x], part);
-            visit(logit(part, fb.local), ok, vv);
+        for (int e = 1; e < NP + NW; ++e) mx = fmaxf(mx, sc[e]);
+        mx = t_ok ? mx : 0.0f;   // every entry absent: keep the arithmetic finite
+        float l = 0.0f, acc[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] = 0.0f;
+        {
+            const float pp = __builtin_amdgcn_exp2f(sc[0] - mx);   // 0 for an absent entry
+            l += pp;
+#pragma unroll
+            for (int x = 0; x < E / 8; ++x) axpy8(acc + 8 * x, pp, cur.vp[x]);
+            if constexpr (BIDIR) {
+                const float pf = __builtin_amdgcn_exp2f(sc[1] - mx);
+                l += pf;
+#pragma unroll
+                for (int x = 0; x < E / 8; ++x) axpy8(acc + 8 * x, pf, cur.vf[x]);
+            }
+        }
+#pragma unroll
+        for (int s = 0; s < NW; ++s) {
+            const float pr = __builtin_amdgcn_exp2f(sc[NP + s] - mx);
+            l += pr;
+#pragma unroll
+            for (int x = 0; x < E / 8; ++x) {
+                const int c = (E / 8) * sl + x;
+                const uint4 vv =
+                    *reinterpret_cast<const uint4 *>(vb + row[s] * ROWB + 16 * chunk_pos<D>(row[s], c));
+                axpy8(acc + 8 * x, pr, vv);
+            }
         }
         // normalise and store
         if (t_ok) {
@@ -296,7 +318,7 @@ __global__ __launch_bounds__(NT) void smallk_bf16_kernel(FwdParams p, GateMlp m,
                 for (int e = 0; e < 8; ++e) o[e] = (__bf16)(acc[8 * x + e] * inv);
                 *reinterpret_cast<bf16x8 *>(op + 8 * x) = o;
             }
-            if (p.lse && sl == 0) p.lse[((int64_t)b * p.H + h) * N + t] = (mref + __log2f(l)) * kLn2 + fb.lse_shift;
+            if (p.lse && sl == 0) p.lse[((int64_t)b * p.H + h) * N + t] = (mx + __log2f(l)) * kLn2 + fb.lse_shift;
         }
         if (h + 1 < h1) {
             stage(nxt, buf ^ 1);
@@ -309,7 +331,7 @@ __global__ __launch_bounds__(NT) void smallk_bf16_kernel(FwdParams p, GateMlp m,
 // The gate logits alone (bf16 operands, MFMA), one work-group per
 // (b, 32 tokens, 32 heads).
 __global__ __launch_bounds__(NT) void gate_bf16_kernel(FwdParams p, GateMlp m, int n_tt, int n_hb) {
-    __shared__ float scratch[4 * 32 * 32];
+    __shared__ float scratch[kGateScratch];
     __shared__ float glds[HG * TT];
     const int hb = blockIdx.x % n_hb;
     const int tt = (blockIdx.x / n_hb) % n_tt;
@@ -331,7 +353,7 @@ __global__ __launch_bounds__(NT) void gate_f32_kernel(FwdParams p, GateMlp m) {
     m.gate_out[x] = s + (m.b2 ? m.b2[h] : 0.0f);
 }
 
-template <int D, bool BIDIR, bool GATED>
+template <int D, bool BIDIR, bool GATED, int KMAX>
 hipError_t launch_sk(const FwdParams &p, const GateMlp &m, hipStream_t stream) {
     const int n_tt = (p.N + TT - 1) / TT;
     // head groups: at least ceil(H / 32); more while the grid is small
@@ -339,14 +361,21 @@ hipError_t launch_sk(const FwdParams &p, const GateMlp &m, hipStream_t stream) {
     while (n_hg < p.H && (int64_t)p.B * n_tt * n_hg < 2048) ++n_hg;
     const int64_t n_logical = (int64_t)p.B * n_tt * n_hg;
     const int64_t grid = xcd_grid(n_logical);
-    return launch_kernel(smallk_bf16_kernel<D, BIDIR, GATED>, dim3((unsigned)grid), dim3(NT), stream, p, m, n_tt,
-                         n_hg, n_logical);
+    return launch_kernel(smallk_bf16_kernel<D, BIDIR, GATED, KMAX>, dim3((unsigned)grid), dim3(NT), stream, p, m,
+                         n_tt, n_hg, n_logical);
+}
+
+template <int D, bool BIDIR, bool GATED>
+hipError_t launch_skk(const FwdParams &p, const GateMlp &m, hipStream_t stream) {
+    if (p.k <= 4) return launch_sk<D, BIDIR, GATED, 4>(p, m, stream);
+    if (p.k <= 8) return launch_sk<D, BIDIR, GATED, 8>(p, m, stream);
+    return launch_sk<D, BIDIR, GATED, kSmallK>(p, m, stream);
 }
 
 template <int D, bool BIDIR>
 hipError_t launch_skg(const FwdParams &p, const GateMlp *m, hipStream_t stream) {
-    if (m) return launch_sk<D, BIDIR, true>(p, *m, stream);
-    return launch_sk<D, BIDIR, false>(p, GateMlp{}, stream);
+    if (m) return launch_skk<D, BIDIR, true>(p, *m, stream);
+    return launch_skk<D, BIDIR, false>(p, GateMlp{}, stream);
 }
 
 }  // namespace
