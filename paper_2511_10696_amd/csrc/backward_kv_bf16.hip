@@ -51,7 +51,7 @@ constexpr int BPT = TQ / 32;
 template <int D>
 struct Tile {
     static constexpr int CPR = D / 8;
-    static constexpr int ROW = 2 * D + 16;   // padded LDS row stride (bytes)
+    static constexpr int ROW = 2 * D + 64;   // LDS row stride (bytes), see chunk_x
     static constexpr int BYTES = TQ * ROW;
     static constexpr int KS = D / 16;
     static constexpr int DB = D / 32;
@@ -73,6 +73,14 @@ struct Stage {
     uint4 o[Tile<D>::CH];
     float lse2, r, bias;
 };
+
+// LDS layout of the Q and dL/dy tiles: rows padded by 64 bytes, and the low
+// two bits of a row's 16-byte chunk index XORed with bits 2-3 of the row.
+// Both reads of a tile are then free of bank conflicts: the row fragments
+// (16 consecutive rows, one chunk each) and the transpose reads (4
+// consecutive rows, 4 consecutive chunks each); the offsets stay affine in
+// the k-step (two bases, even and odd steps) and in the dimension block.
+__device__ inline int chunk_x(int row) { return (row >> 2) & 3; }
 
 __device__ inline float other_half(float x) {
     const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -181,8 +189,8 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
         for (int u = 0; u < T::CH; ++u) {
             const int cid = tid + NT * u;
             const int row = cid / T::CPR, pc = cid % T::CPR;
-            *reinterpret_cast<uint4 *>(tb.q + row * T::ROW + pc * 16) = st.q[u];
-            *reinterpret_cast<uint4 *>(tb.o + row * T::ROW + pc * 16) = st.o[u];
+            *reinterpret_cast<uint4 *>(tb.q + row * T::ROW + (pc ^ chunk_x(row)) * 16) = st.q[u];
+            *reinterpret_cast<uint4 *>(tb.o + row * T::ROW + (pc ^ chunk_x(row)) * 16) = st.o[u];
         }
         if (tid < TQ) {
             tb.lse2[tid] = st.lse2;
@@ -207,18 +215,20 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
         const bool edge = BIDIR ? partner || !(t0b + 31 - kq0 <= kw && kq0 + 31 - t0b <= kw) || t0b + 31 >= N ||
                                       kq0 + 31 >= N
                                 : partner || !(t0b >= kq0 + 31 && t0b + 31 <= kq0 + kw) || t0b + 31 >= N || kq0 + 31 >= N;
-        // rows of this block (A operands: query l%32, dims 16s + 8g)
-        const unsigned char *qrow = tb.q + (32 * blk + c) * T::ROW + 16 * g;
-        const unsigned char *orow = tb.o + (32 * blk + c) * T::ROW + 16 * g;
+        // rows of this block (A operands: query l%32, dims 16s + 8g): chunk
+        // (2s + g) ^ x = 2(s ^ (x >> 1)) + (g ^ (x & 1)), x = chunk_x(row)
+        const int xr = chunk_x(32 * blk + c);
+        const int rb = (32 * blk + c) * T::ROW + 16 * (g ^ (xr & 1));
+        const int rbo[2] = {rb + 32 * (xr >> 1), rb - 32 * (xr >> 1)};   // even, odd k-steps
         f32x16 sc = {}, dp = {};
 #pragma unroll
         for (int s = 0; s < KS; ++s)
-            sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8 *>(qrow + 32 * s), kf[s], sc,
-                                                         0, 0, 0);
+            sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                *reinterpret_cast<const bf16x8 *>(tb.q + rbo[s & 1] + 32 * s), kf[s], sc, 0, 0, 0);
 #pragma unroll
         for (int s = 0; s < KS; ++s)
-            dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8 *>(orow + 32 * s), vf[s], dp,
-                                                         0, 0, 0);
+            dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                *reinterpret_cast<const bf16x8 *>(tb.o + rbo[s & 1] + 32 * s), vf[s], dp, 0, 0, 0);
         // per-query terms of this lane's queries 8i + 4g + jj
         float pr[16], ds[16];
 #pragma unroll
@@ -265,8 +275,11 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
             }
         }
         // transposed tiles (A operands: dim 32db + l%32, queries permuted)
+        // rows 32 blk + 4g + rr + 8hh + 16cc, chunks 4d + (j ^ (g + 2hh))
         const int G = lane >> 4, rr = (lane >> 2) & 3, qd = lane & 3;
-        const int toff = (32 * blk + 4 * g + rr) * T::ROW + (2 * (G & 1) + (qd >> 1)) * 16 + (qd & 1) * 8;
+        const int jq = 2 * (G & 1) + (qd >> 1);
+        const int toff[2] = {(32 * blk + 4 * g + rr) * T::ROW + 16 * (jq ^ g) + (qd & 1) * 8,
+                             (32 * blk + 4 * g + rr + 8) * T::ROW + 16 * (jq ^ (g + 2)) + (qd & 1) * 8};
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc) {
 #pragma unroll
@@ -274,7 +287,7 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
                 bf16x8 ao, aq;
 #pragma unroll
                 for (int hh = 0; hh < 2; ++hh) {
-                    const int off = toff + (16 * cc + 8 * hh) * T::ROW + 64 * d;
+                    const int off = toff[hh] + 16 * cc * T::ROW + 64 * d;
                     const bf16x4 yo = __builtin_bit_cast(
                         bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(tb.o + off)));
                     const bf16x4 yq = __builtin_bit_cast(
