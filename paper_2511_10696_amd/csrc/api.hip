@@ -32,6 +32,41 @@ bool tile_span_ok(int32_t k, int32_t N, bool causal, int64_t sn, int es) {
     return rows * sn * es < ((int64_t)1 << 31);
 }
 
+// Checks shared by the full-sequence calls (forward, gated forward,
+// backward): dtype, sizes, head dimension, scale and clamp, the q/k/v/out
+// pointers, their alignment and strides, and the bf16 tile span.  Returns a
+// status; on PI_ATTN_OK, `empty` tells whether the problem has no rows (then
+// nothing else is checked and the call is a no-op), and p holds the shared
+// fields.
+int check_sequence(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, int32_t k, int32_t pi, int32_t causal,
+                   const void *q, const void *kk, const void *v, int64_t sb, int64_t sh, int64_t sn, float scale,
+                   float logit_clamp, const void *out, int64_t osb, int64_t osh, int64_t osn, FwdParams &p,
+                   bool &empty) {
+    const int es = elem_size(dtype);
+    empty = false;
+    if (es == 0) return PI_ATTN_EUNSUPPORTED;
+    if (B < 0 || H < 0 || N < 0 || k < 0 || pi < 0) return PI_ATTN_EINVAL;
+    if (D != 64 && D != 128) return PI_ATTN_EUNSUPPORTED;
+    if (!isfinite(scale) || scale <= 0.0f || isnan(logit_clamp)) return PI_ATTN_EINVAL;
+    const int64_t rows = (int64_t)B * H * N;
+    if (rows >= kMaxRows) return PI_ATTN_EINVAL;
+    if (rows == 0) {
+        empty = true;
+        return PI_ATTN_OK;
+    }
+    if (!q || !kk || !v || !out) return PI_ATTN_EINVAL;
+    if (!aligned16(q) || !aligned16(kk) || !aligned16(v) || !aligned16(out)) return PI_ATTN_EINVAL;
+    if (!stride16(sb, es) || !stride16(sh, es) || !stride16(sn, es)) return PI_ATTN_EINVAL;
+    if (!stride16(osb, es) || !stride16(osh, es) || !stride16(osn, es)) return PI_ATTN_EINVAL;
+    if (dtype == PI_ATTN_BF16 && !tile_span_ok(k, N, causal != 0, sn, es)) return PI_ATTN_EUNSUPPORTED;
+    p.B = B; p.H = H; p.N = N; p.D = D; p.k = k; p.pi = pi; p.causal = causal != 0;
+    p.q = q; p.k_ptr = kk; p.v = v;
+    p.sb = sb; p.sh = sh; p.sn = sn;
+    p.scale = scale;
+    p.clamp = logit_clamp > 0.0f ? logit_clamp : 0.0f;
+    return PI_ATTN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -66,29 +101,14 @@ int pi_attn_forward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, i
                     int32_t causal, const void *q, const void *kk, const void *v, int64_t sb, int64_t sh, int64_t sn,
                     const float *gate, int64_t gsb, int64_t gsh, int64_t gsn, float scale, float logit_clamp,
                     void *out, int64_t osb, int64_t osh, int64_t osn, float *lse, void *stream) {
-    const int es = elem_size(dtype);
-    if (es == 0) return PI_ATTN_EUNSUPPORTED;
-    if (B < 0 || H < 0 || N < 0 || k < 0 || pi < 0) return PI_ATTN_EINVAL;
-    if (D != 64 && D != 128) return PI_ATTN_EUNSUPPORTED;
-    if (!isfinite(scale) || scale <= 0.0f || isnan(logit_clamp)) return PI_ATTN_EINVAL;
-    const int64_t rows = (int64_t)B * H * N;
-    if (rows >= kMaxRows) return PI_ATTN_EINVAL;
-    if (rows == 0) return PI_ATTN_OK;
-    if (!q || !kk || !v || !gate || !out) return PI_ATTN_EINVAL;
-    if (!aligned16(q) || !aligned16(kk) || !aligned16(v) || !aligned16(out)) return PI_ATTN_EINVAL;
-    if (!stride16(sb, es) || !stride16(sh, es) || !stride16(sn, es)) return PI_ATTN_EINVAL;
-    if (!stride16(osb, es) || !stride16(osh, es) || !stride16(osn, es)) return PI_ATTN_EINVAL;
-    if (!aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
-    if (lse && !aligned4(lse)) return PI_ATTN_EINVAL;
-    if (dtype == PI_ATTN_BF16 && !tile_span_ok(k, N, causal != 0, sn, es)) return PI_ATTN_EUNSUPPORTED;
-
     FwdParams p{};
-    p.B = B; p.H = H; p.N = N; p.D = D; p.k = k; p.pi = pi; p.causal = causal != 0;
-    p.q = q; p.k_ptr = kk; p.v = v;
-    p.sb = sb; p.sh = sh; p.sn = sn;
+    bool empty;
+    const int status = check_sequence(dtype, B, H, N, D, k, pi, causal, q, kk, v, sb, sh, sn, scale, logit_clamp,
+                                      out, osb, osh, osn, p, empty);
+    if (status != PI_ATTN_OK || empty) return status;
+    if (!gate || !aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
+    if (lse && !aligned4(lse)) return PI_ATTN_EINVAL;
     p.gate = gate; p.gsb = gsb; p.gsh = gsh; p.gsn = gsn;
-    p.scale = scale;
-    p.clamp = logit_clamp > 0.0f ? logit_clamp : 0.0f;
     p.out = out; p.osb = osb; p.osh = osh; p.osn = osn;
     p.lse = lse;
     const hipStream_t st = (hipStream_t)stream;
@@ -102,30 +122,17 @@ int pi_attn_forward_gated(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_
                           int64_t sn, const void *u, int64_t usb, int64_t usn, int32_t dh, const void *w2,
                           const float *b2, float scale, float logit_clamp, void *out, int64_t osb, int64_t osh,
                           int64_t osn, float *lse, float *gate_out, void *stream) {
+    if (dh < 1) return PI_ATTN_EINVAL;
+    FwdParams p{};
+    bool empty;
+    const int status = check_sequence(dtype, B, H, N, D, k, pi, causal, q, kk, v, sb, sh, sn, scale, logit_clamp,
+                                      out, osb, osh, osn, p, empty);
+    if (status != PI_ATTN_OK || empty) return status;
     const int es = elem_size(dtype);
-    if (es == 0) return PI_ATTN_EUNSUPPORTED;
-    if (B < 0 || H < 0 || N < 0 || k < 0 || pi < 0 || dh < 1) return PI_ATTN_EINVAL;
-    if (D != 64 && D != 128) return PI_ATTN_EUNSUPPORTED;
-    if (!isfinite(scale) || scale <= 0.0f || isnan(logit_clamp)) return PI_ATTN_EINVAL;
-    const int64_t rows = (int64_t)B * H * N;
-    if (rows >= kMaxRows) return PI_ATTN_EINVAL;
-    if (rows == 0) return PI_ATTN_OK;
-    if (!q || !kk || !v || !u || !w2 || !out || !gate_out) return PI_ATTN_EINVAL;
-    if (!aligned16(q) || !aligned16(kk) || !aligned16(v) || !aligned16(out) || !aligned16(u) || !aligned16(w2))
-        return PI_ATTN_EINVAL;
-    if (!stride16(sb, es) || !stride16(sh, es) || !stride16(sn, es)) return PI_ATTN_EINVAL;
-    if (!stride16(osb, es) || !stride16(osh, es) || !stride16(osn, es)) return PI_ATTN_EINVAL;
+    if (!u || !w2 || !gate_out || !aligned16(u) || !aligned16(w2)) return PI_ATTN_EINVAL;
     if (!stride16(usb, es) || !stride16(usn, es) || ((int64_t)dh * es) % 16 != 0) return PI_ATTN_EINVAL;
     if ((b2 && !aligned4(b2)) || !aligned4(gate_out) || (lse && !aligned4(lse))) return PI_ATTN_EINVAL;
-    if (dtype == PI_ATTN_BF16 && !tile_span_ok(k, N, causal != 0, sn, es)) return PI_ATTN_EUNSUPPORTED;
-
-    FwdParams p{};
-    p.B = B; p.H = H; p.N = N; p.D = D; p.k = k; p.pi = pi; p.causal = causal != 0;
-    p.q = q; p.k_ptr = kk; p.v = v;
-    p.sb = sb; p.sh = sh; p.sn = sn;
     p.gate = gate_out; p.gsb = (int64_t)H * N; p.gsh = N; p.gsn = 1;   // the logits this call computes
-    p.scale = scale;
-    p.clamp = logit_clamp > 0.0f ? logit_clamp : 0.0f;
     p.out = out; p.osb = osb; p.osh = osh; p.osn = osn;
     p.lse = lse;
     GateMlp m{};
@@ -144,34 +151,19 @@ int pi_attn_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, 
                      const float *lse, const void *out, const void *dout, int64_t osb, int64_t osh,
                      int64_t osn, float *dq,
                      float *dk, float *dv, float *dgate, float *rowterm, void *stream) {
-    const int es = elem_size(dtype);
-    if (es == 0) return PI_ATTN_EUNSUPPORTED;
-    if (B < 0 || H < 0 || N < 0 || k < 0 || pi < 0) return PI_ATTN_EINVAL;
-    if (D != 64 && D != 128) return PI_ATTN_EUNSUPPORTED;
-    if (!isfinite(scale) || scale <= 0.0f || isnan(logit_clamp)) return PI_ATTN_EINVAL;
-    const int64_t rows = (int64_t)B * H * N;
-    if (rows >= kMaxRows) return PI_ATTN_EINVAL;
-    if (rows == 0) return PI_ATTN_OK;
-    if (!q || !kk || !v || !gate || !lse || !out || !dout || !dq || !dk || !dv || !dgate || !rowterm)
-        return PI_ATTN_EINVAL;
-    if (!aligned16(q) || !aligned16(kk) || !aligned16(v) || !aligned16(dout) || !aligned16(out))
-        return PI_ATTN_EINVAL;
-    if (!stride16(sb, es) || !stride16(sh, es) || !stride16(sn, es)) return PI_ATTN_EINVAL;
-    if (!stride16(osb, es) || !stride16(osh, es) || !stride16(osn, es)) return PI_ATTN_EINVAL;
-    if (!aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
-    if (dtype == PI_ATTN_BF16 && !tile_span_ok(k, N, causal != 0, sn, es)) return PI_ATTN_EUNSUPPORTED;
+    BwdParams p{};
+    FwdParams &f = p.f;
+    bool empty;
+    // out shares dout's strides; it stands in for the forward output in the shared checks
+    const int status = check_sequence(dtype, B, H, N, D, k, pi, causal, q, kk, v, sb, sh, sn, scale, logit_clamp,
+                                      out, osb, osh, osn, f, empty);
+    if (status != PI_ATTN_OK || empty) return status;
+    if (!gate || !lse || !dout || !dq || !dk || !dv || !dgate || !rowterm) return PI_ATTN_EINVAL;
+    if (!aligned16(dout) || !aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
     if (!aligned4(lse) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv) || !aligned4(dgate) ||
         !aligned4(rowterm))
         return PI_ATTN_EINVAL;
-
-    BwdParams p{};
-    FwdParams &f = p.f;
-    f.B = B; f.H = H; f.N = N; f.D = D; f.k = k; f.pi = pi; f.causal = causal != 0;
-    f.q = q; f.k_ptr = kk; f.v = v;
-    f.sb = sb; f.sh = sh; f.sn = sn;
     f.gate = gate; f.gsb = gsb; f.gsh = gsh; f.gsn = gsn;
-    f.scale = scale;
-    f.clamp = logit_clamp > 0.0f ? logit_clamp : 0.0f;
     p.dtype = dtype == PI_ATTN_BF16 ? 1 : 0;
     p.lse = lse;
     p.out = out; p.dout = dout; p.osb = osb; p.osh = osh; p.osn = osn;

@@ -93,6 +93,38 @@ def test_forward_empty_is_noop(lib, kw):
     assert fwd(lib, **kw) == 0
 
 
+def gated(lib, **kw):
+    a = dict(dtype=1, B=1, H=2, N=256, D=64, k=4, pi=16, causal=1, q=16, kk=16, v=16, sb=32768, sh=16384, sn=64,
+             u=16, usb=256 * 64, usn=64, dh=64, w2=16, b2=16, scale=0.125, clamp=0.0, out=16, osb=32768, osh=16384,
+             osn=64, lse=None, gate_out=16, stream=None)
+    a.update(kw)
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.pi_attn_forward_gated(a["dtype"], a["B"], a["H"], a["N"], a["D"], a["k"], a["pi"], a["causal"],
+                                     vp(a["q"]), vp(a["kk"]), vp(a["v"]), a["sb"], a["sh"], a["sn"], vp(a["u"]),
+                                     a["usb"], a["usn"], a["dh"], vp(a["w2"]), vp(a["b2"]), a["scale"], a["clamp"],
+                                     vp(a["out"]), a["osb"], a["osh"], a["osn"], vp(a["lse"]), vp(a["gate_out"]),
+                                     vp(a["stream"]))
+
+
+# every case has exactly one fault, so nothing is ever launched
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=4), EUNSUP), (dict(D=32), EUNSUP), (dict(B=-1), EINVAL), (dict(k=-1), EINVAL),
+    (dict(dh=0), EINVAL), (dict(dh=12), EINVAL), (dict(u=None), EINVAL), (dict(u=8), EINVAL),
+    (dict(w2=None), EINVAL), (dict(w2=24), EINVAL), (dict(b2=18), EINVAL), (dict(gate_out=None), EINVAL),
+    (dict(gate_out=2), EINVAL), (dict(usn=4), EINVAL), (dict(usb=-64), EINVAL), (dict(q=None), EINVAL),
+    (dict(out=8), EINVAL), (dict(lse=6), EINVAL), (dict(scale=0.0), EINVAL), (dict(clamp=float("nan")), EINVAL),
+    (dict(dtype=0, dh=6), EINVAL),
+    (dict(causal=0, N=1 << 16, k=40000, sn=1 << 14, sh=1 << 30, sb=1 << 31), EUNSUP),
+])
+def test_forward_gated_rejects(lib, kw, code):
+    assert gated(lib, **kw) == code
+
+
+@pytest.mark.parametrize("kw", [dict(N=0), dict(H=0), dict(N=0, u=None, gate_out=None)])
+def test_forward_gated_empty_is_noop(lib, kw):
+    assert gated(lib, **kw) == 0
+
+
 def bwd(lib, **kw):
     a = dict(dtype=1, B=1, H=2, N=256, D=64, k=32, pi=64, causal=1, q=16, kk=16, v=16, sb=32768, sh=16384,
              sn=64, gate=16, gsb=0, gsh=1, gsn=0, scale=0.125, clamp=0.0, lse=16, out=16, dout=16, osb=32768,
