@@ -41,9 +41,14 @@ BACKWARD_TRAFFIC = {True: os.path.join(ROOT, "profiles", "backward_bf16_fwd32k_h
 SMALLK_TRAFFIC = {"gated": os.path.join(ROOT, "profiles", "smallk_bf16_gated_smallk8k_hbm_traffic.txt"),
                   "gated_bidirectional": os.path.join(ROOT, "profiles",
                                                       "smallk_bf16_gated_bidir_smallk8k_hbm_traffic.txt"),
-                  "per_head_gate": os.path.join(ROOT, "profiles", "smallk_bf16_smallk8k_hbm_traffic.txt")}
+                  "per_head_gate": os.path.join(ROOT, "profiles", "smallk_bf16_smallk8k_hbm_traffic.txt"),
+                  "backward": os.path.join(ROOT, "profiles", "smallk_bwd_bf16_smallk8k_hbm_traffic.txt"),
+                  "backward_bidirectional": os.path.join(ROOT, "profiles",
+                                                         "smallk_bwd_bf16_bidir_smallk8k_hbm_traffic.txt")}
 FORWARD_SOURCES = ("forward_bf16.hip", "pi_common.h", "kernels.h")
-SMALLK_SOURCES = ("smallk_bf16.hip", "smallk.h", "pi_common.h", "kernels.h")
+SMALLK_SOURCES = ("smallk_bf16.hip", "smallk_common.h", "smallk.h", "pi_common.h", "kernels.h")
+SMALLK_BWD_SOURCES = ("smallk_bwd_bf16.hip", "smallk_common.h", "smallk.h", "backward.hip", "pi_common.h",
+                      "kernels.h")
 BACKWARD_SOURCES = ("backward_bf16.hip", "backward_kv_bf16.hip", "backward.hip", "pi_common.h", "kernels.h")
 
 
@@ -222,7 +227,15 @@ def pmc_probe(W, pa, torch, dev):
             pa.pi_attn_forward_gated(q, k, v, u, w2, b2, scfg.k, scfg.pi, out=out, causal=causal)
     torch.cuda.synchronize()
     print("probe: 3 x small-window forward, 3 x gated (causal, bidirectional) smallk8k", flush=True)
-    del q, k, v, u, w2, out
+    dout = W.cotangent(q.shape, q.dtype, 0, dev)
+    for causal in (True, False):
+        y, lse = pa.pi_attn_forward(q, k, v, gate, scfg.k, scfg.pi, return_lse=True, causal=causal)
+        for _ in range(3):
+            pa.pi_attn_backward(q, k, v, gate, scfg.k, scfg.pi, y, lse, dout, causal=causal)
+        torch.cuda.synchronize()
+        print(f"probe: 3 x small-window backward smallk8k causal={causal}", flush=True)
+        del y, lse
+    del q, k, v, u, w2, out, dout
     dcfg = W.DECODE["decode"]
     kc, vc, lens, dgate = W.decode_state(dcfg, 0, dev)
     qs, ks, vs = W.decode_tokens(dcfg, 3, 1, dev)
@@ -379,8 +392,8 @@ def main():
 
 def bench_smallk(W, pa, torch, dev, stream, steps, warmup):
     """The small-window gather path on smallk8k: the gated forward (gate MLP's
-    last layer fused), causal and bidirectional, and the forward with given
-    per-head gate logits."""
+    last layer fused), causal and bidirectional, the forward with given
+    per-head gate logits, and the backward (causal and bidirectional)."""
     cfg = W.FORWARD["smallk8k"]
     q, k, v, gate = W.forward_inputs(cfg, 0, dev)
     u, w2, b2 = W.gate_mlp_inputs(cfg, 0, dev)
@@ -405,7 +418,23 @@ def bench_smallk(W, pa, torch, dev, stream, steps, warmup):
                      "query_positions_per_s": round(cfg.B * cfg.N / (ms / 1e3), 1),
                      "attended_keys_per_s": round(keys / (ms / 1e3), 1),
                      "bytes_per_step": nbytes, "roofline": rl}
-    del q, k, v, u, w2, out, g
+    del u, w2, out, g
+    for name, causal in (("backward", True), ("backward_bidirectional", False)):
+        y, lse = pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi, return_lse=True, causal=causal)
+        dout = W.cotangent(q.shape, q.dtype, 0, dev)
+        ms, _, _ = time_launches(
+            torch, lambda c=causal: pa.pi_attn_backward(q, k, v, gate, cfg.k, cfg.pi, y, lse, dout, causal=c),
+            steps, warmup, stream)
+        keys, flops, nbytes = backward_algorithmic(cfg, causal)
+        mode = "false" if causal else "true"
+        rl, _ = roofline_of(flops, nbytes, ms / 1e3,
+                            f"smallk_bwd_q_kernel<64,{mode},4> + smallk_bwd_kv_kernel<64,{mode},4>",
+                            measured_traffic(csrc_digest(SMALLK_BWD_SOURCES), SMALLK_TRAFFIC[name]))
+        res[name] = {"us_per_step": round(ms * 1e3, 2),
+                     "query_positions_per_s": round(cfg.B * cfg.N / (ms / 1e3), 1),
+                     "bytes_per_step": nbytes, "roofline": rl}
+        del y, lse, dout
+    del q, k, v
     torch.cuda.empty_cache()
     return res
 

@@ -23,6 +23,7 @@
 // inputs run the MFMA passes of backward_bf16.hip and backward_kv_bf16.hip.
 #include "kernels.h"
 #include "pi_common.h"
+#include "smallk.h"
 
 namespace pi_attn {
 
@@ -234,6 +235,7 @@ hipError_t launch(const BwdParams &p, hipStream_t stream) {
 
 hipError_t launch_backward(const BwdParams &p, hipStream_t stream) {
     if ((int64_t)p.f.B * p.f.H * p.f.N == 0) return hipSuccess;
+    if (p.dtype == 1 && p.f.k <= kSmallK) return launch_backward_smallk(p, stream);
     if (p.dtype == 1) return p.f.D == 64 ? launch<64, __bf16>(p, stream) : launch<128, __bf16>(p, stream);
     return p.f.D == 64 ? launch<64, float>(p, stream) : launch<128, float>(p, stream);
 }

@@ -30,4 +30,9 @@ hipError_t launch_forward_smallk(const FwdParams &p, const GateMlp *mlp, hipStre
 // The gate logits alone, into mlp.gate_out (bf16 on MFMA, float32 on VALU).
 hipError_t launch_gate_logits(const FwdParams &p, const GateMlp &mlp, int dtype, hipStream_t stream);
 
+// Small-window backward (k <= kSmallK), bf16, D = 64 or 128: a query pass
+// (dq, gate gradient, exact row terms) and a key pass (dk, dv), both in the
+// forward's work decomposition.  Needs the forward's lse.
+hipError_t launch_backward_smallk(const BwdParams &p, hipStream_t stream);
+
 }  // namespace pi_attn

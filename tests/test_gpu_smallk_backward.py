@@ -1,0 +1,139 @@
+"""GPU parity of the small-window backward (bf16, k <= 16: the gather-style
+query and key passes) against the fp64 oracle gradients, through the C ABI.
+
+Every weight and product of this path is fp32 from exact bf16 products (no
+bf16 rounding of the softmax weights), so the bf16 bar of the other
+backward tests -- per gradient tensor max-abs within 2e-2 * max(1, max|ref|)
+and relative L2 within 5e-3 -- is loose here; the cases also hold a tighter
+bar of 2e-3 relative L2 that catches a dropped term or a misplaced entry
+(one missing entry out of k + 2 moves a gradient by far more), plus an
+absolute RMS floor of 1e-5 for gradients that are zero in exact arithmetic
+(the gate gradient when pi <= k: every entry then carries the same prior).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2511_10696_amd as pa
+from paper_2511_10696_amd import workloads as W
+from tests.test_gpu_backward import assert_grad, np32
+
+pytestmark = pytest.mark.gpu
+
+TIGHT_RELL2 = 2e-3
+
+
+def run_case(q, k, v, gate, kw, pi, seed, causal, clamp=0.0, scale=None, tight=True):
+    out, lse = pa.pi_attn_forward(q, k, v, gate, kw, pi, return_lse=True, logit_clamp=clamp, scale=scale,
+                                  causal=causal)
+    dout = W.cotangent(q.shape, q.dtype, seed, q.device)
+    dq, dk, dv, dg = pa.pi_attn_backward(q, k, v, gate, kw, pi, out, lse, dout, logit_clamp=clamp, scale=scale,
+                                         gate_grad_per_query=True, causal=causal)
+    torch.cuda.synchronize()
+    refs = oracle.backward(q, k, v, gate, kw, pi, dout, scale=scale, clamp=clamp, causal=causal)
+    for name, got, ref in zip(("dq", "dk", "dv", "dgate"), (dq, dk, dv, dg), refs):
+        g = np32(got)
+        assert_grad(g, ref, name, q.dtype)
+        if tight:
+            nr, ne = np.linalg.norm(ref), float(np.linalg.norm(g - ref))
+            assert ne <= TIGHT_RELL2 * nr + 1e-5 * np.sqrt(ref.size), f"{name}: rel-L2 {ne / max(nr, 1e-300):.3g}"
+    return dq, dk, dv, dg
+
+
+def inputs(B, H, N, D, seed, per_query_gate=False):
+    cfg = W.ForwardConfig("custom", B, H, N, D, 0, 0, torch.bfloat16)
+    return W.forward_inputs(cfg, seed, "cuda", per_query_gate)
+
+
+SHAPES = [
+    (2, 3, 100, 64, 4, 16),       # the paper's default window and period, ragged tail
+    (1, 2, 257, 128, 4, 16),      # D = 128
+    (1, 1, 1, 64, 4, 16),         # a single position
+    (1, 2, 70, 64, 0, 0),         # self only
+    (1, 2, 90, 64, 16, 40),       # the largest window of the path
+    (1, 40, 65, 64, 2, 8),        # more heads than one group
+    (1, 3, 200, 128, 8, 3),       # pi <= k: no partner slot
+    (1, 2, 300, 64, 4, 1000),     # partner beyond the sequence
+    (2, 5, 1000, 64, 3, 64),
+    (1, 2, 33, 128, 16, 32),      # tile boundary, band wider than the tile
+    (1, 2, 64, 64, 5, 31),        # partner exactly one tile back
+]
+
+
+@pytest.mark.parametrize("B,H,N,D,k,pi", SHAPES)
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("pq", [False, True])
+def test_backward_shapes(device, B, H, N, D, k, pi, causal, pq):
+    q, k_, v, gate = inputs(B, H, N, D, 21, pq)
+    run_case(q, k_, v, gate, k, pi, 21, causal)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_backward_clamp(device, causal):
+    """Heavy-tailed rows with a clamp that saturates some logits (their
+    gradient through the clamp is zero) and one that does not."""
+    cfg = W.ForwardConfig("hh", 1, 2, 300, 64, 4, 16, torch.bfloat16, heavy_frac=0.05, heavy_mult=8.0)
+    q, k, v, gate = W.forward_inputs(cfg, 2, device, per_query_gate=True)
+    for clamp in (20.0, 3.0):
+        run_case(q, k, v, gate, 4, 16, 2, causal, clamp=clamp, scale=0.5)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_backward_per_head_gate_sum(device, causal):
+    """The per-head gate gradient (the binding's sum over b and t) equals the
+    oracle's per-query gradient summed, within the bf16 factor of the summed
+    magnitudes."""
+    q, k, v, gate = inputs(2, 3, 400, 64, 5)
+    out, lse = pa.pi_attn_forward(q, k, v, gate, 4, 16, return_lse=True, causal=causal)
+    dout = W.cotangent(q.shape, q.dtype, 5, device)
+    *_, dgh = pa.pi_attn_backward(q, k, v, gate, 4, 16, out, lse, dout, causal=causal)
+    torch.cuda.synchronize()
+    rg = oracle.backward(q, k, v, gate, 4, 16, dout, causal=causal)[3]
+    bound = 2e-3 * np.maximum(1.0, np.abs(rg).sum(axis=(0, 2)))
+    assert (np.abs(np32(dgh) - rg.sum(axis=(0, 2))) <= bound).all()
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_backward_deterministic(device, causal):
+    q, k, v, gate = inputs(1, 4, 500, 128, 8, True)
+    out, lse = pa.pi_attn_forward(q, k, v, gate, 4, 16, return_lse=True, causal=causal)
+    dout = W.cotangent(q.shape, q.dtype, 8, device)
+    a = pa.pi_attn_backward(q, k, v, gate, 4, 16, out, lse, dout, gate_grad_per_query=True, causal=causal)
+    b = pa.pi_attn_backward(q, k, v, gate, 4, 16, out, lse, dout, gate_grad_per_query=True, causal=causal)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+def test_backward_causal_key_support(device):
+    """Causal: the gradient of key j comes only from queries t >= j, so
+    changing q and dL/dy after row c leaves dk, dv of keys whose queries all
+    lie at or before c unchanged -- keys j with j + k <= c and, where the
+    partner exists, j + pi <= c."""
+    kw, pi, N = 4, 16, 300
+    q, k, v, gate = inputs(1, 2, N, 64, 9, True)
+    out, lse = pa.pi_attn_forward(q, k, v, gate, kw, pi, return_lse=True)
+    dout = W.cotangent(q.shape, q.dtype, 9, device)
+    base = pa.pi_attn_backward(q, k, v, gate, kw, pi, out, lse, dout, gate_grad_per_query=True)
+    c = 150
+    q2, d2 = q.clone(), dout.clone()
+    q2[:, :, c + 1:] = -q2[:, :, c + 1:]
+    d2[:, :, c + 1:] = 2 * d2[:, :, c + 1:]
+    out2, lse2 = pa.pi_attn_forward(q2, k, v, gate, kw, pi, return_lse=True)
+    g2 = pa.pi_attn_backward(q2, k, v, gate, kw, pi, out2, lse2, d2, gate_grad_per_query=True)
+    torch.cuda.synchronize()
+    keep = c - pi + 1    # keys j < keep have every query (j .. j + k and j + pi) at or before c
+    for i in (1, 2):
+        assert torch.equal(base[i][:, :, :keep], g2[i][:, :, :keep])
+    for i in (0, 3):     # dq and dgate of rows <= c depend on rows <= c only
+        assert torch.equal(base[i][:, :, :c + 1], g2[i][:, :, :c + 1])
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_backward_config_smallk8k(device, causal):
+    """The full small-window workload (B8 H16 N8192 D64 k4 pi16), all gradients
+    against the oracle."""
+    cfg = W.FORWARD["smallk8k"]
+    q, k, v, gate = W.forward_inputs(cfg, 0, device, per_query_gate=True)
+    run_case(q, k, v, gate, cfg.k, cfg.pi, 0, causal)
