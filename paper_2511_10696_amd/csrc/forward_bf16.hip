@@ -21,8 +21,8 @@
 // and A = V^T comes from the LDS transpose read (ds_read_b64_tr_b16) of the
 // row-major value tile, with the same permutation.
 //
-// Tiles are staged global -> registers -> LDS, the next tile in two halves
-// while the two blocks of the current one are consumed, row-major with the
+// Tiles are staged global -> registers -> LDS, the next tile while the two
+// blocks of the current one are consumed, row-major with the
 // 16-byte chunks of row r XOR-swizzled (K: chunk ^ (r mod chunks-per-row);
 // V: chunk ^ 2(r mod 4)) so that the fragment reads and the transpose reads
 // are free of bank conflicts.  The global side uses buffer loads whose
@@ -432,15 +432,31 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
                 ws.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[cc][db], pb[cc], ws.o[db], 0, 0, 0);
         }
     };
-    // One 64-row tile; while block blk is consumed, half blk of the next tile
-    // (if any) is loaded into registers and then stored to the other buffer,
-    // which every wavefront finished reading before the last barrier.
+    // One 64-row tile; the next tile (if any) is loaded into registers and
+    // stored to the other buffer, which every wavefront finished reading
+    // before the last barrier.  D = 128 loads the whole next tile before the
+    // first block (two blocks of latency cover the loads); D = 64 loads half
+    // blk while block blk is consumed (its four wavefronts per SIMD leave no
+    // registers for a second half).
     auto tile = [&](const TileBuf<D> &cur, int row0, TileBuf<D> &nxt, bool has_next) {
+        if constexpr (D == 128) {
+            if (has_next) {
 #pragma unroll
-        for (int blk = 0; blk < BPT; ++blk) {
-            if (has_next) tile_load<D>(st, rk, rv, rowb, row0 - kb0 + TK, blk, tid);
-            block(cur.k, cur.v, row0 + 32 * blk, blk);
-            if (has_next) tile_store<D>(st, nxt, blk, tid);
+                for (int hf = 0; hf < BPT; ++hf) tile_load<D>(st0[hf], rk, rv, rowb, row0 - kb0 + TK, hf, tid);
+            }
+#pragma unroll
+            for (int blk = 0; blk < BPT; ++blk) block(cur.k, cur.v, row0 + 32 * blk, blk);
+            if (has_next) {
+#pragma unroll
+                for (int hf = 0; hf < BPT; ++hf) tile_store<D>(st0[hf], nxt, hf, tid);
+            }
+        } else {
+#pragma unroll
+            for (int blk = 0; blk < BPT; ++blk) {
+                if (has_next) tile_load<D>(st, rk, rv, rowb, row0 - kb0 + TK, blk, tid);
+                block(cur.k, cur.v, row0 + 32 * blk, blk);
+                if (has_next) tile_store<D>(st, nxt, blk, tid);
+            }
         }
     };
     // Double buffering, unrolled by two so that every store and every read
