@@ -11,6 +11,12 @@ bidirectional forward on the same shape, the backward (pi_attn_backward,
 causal and bidirectional) on that shape with a seeded dL/dy, and the fp64
 CPU oracle on a bounded sample of the forward workload.
 
+The forward is also timed cold: single launches, each after a 1 GiB device
+fill that evicts the L2s and the last-level cache (reported beside the
+steady-state figure, which is the headline).  The decode step reports the mean
+over its 1000 steps and, from a second pass over the same steps with an event
+after each, the median and p99 of the per-step times.
+
 Every timed loop is preceded by a settling phase (the same launches, untimed,
 for at least SETTLE_S seconds, so the GPU clocks have left their idle state)
 and by the warm-up launches; the timed region is exactly the stated number
@@ -63,6 +69,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--cold-reps", type=int, default=10,
+                    help="single forward launches timed after an L2/last-level-cache flush")
     ap.add_argument("--decode-steps", type=int, default=1000)
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--backward-steps", type=int, default=20)
@@ -130,6 +138,34 @@ def time_launches(torch, fn, steps, warmup, stream):
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     return e0.elapsed_time(e1) / steps, t_wall, settle
+
+
+FLUSH_BYTES = 1 << 30    # written between cold launches: 4x the 256 MB last-level cache plus the L2s
+
+
+def device_info(torch, dev):
+    pr = torch.cuda.get_device_properties(dev)
+    return {"name": pr.name, "arch": getattr(pr, "gcnArchName", None), "compute_units": pr.multi_processor_count,
+            "hbm_bytes": pr.total_memory, "hbm_peak_gbs": HBM_PEAK_GBS, "mfma_bf16_peak_tflops": MFMA_BF16_PEAK_TFLOPS}
+
+
+def time_cold(torch, fn, reps, stream):
+    """Median and minimum ms of `reps` single launches, each after a 1 GiB
+    device fill (untimed) that evicts the inputs from the L2s and the
+    last-level cache, so every launch reads its inputs from HBM."""
+    flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=stream.device)
+    times = []
+    for i in range(reps):
+        flush.fill_(float(i))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    del flush
+    times.sort()
+    return times[len(times) // 2], times[0]
 
 
 def roofline_of(flops, nbytes, sec, kernel, traffic=None):
@@ -281,6 +317,8 @@ def main():
         torch, lambda: pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi, out=out), args.steps, args.warmup, stream)
     sec = ms / 1e3
     value = cfg.B * cfg.N / sec
+    cold_ms, cold_min = time_cold(torch, lambda: pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi, out=out),
+                                  args.cold_reps, stream)
     keys, flops, nbytes = forward_algorithmic(cfg)
     digest = csrc_digest(FORWARD_SOURCES)
     roofline, roofline_mfma = roofline_of(flops, nbytes, sec, "forward_bf16_kernel<128,false,false,false>",
@@ -330,6 +368,7 @@ def main():
             pa.pi_attn_decode_step(lbuf[i % 2], qs[i], ks[i], vs[i], kc, vc, dgate, dcfg.k, dcfg.pi,
                                    len_out=lbuf[(i + 1) % 2], out=dout)
             si[0] += 1
+        lens0 = lens.clone()
         d0, d1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         d0.record(stream)
         for _ in range(nsteps):
@@ -337,6 +376,18 @@ def main():
         d1.record(stream)
         torch.cuda.synchronize()
         dms = d0.elapsed_time(d1) / nsteps
+        # the same steps again from the same lengths, an event after each, for
+        # the per-step distribution (the events add a little time per step,
+        # so the mean above is taken without them)
+        lbuf[0].copy_(lens0)
+        si[0] = 0
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(nsteps + 1)]
+        ev[0].record(stream)
+        for i in range(nsteps):
+            step()
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        per = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(nsteps))
         dkeys, dbytes = decode_algorithmic(dcfg, dcfg.cache_len)
         ddigest = source_digest([os.path.join(ROOT, "paper_2511_10696_amd", "csrc", f)
                                  for f in ("decode_bf16.hip", "pi_common.h", "kernels.h")])
@@ -344,6 +395,8 @@ def main():
         dgbs = dbytes / (dms / 1e3) / 1e9
         decode = {"workload": "decode S64 H32 D128 k512 pi1024 cache32768 bf16", "steps": nsteps,
                   "ms_per_step": round(dms, 5), "us_per_step": round(dms * 1e3, 2),
+                  "us_per_step_p50": round(per[len(per) // 2] * 1e3, 2),
+                  "us_per_step_p99": round(per[min(len(per) - 1, (99 * len(per)) // 100)] * 1e3, 2),
                   "queries_per_s": round(dcfg.S / (dms / 1e3), 1),
                   "roofline": {"bound": "hbm", "kernel": "decode_bf16_kernel<128>",
                                "achieved": round(dgbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -379,6 +432,11 @@ def main():
         "roofline": roofline,
         "roofline_mfma": roofline_mfma,
         "settle_s": round(settle, 3),
+        "cold": {"ms_per_step_median": round(cold_ms, 5), "ms_per_step_min": round(cold_min, 5),
+                 "reps": args.cold_reps,
+                 "note": "single launches, each after a 1 GiB device fill that evicts the L2s and the "
+                         "last-level cache; the headline value is the steady-state (hot) loop"},
+        "device": device_info(torch, dev),
         "bidirectional": bidir,
         "smallk": smallk,
         "decode": decode,
