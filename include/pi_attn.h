@@ -209,7 +209,10 @@ int pi_attn_decode_step(int32_t dtype, int32_t S, int32_t H, int32_t D, int32_t 
  *                (float32: from out; bf16: as recomputed by the query pass).
  * Kernels on the stream, in order: (float32) the row terms, then a query
  * pass (dq, dgate; for bf16 it also writes the row terms) and a key pass
- * (dk, dv).  Nothing is allocated; buffers must not overlap.
+ * (dk, dv).  bf16 with k <= 16 takes gather-style passes whose weights and
+ * products stay in float32 throughout (the row terms exact); larger windows
+ * take the banded MFMA passes, whose softmax gradients enter the products
+ * rounded to bf16.  Nothing is allocated; buffers must not overlap.
  * Errors: as pi_attn_forward, plus EINVAL for a null or misaligned lse,
  * out, dout, dq, dk, dv, dgate or rowterm.
  */
