@@ -226,6 +226,23 @@ int pi_attn_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D,
                      float *dq, float *dk, float *dv, float *dgate, float *rowterm,
                      void *stream);
 
+/*
+ * pi_attn_gate_grad_per_head -- the gradient of a per-head gate logit g_h
+ * shared by every b and t: out[h] = sum over b, t of dgate[b][h][t], the
+ * per-query gradients pi_attn_backward writes (the gate enters each query's
+ * prior separately, Sec. 3.5 eqs. ddelta_da and dalpha_da, so its gradient
+ * is the sum of the per-query ones).
+ *   B, H, N      sizes, >= 0; B*H*N below 2^31.
+ *   dgate        device float32 [B][H][N] contiguous (may be null when
+ *                B*N == 0).
+ *   out          device float32 [H], overwritten (zeros when B*N == 0).
+ * The sums are taken in fp64 in a fixed order: results are deterministic.
+ * One kernel on the stream; nothing is allocated.
+ * Errors: EINVAL for negative sizes, B*H*N too large, a null or misaligned
+ * out (H > 0) or dgate (B*N > 0).
+ */
+int pi_attn_gate_grad_per_head(int32_t B, int32_t H, int32_t N, const float *dgate, float *out, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -26,7 +26,8 @@ __all__ = ["pi_attn_index_set", "pi_attn_forward", "pi_attn_forward_gated", "pi_
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpi_attn.so")
 EXPORTED_SYMBOLS = ("pi_attn_strerror", "pi_attn_ws_width", "pi_attn_index_set",
-                    "pi_attn_forward", "pi_attn_forward_gated", "pi_attn_decode_step", "pi_attn_backward")
+                    "pi_attn_forward", "pi_attn_forward_gated", "pi_attn_decode_step", "pi_attn_backward",
+                    "pi_attn_gate_grad_per_head")
 
 PI_ATTN_F32, PI_ATTN_BF16 = 0, 1
 
@@ -68,6 +69,8 @@ def library() -> ctypes.CDLL:
                                                          f32, f32, vp, vp, vp, i64, i64, i64,
                                                          vp, vp, vp, vp, vp, vp])
             lib.pi_attn_backward.restype = ctypes.c_int
+            lib.pi_attn_gate_grad_per_head.argtypes = [i32, i32, i32, vp, vp, vp]
+            lib.pi_attn_gate_grad_per_head.restype = ctypes.c_int
             _lib = lib
     return _lib
 
@@ -291,7 +294,10 @@ def pi_attn_backward(q, k, v, gate, k_window: int, pi: int, out, lse, dout, scal
         _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg), _ptr(rowterm), _stream_handle(stream, q.device))
     _check(st, "pi_attn_backward")
     if tuple(gate.shape) == (H,) and not gate_grad_per_query:
-        dg = dg.sum(dim=(0, 2))
+        dgh = torch.empty((H,), **f32)
+        _check(library().pi_attn_gate_grad_per_head(B, H, N, _ptr(dg), _ptr(dgh), _stream_handle(stream, q.device)),
+               "pi_attn_gate_grad_per_head")
+        dg = dgh
     return dq, dk, dv, dg
 
 

@@ -205,4 +205,13 @@ int pi_attn_decode_step(int32_t dtype, int32_t S, int32_t H, int32_t D, int32_t 
     return from_hip(dtype == PI_ATTN_BF16 ? launch_decode_bf16(p, st) : launch_decode_f32(p, st));
 }
 
+int pi_attn_gate_grad_per_head(int32_t B, int32_t H, int32_t N, const float *dgate, float *out, void *stream) {
+    if (B < 0 || H < 0 || N < 0) return PI_ATTN_EINVAL;
+    if ((int64_t)B * H * N >= kMaxRows) return PI_ATTN_EINVAL;
+    if (H == 0) return PI_ATTN_OK;
+    if (!out || !aligned4(out)) return PI_ATTN_EINVAL;
+    if ((int64_t)B * N > 0 && (!dgate || !aligned4(dgate))) return PI_ATTN_EINVAL;
+    return from_hip(launch_gate_grad_per_head(B, H, N, dgate, out, (hipStream_t)stream));
+}
+
 }  // extern "C"

@@ -233,6 +233,36 @@ hipError_t launch(const BwdParams &p, hipStream_t stream) {
 
 }  // namespace
 
+namespace {
+
+// One work-group per head: thread i sums entries i, i + 256, ... of the
+// head's B*N per-query gradients in fp64, then a fixed-shape tree in LDS.
+__global__ __launch_bounds__(256) void gate_grad_per_head_kernel(int B, int H, int N, const float *dgate,
+                                                                 float *out) {
+    __shared__ double part[256];
+    const int h = blockIdx.x;
+    const int64_t count = (int64_t)B * N;
+    double acc = 0.0;
+    for (int64_t i = threadIdx.x; i < count; i += 256) {
+        const int64_t b = i / N, t = i - b * N;
+        acc += (double)dgate[(b * H + h) * N + t];
+    }
+    part[threadIdx.x] = acc;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) out[h] = (float)part[0];
+}
+
+}  // namespace
+
+hipError_t launch_gate_grad_per_head(int B, int H, int N, const float *dgate, float *out, hipStream_t stream) {
+    if (H == 0) return hipSuccess;
+    return launch_kernel(gate_grad_per_head_kernel, dim3((unsigned)H), dim3(256), stream, B, H, N, dgate, out);
+}
+
 hipError_t launch_backward(const BwdParams &p, hipStream_t stream) {
     if ((int64_t)p.f.B * p.f.H * p.f.N == 0) return hipSuccess;
     if (p.dtype == 1 && p.f.k <= kSmallK) return launch_backward_smallk(p, stream);

@@ -72,6 +72,9 @@ hipError_t launch_decode_bf16(const DecodeParams &p, hipStream_t stream);
 // key pass (dk, dv).
 hipError_t launch_backward(const BwdParams &p, hipStream_t stream);
 
+// out[h] = sum over b and t of dgate[b][h][t] (fixed order, fp64 sums).
+hipError_t launch_gate_grad_per_head(int B, int H, int N, const float *dgate, float *out, hipStream_t stream);
+
 // MFMA query pass (dq, dgate) for bf16 inputs; needs the row terms.
 hipError_t launch_backward_q_bf16(const BwdParams &p, hipStream_t stream);
 

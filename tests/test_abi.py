@@ -157,6 +157,27 @@ def test_backward_empty_is_noop(lib, kw):
     assert bwd(lib, **kw) == 0
 
 
+def ggh(lib, **kw):
+    a = dict(B=2, H=3, N=100, dg=16, out=16, stream=None)
+    a.update(kw)
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.pi_attn_gate_grad_per_head(a["B"], a["H"], a["N"], vp(a["dg"]), vp(a["out"]), vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=-1), EINVAL), (dict(H=-1), EINVAL), (dict(N=-1), EINVAL), (dict(out=None), EINVAL),
+    (dict(out=2), EINVAL), (dict(dg=None), EINVAL), (dict(dg=6), EINVAL),
+    (dict(B=1 << 16, H=1 << 8, N=1 << 8), EINVAL),
+])
+def test_gate_grad_per_head_rejects(lib, kw, code):
+    assert ggh(lib, **kw) == code
+
+
+@pytest.mark.parametrize("kw", [dict(H=0), dict(H=0, dg=None, out=None)])
+def test_gate_grad_per_head_no_heads_is_noop(lib, kw):
+    assert ggh(lib, **kw) == 0
+
+
 def dec(lib, **kw):
     a = dict(dtype=1, S=2, H=2, D=128, cap=64, k=4, pi=8, len_in=64, len_out=128, q=16, kn=16, vn=16,
              kc=16, vc=16, gate=16, gss=0, gsh=1, scale=0.1, clamp=0.0, out=16, lse=None, stream=None)

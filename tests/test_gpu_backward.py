@@ -133,3 +133,27 @@ def test_backward_clamp(device, dtype):
     assert margin > 1e-3
     gate = torch.full((H,), g, device="cuda")
     run_case(q, kk, v, gate, kw, pi, 5, clamp=clamp, scale=0.125)
+
+
+@pytest.mark.parametrize("B,H,N", [(2, 3, 1000), (1, 40, 70001), (3, 1, 1), (2, 5, 0)])
+def test_gate_grad_per_head(device, B, H, N):
+    """pi_attn_gate_grad_per_head sums the per-query gate gradients over b
+    and t: against an fp64 sum of the same values, within 1e-6 of the summed
+    magnitudes (fp64 sums, one float32 rounding at the end); zeros when
+    there are no queries; deterministic."""
+    import ctypes
+    g = torch.Generator(device="cuda").manual_seed(B * 1000 + H)
+    dg = torch.randn(B, H, N, generator=g, device="cuda") * 3
+    out = torch.full((H,), float("nan"), device="cuda")
+    lib = pa.library()
+    st = lib.pi_attn_gate_grad_per_head(B, H, N, ctypes.c_void_p(dg.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+                                        None)
+    assert st == 0
+    torch.cuda.synchronize()
+    ref = np32(dg).astype(np.float64).sum(axis=(0, 2))
+    bound = 1e-6 * np.maximum(1.0, np.abs(np32(dg)).astype(np.float64).sum(axis=(0, 2)))
+    assert (np.abs(np32(out) - ref) <= bound).all()
+    out2 = torch.empty_like(out)
+    lib.pi_attn_gate_grad_per_head(B, H, N, ctypes.c_void_p(dg.data_ptr()), ctypes.c_void_p(out2.data_ptr()), None)
+    torch.cuda.synchronize()
+    assert torch.equal(out, out2)
