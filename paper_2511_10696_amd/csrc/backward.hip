@@ -235,21 +235,31 @@ hipError_t launch(const BwdParams &p, hipStream_t stream) {
 
 namespace {
 
-// One work-group per head: thread i sums entries i, i + 256, ... of the
-// head's B*N per-query gradients in fp64, then a fixed-shape tree in LDS.
-__global__ __launch_bounds__(256) void gate_grad_per_head_kernel(int B, int H, int N, const float *dgate,
-                                                                 float *out) {
-    __shared__ double part[256];
+// One work-group per head: thread i sums entries t = i, i + 1024, ... of
+// every batch row of the head into four fp64 partial sums (a fixed order,
+// independent additions in flight), then a fixed-shape tree in LDS.
+constexpr int kGateRedThreads = 1024;
+
+__global__ __launch_bounds__(kGateRedThreads) void gate_grad_per_head_kernel(int B, int H, int N,
+                                                                              const float *dgate, float *out) {
+    __shared__ double part[kGateRedThreads];
     const int h = blockIdx.x;
-    const int64_t count = (int64_t)B * N;
-    double acc = 0.0;
-    for (int64_t i = threadIdx.x; i < count; i += 256) {
-        const int64_t b = i / N, t = i - b * N;
-        acc += (double)dgate[(b * H + h) * N + t];
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int b = 0; b < B; ++b) {
+        const float *row = dgate + ((int64_t)b * H + h) * N;
+        int64_t t = threadIdx.x;
+        for (; t + 3 * kGateRedThreads < N; t += 4 * kGateRedThreads) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) acc[u] += (double)row[t + u * kGateRedThreads];
+        }
+        // at most three entries remain for this thread
+#pragma unroll
+        for (int u = 0; u < 3; ++u)
+            if (t + u * kGateRedThreads < N) acc[u] += (double)row[t + u * kGateRedThreads];
     }
-    part[threadIdx.x] = acc;
+    part[threadIdx.x] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
     __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
+    for (int w = kGateRedThreads / 2; w > 0; w >>= 1) {
         if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
         __syncthreads();
     }
@@ -260,7 +270,8 @@ __global__ __launch_bounds__(256) void gate_grad_per_head_kernel(int B, int H, i
 
 hipError_t launch_gate_grad_per_head(int B, int H, int N, const float *dgate, float *out, hipStream_t stream) {
     if (H == 0) return hipSuccess;
-    return launch_kernel(gate_grad_per_head_kernel, dim3((unsigned)H), dim3(256), stream, B, H, N, dgate, out);
+    return launch_kernel(gate_grad_per_head_kernel, dim3((unsigned)H), dim3(kGateRedThreads), stream, B, H, N,
+                         dgate, out);
 }
 
 hipError_t launch_backward(const BwdParams &p, hipStream_t stream) {
