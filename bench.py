@@ -7,7 +7,8 @@ H=32, N=32768, D=128, k=512, pi=1024, bf16 q/k/v ~ N(0,1), per-head gate
 logits ~ U(-1,1).  One step = one pi_attn_forward over the whole sequence.
 Also timed in the same run: the KV-cached decode step (64 sequences, 32
 heads, 32768 cached rows, k=512, pi=1024, 1000 consecutive steps), the
-bidirectional forward on the same shape, the backward (pi_attn_backward,
+bidirectional forward on the same shape, one rank's share of the sequence
+sharded eight ways (pi_attn_forward_shard), the backward (pi_attn_backward,
 causal and bidirectional) on that shape with a seeded dL/dy, and the fp64
 CPU oracle on a bounded sample of the forward workload.
 
@@ -77,6 +78,7 @@ def parse():
     ap.add_argument("--no-backward", action="store_true")
     ap.add_argument("--no-bidirectional", action="store_true")
     ap.add_argument("--no-smallk", action="store_true")
+    ap.add_argument("--no-shard", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pmc-probe", action="store_true",
                     help="run 3 launches of each timed kernel (forward, bidirectional forward, backward "
@@ -101,6 +103,18 @@ def forward_algorithmic(cfg, causal=True):
     es = 2
     nbytes = 4 * cfg.B * cfg.H * cfg.N * cfg.D * es
     return keys, flops, nbytes
+
+
+def shard_algorithmic(cfg, s0, s1, lo):
+    """Algorithmic work of the causal forward of one sequence shard: queries
+    [s0, s1) against the k/v rows [lo, s1) held (the shard and its halo):
+    attended keys summed per query, FLOPs (QK + PV), bytes (q and out of the
+    shard, k and v of the rows held, each once)."""
+    k, pi = cfg.k, cfg.pi
+    keys = sum(min(t, k) + 1 + (1 if pi > k and t >= pi else 0) for t in range(s0, s1)) * cfg.B * cfg.H
+    es = 2
+    nbytes = cfg.B * cfg.H * cfg.D * es * (2 * (s1 - s0) + 2 * (s1 - lo))
+    return keys, 4 * cfg.D * keys, nbytes
 
 
 def smallk_algorithmic(cfg, causal=True, gated=True):
@@ -347,6 +361,11 @@ def main():
     if not args.no_smallk:
         smallk = bench_smallk(W, pa, torch, dev, stream, args.steps, args.warmup)
 
+    # ---- one rank's share of a sequence-sharded fwd32k ----------------------
+    shard = None
+    if not args.no_shard:
+        shard = bench_shard(cfg, W, pa, torch, dev, stream, args.steps, args.warmup)
+
     # ---- decode step --------------------------------------------------------
     decode = None
     if not args.no_decode:
@@ -439,6 +458,7 @@ def main():
         "device": device_info(torch, dev),
         "bidirectional": bidir,
         "smallk": smallk,
+        "sequence_shard": shard,
         "decode": decode,
         "backward": backward,
         "backward_bidirectional": backward_bidir,
@@ -495,6 +515,32 @@ def bench_smallk(W, pa, torch, dev, stream, steps, warmup):
     del q, k, v
     torch.cuda.empty_cache()
     return res
+
+
+def bench_shard(cfg, W, pa, torch, dev, stream, steps, warmup, nshard=8):
+    """The forward of one rank's share of the fwd32k sequence sharded
+    ``nshard`` ways: the last shard's queries and its k/v rows plus the pi
+    halo rows before it, held as contiguous tensors as a rank would hold
+    them."""
+    q, k, v, gate = W.forward_inputs(cfg, 0, dev)
+    n = cfg.N
+    s0 = n - n // nshard
+    lo = max(0, s0 - max(cfg.k, cfg.pi))
+    qs, ks, vs = (x[:, :, a:].contiguous() for x, a in ((q, s0), (k, lo), (v, lo)))
+    del q, k, v
+    out = torch.empty_like(qs)
+    ms, _, _ = time_launches(
+        torch, lambda: pa.pi_attn_forward_shard(qs, ks, vs, gate, cfg.k, cfg.pi, n, s0, lo, out=out),
+        steps, warmup, stream)
+    keys, flops, nbytes = shard_algorithmic(cfg, s0, n, lo)
+    rl, mf = roofline_of(flops, nbytes, ms / 1e3, "forward_bf16_kernel<128,false,false,false> (one shard)")
+    del qs, ks, vs, out
+    torch.cuda.empty_cache()
+    return {"workload": (f"fwd32k sequence-sharded {nshard} ways, one rank's share: queries [{s0}, {n}), "
+                         f"k/v rows [{lo}, {n}) (its own and the pi = {cfg.pi} halo rows), B1 H32 D128 k512"),
+            "steps": steps, "us_per_step": round(ms * 1e3, 2),
+            "query_positions_per_s": round(cfg.B * (n - s0) / (ms / 1e3), 1),
+            "attended_keys_per_s": round(keys / (ms / 1e3), 1), "roofline": rl, "roofline_mfma": mf}
 
 
 def bench_backward(cfg, W, pa, torch, dev, stream, steps, causal):

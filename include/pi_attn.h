@@ -227,6 +227,44 @@ int pi_attn_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D,
                      void *stream);
 
 /*
+ * pi_attn_forward_shard -- pi_attn_forward over one shard of a sequence:
+ * the queries at absolute positions [qpos0, qpos0 + nq) of a sequence of
+ * nseq positions, with the k/v rows held from absolute position kvpos0 on
+ * (the shard's own rows plus the halo before it, and for the bidirectional
+ * mode after it).  The working set of a query is that of the whole sequence
+ * (Sec. 3.2 eq. Nr, Sec. 3.4 eq. Npi: window and partners by absolute
+ * position), so the outputs equal the corresponding rows of pi_attn_forward
+ * over the whole sequence; this is the part of a sequence-sharded run that
+ * one GPU executes once its halo has arrived (the network term of the cost
+ * model, Sec. 3.5 eq. online_cost).  bf16 only.
+ *   dtype, B, H, D, k, pi, causal, scale, logit_clamp   as pi_attn_forward.
+ *   nseq, qpos0, nq   sequence length and the shard's queries; 0 <= qpos0,
+ *                qpos0 + nq <= nseq.
+ *   kvpos0, nkv  absolute position of k/v row 0 and the rows held:
+ *                kvpos0 <= min(window start of qpos0 rounded down to a
+ *                multiple of 32, max(0, qpos0 - pi) when pi > k), and
+ *                kvpos0 + nkv >= qpos0 + nq (causal) or
+ *                min(nseq, qpos0 + nq + max(k, pi)) (bidirectional; k when
+ *                pi <= k); kvpos0 + nkv <= nseq.
+ *   q            device [B][H][nq][D] through (sb, sh, sn).
+ *   kk, v        device [B][H][nkv][D] through (ksb, ksh, ksn).
+ *   gate         per head [H] or per query [B][H][nq] (query rows of the
+ *                shard) through (gsb, gsh, gsn).
+ *   out, lse     [B][H][nq][D] through (osb, osh, osn) and [B][H][nq].
+ * Results: rows equal to pi_attn_forward's for the same absolute positions
+ * up to rounding, and bit-identical when qpos0 is a multiple of 128 and
+ * kvpos0 a multiple of 32 (the same tiles in the same order).
+ * Errors: as pi_attn_forward; EUNSUPPORTED for float32; EINVAL for
+ * positions or k/v rows that do not satisfy the conditions above.
+ */
+int pi_attn_forward_shard(int32_t dtype, int32_t B, int32_t H, int32_t D, int32_t k, int32_t pi, int32_t causal,
+                          int32_t nseq, int32_t qpos0, int32_t nq, int32_t kvpos0, int32_t nkv, const void *q,
+                          int64_t sb, int64_t sh, int64_t sn, const void *kk, const void *v, int64_t ksb, int64_t ksh,
+                          int64_t ksn, const float *gate, int64_t gsb, int64_t gsh, int64_t gsn, float scale,
+                          float logit_clamp, void *out, int64_t osb, int64_t osh, int64_t osn, float *lse,
+                          void *stream);
+
+/*
  * pi_attn_gate_grad_per_head -- the gradient of a per-head gate logit g_h
  * shared by every b and t: out[h] = sum over b, t of dgate[b][h][t], the
  * per-query gradients pi_attn_backward writes (the gate enters each query's

@@ -22,12 +22,13 @@ import threading
 
 __all__ = ["pi_attn_index_set", "pi_attn_forward", "pi_attn_forward_gated", "pi_attn_backward",
            "pi_attn_decode_step", "pi_attn_ws_width",
-           "pi_attn_strerror", "library", "LIB_PATH", "EXPORTED_SYMBOLS", "PiAttnError"]
+           "pi_attn_forward_shard", "pi_attn_strerror", "library", "LIB_PATH", "EXPORTED_SYMBOLS",
+           "PiAttnError"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpi_attn.so")
 EXPORTED_SYMBOLS = ("pi_attn_strerror", "pi_attn_ws_width", "pi_attn_index_set",
                     "pi_attn_forward", "pi_attn_forward_gated", "pi_attn_decode_step", "pi_attn_backward",
-                    "pi_attn_gate_grad_per_head")
+                    "pi_attn_gate_grad_per_head", "pi_attn_forward_shard")
 
 PI_ATTN_F32, PI_ATTN_BF16 = 0, 1
 
@@ -71,6 +72,9 @@ def library() -> ctypes.CDLL:
             lib.pi_attn_backward.restype = ctypes.c_int
             lib.pi_attn_gate_grad_per_head.argtypes = [i32, i32, i32, vp, vp, vp]
             lib.pi_attn_gate_grad_per_head.restype = ctypes.c_int
+            lib.pi_attn_forward_shard.argtypes = ([i32] * 12 + [vp, i64, i64, i64, vp, vp, i64, i64, i64,
+                                                                vp, i64, i64, i64, f32, f32, vp, i64, i64, i64, vp, vp])
+            lib.pi_attn_forward_shard.restype = ctypes.c_int
             _lib = lib
     return _lib
 
@@ -185,6 +189,56 @@ def pi_attn_forward(q, k, v, gate, k_window: int, pi: int, scale: float | None =
         _stream_handle(stream, q.device))
     _check(st, "pi_attn_forward")
     return (out, lse) if (return_lse or lse is not None) else out
+
+
+def pi_attn_forward_shard(q, k, v, gate, k_window: int, pi: int, nseq: int, qpos0: int, kvpos0: int,
+                          scale: float | None = None, logit_clamp: float = 0.0, out=None, return_lse: bool = False,
+                          lse=None, stream=None, causal: bool = True):
+    """The forward over one shard of a sequence of ``nseq`` positions: q
+    [B, H, nq, D] holds the queries at absolute positions
+    [qpos0, qpos0 + nq), k and v [B, H, nkv, D] the rows from absolute
+    position ``kvpos0`` on (the shard plus its halo; see
+    pi_attn_forward_shard in include/pi_attn.h for the rows required).
+    bfloat16 only.  gate: [H] or [B, H, nq].  Returns out [B, H, nq, D]
+    (and lse [B, H, nq])."""
+    torch = _torch()
+    _require_cuda(q, k, v, gate, out, lse)
+    if q.dim() != 4 or k.dim() != 4 or k.shape != v.shape or k.stride() != v.stride():
+        raise ValueError("q [B, H, nq, D] and k, v [B, H, nkv, D] with k and v sharing strides")
+    B, H, nq, D = q.shape
+    if k.shape[0] != B or k.shape[1] != H or k.shape[3] != D:
+        raise ValueError("k and v must share q's B, H and D")
+    nkv = k.shape[2]
+    if q.dtype != torch.bfloat16 or k.dtype != q.dtype or v.dtype != q.dtype:
+        raise TypeError("q, k, v must be bfloat16")
+    if q.stride(3) != 1 or k.stride(3) != 1:
+        raise ValueError("the head dimension must be contiguous")
+    if gate.dtype != torch.float32:
+        raise TypeError("gate logits must be float32")
+    if tuple(gate.shape) == (H,):
+        g = gate.view(1, H, 1).expand(B, H, nq)
+    elif tuple(gate.shape) == (B, H, nq):
+        g = gate
+    else:
+        raise ValueError(f"gate must be [H] or [B, H, nq], got {tuple(gate.shape)}")
+    if out is None:
+        out = torch.empty_like(q, memory_format=torch.contiguous_format)
+    if out.shape != q.shape or out.dtype != q.dtype or out.stride(3) != 1:
+        raise ValueError("out must match q's shape and dtype with a contiguous last dimension")
+    if return_lse and lse is None:
+        lse = torch.empty((B, H, nq), dtype=torch.float32, device=q.device)
+    if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, nq)
+                            or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous float32 [B, H, nq] tensor")
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    st = library().pi_attn_forward_shard(
+        PI_ATTN_BF16, B, H, D, int(k_window), int(pi), int(bool(causal)), int(nseq), int(qpos0), nq, int(kvpos0),
+        nkv, _ptr(q), q.stride(0), q.stride(1), q.stride(2), _ptr(k), _ptr(v), k.stride(0), k.stride(1),
+        k.stride(2), _ptr(g), g.stride(0), g.stride(1), g.stride(2), float(scale), float(logit_clamp),
+        _ptr(out), out.stride(0), out.stride(1), out.stride(2), _ptr(lse), _stream_handle(stream, q.device))
+    _check(st, "pi_attn_forward_shard")
+    return (out, lse) if return_lse else out
 
 
 def pi_attn_forward_gated(q, k, v, u, w2, b2, k_window: int, pi: int, scale: float | None = None,

@@ -64,6 +64,8 @@ int check_sequence(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, in
     p.sb = sb; p.sh = sh; p.sn = sn;
     p.scale = scale;
     p.clamp = logit_clamp > 0.0f ? logit_clamp : 0.0f;
+    p.qpos0 = 0; p.kvpos0 = 0; p.kvend = N; p.nseq = N;
+    p.ksb = sb; p.ksh = sh; p.ksn = sn;
     return PI_ATTN_OK;
 }
 
@@ -203,6 +205,49 @@ int pi_attn_decode_step(int32_t dtype, int32_t S, int32_t H, int32_t D, int32_t 
     p.out = out; p.lse = lse;
     const hipStream_t st = (hipStream_t)stream;
     return from_hip(dtype == PI_ATTN_BF16 ? launch_decode_bf16(p, st) : launch_decode_f32(p, st));
+}
+
+int pi_attn_forward_shard(int32_t dtype, int32_t B, int32_t H, int32_t D, int32_t k, int32_t pi, int32_t causal,
+                          int32_t nseq, int32_t qpos0, int32_t nq, int32_t kvpos0, int32_t nkv, const void *q,
+                          int64_t sb, int64_t sh, int64_t sn, const void *kk, const void *v, int64_t ksb, int64_t ksh,
+                          int64_t ksn, const float *gate, int64_t gsb, int64_t gsh, int64_t gsn, float scale,
+                          float logit_clamp, void *out, int64_t osb, int64_t osh, int64_t osn, float *lse,
+                          void *stream) {
+    if (dtype != PI_ATTN_BF16) return PI_ATTN_EUNSUPPORTED;
+    if (nseq < 0 || qpos0 < 0 || nq < 0 || kvpos0 < 0 || nkv < 0) return PI_ATTN_EINVAL;
+    if ((int64_t)qpos0 + nq > nseq || (int64_t)kvpos0 + nkv > nseq) return PI_ATTN_EINVAL;
+    if (B < 0 || H < 0 || k < 0 || pi < 0) return PI_ATTN_EINVAL;
+    if ((int64_t)B * H * nkv >= kMaxRows) return PI_ATTN_EINVAL;
+    // the query checks of a whole-sequence forward over the nq query rows
+    // (the k/v pointers are checked against the k/v strides below)
+    FwdParams p{};
+    bool empty;
+    const int status = check_sequence(dtype, B, H, nq, D, k, pi, causal, q, q, q, sb, sh, sn, scale, logit_clamp, out,
+                                      osb, osh, osn, p, empty);
+    if (status != PI_ATTN_OK || empty) return status;
+    const int es = 2;
+    if (!kk || !v || !aligned16(kk) || !aligned16(v)) return PI_ATTN_EINVAL;
+    if (!stride16(ksb, es) || !stride16(ksh, es) || !stride16(ksn, es)) return PI_ATTN_EINVAL;
+    if (!tile_span_ok(k, nseq, causal != 0, ksn, es)) return PI_ATTN_EUNSUPPORTED;
+    // the k/v rows held must cover every row the shard's tiles stage or read:
+    // from the 32-aligned window start of its first query (and the partner
+    // t - pi of its first query) to its last query (causal) or k and pi rows
+    // past it (bidirectional), within the sequence
+    const bool par = pi > k;
+    int64_t lo = window_lo(qpos0, k) & ~31;
+    if (par) lo = std::min<int64_t>(lo, std::max(0, qpos0 - pi));
+    const int64_t qend = (int64_t)qpos0 + nq;
+    const int64_t hi = causal ? qend : std::min<int64_t>(nseq, qend + (par ? std::max(k, pi) : k));
+    if (kvpos0 > lo || (int64_t)kvpos0 + nkv < hi) return PI_ATTN_EINVAL;
+    if (!gate || !aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
+    if (lse && !aligned4(lse)) return PI_ATTN_EINVAL;
+    p.k_ptr = kk; p.v = v;
+    p.ksb = ksb; p.ksh = ksh; p.ksn = ksn;
+    p.qpos0 = qpos0; p.kvpos0 = kvpos0; p.kvend = kvpos0 + nkv; p.nseq = nseq;
+    p.gate = gate; p.gsb = gsb; p.gsh = gsh; p.gsn = gsn;
+    p.out = out; p.osb = osb; p.osh = osh; p.osn = osn;
+    p.lse = lse;
+    return from_hip(launch_forward_bf16(p, (hipStream_t)stream));
 }
 
 int pi_attn_gate_grad_per_head(int32_t B, int32_t H, int32_t N, const float *dgate, float *out, void *stream) {

@@ -245,32 +245,35 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
     const int lane = __lane_id();
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 5, c = lane & 31;
-    const int N = p.N, kw = p.k, pi = p.pi;
-    const int t0 = qt * BM;
+    const int kw = p.k, pi = p.pi;
+    // absolute positions: queries [qpos0, NQ), keys and partners below NS
+    const int NQ = p.qpos0 + p.N, NS = p.nseq;
+    const int t0 = p.qpos0 + qt * BM;
     const int q0 = t0 + 32 * w;   // first query of this wavefront
     const int t = q0 + c;         // this lane's query
-    const bool t_ok = t < N;
+    const bool t_ok = t < NQ;
 
-    const int64_t base = b * p.sb + h * p.sh;
-    const __bf16 *qp = (const __bf16 *)p.q + base;
-    const __bf16 *kp = (const __bf16 *)p.k_ptr + base;
-    const __bf16 *vp = (const __bf16 *)p.v + base;
-    const int64_t sn = p.sn;
+    const int64_t sn = p.sn, ksn = p.ksn;
+    // row pointers indexed by absolute position (only rows held are read)
+    const __bf16 *qp = (const __bf16 *)p.q + b * p.sb + h * p.sh - (int64_t)p.qpos0 * sn;
+    const int64_t kvbase = b * p.ksb + h * p.ksh - (int64_t)p.kvpos0 * ksn;
+    const __bf16 *kp = (const __bf16 *)p.k_ptr + kvbase;
+    const __bf16 *vp = (const __bf16 *)p.v + kvbase;
 
     // Window tiles: rows [kb0, kend) in 64-row steps, blocks aligned to 32.
     const int kb0 = window_lo(t0, kw) & ~31;
-    const int kend = BIDIR ? (int)min((int64_t)t0 + BM + kw, (int64_t)N) : min(t0 + BM, N);
+    const int kend = min(BIDIR ? (int)min((int64_t)t0 + BM + kw, (int64_t)NS) : min(t0 + BM, NQ), p.kvend);
     const int ntiles = (kend - kb0 + TK - 1) / TK;
     // ---- prologue: every load is issued before any is waited for ----------
     // (the first tile, the query fragments, the gate logit and the partner
     // key/value rows), so the prologue costs one memory round trip.
     // Buffer descriptors over rows [kb0, kend) of this head's keys and values
     // (word 3 is the gfx9 raw-buffer format: 32-bit data, range checked).
-    const int rowb = (int)(2 * sn);
+    const int rowb = (int)(2 * ksn);
     const __amdgpu_buffer_rsrc_t rk =
-        __builtin_amdgcn_make_buffer_rsrc((void *)(kp + (int64_t)kb0 * sn), (short)0, (kend - kb0) * rowb, 0x00020000);
+        __builtin_amdgcn_make_buffer_rsrc((void *)(kp + (int64_t)kb0 * ksn), (short)0, (kend - kb0) * rowb, 0x00020000);
     const __amdgpu_buffer_rsrc_t rv =
-        __builtin_amdgcn_make_buffer_rsrc((void *)(vp + (int64_t)kb0 * sn), (short)0, (kend - kb0) * rowb, 0x00020000);
+        __builtin_amdgcn_make_buffer_rsrc((void *)(vp + (int64_t)kb0 * ksn), (short)0, (kend - kb0) * rowb, 0x00020000);
     Stage<D> st;
     Stage<D> st0[BPT];
 #pragma unroll
@@ -279,11 +282,11 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
     // Loads use a clamped, always-readable row; lanes without a query or a
     // partner zero the data afterwards.
     W ws;
-    const int tq = t_ok ? t : 0;
+    const int tq = t_ok ? t : p.qpos0;
     bf16x8 qraw[W::KS];
 #pragma unroll
     for (int s = 0; s < W::KS; ++s) qraw[s] = *reinterpret_cast<const bf16x8 *>(qp + tq * sn + 16 * s + 8 * g);
-    const float gl = p.gate[b * p.gsb + h * p.gsh + tq * p.gsn];
+    const float gl = p.gate[b * p.gsb + h * p.gsh + (tq - p.qpos0) * p.gsn];
 
     // Partner rows: A-operand row c of the wavefront is row q0 + c - pi, the
     // partner of query q0 + c; the accumulator seed is that row's value, of
@@ -291,32 +294,32 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
     const int prow = t - pi;
     const bool has_p = partner_enabled(kw, pi) && prow >= 0 && t_ok;   // depends on c only
     const bool any_p = __builtin_amdgcn_ballot_w64(has_p) != 0;       // wave-uniform
-    const int prc = has_p ? prow : 0;
+    const int prc = has_p ? prow : p.kvpos0;
     bf16x8 kpf[W::KS];
     uint2 vraw[W::DB][4];
     if (any_p) {
 #pragma unroll
-        for (int s = 0; s < W::KS; ++s) kpf[s] = *reinterpret_cast<const bf16x8 *>(kp + prc * sn + 16 * s + 8 * g);
+        for (int s = 0; s < W::KS; ++s) kpf[s] = *reinterpret_cast<const bf16x8 *>(kp + prc * ksn + 16 * s + 8 * g);
 #pragma unroll
         for (int db = 0; db < W::DB; ++db)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                vraw[db][i] = *reinterpret_cast<const uint2 *>(vp + prc * sn + 32 * db + 8 * i + 4 * g);
+                vraw[db][i] = *reinterpret_cast<const uint2 *>(vp + prc * ksn + 32 * db + 8 * i + 4 * g);
     }
     // Bidirectional: the second partner t + pi, loaded the same way.
-    const bool has_f = BIDIR && t_ok && partner_fwd_of(t, kw, pi, N) >= 0;
+    const bool has_f = BIDIR && t_ok && partner_fwd_of(t, kw, pi, NS) >= 0;
     const bool any_f = BIDIR && __builtin_amdgcn_ballot_w64(has_f) != 0;
-    const int frc = has_f ? t + pi : 0;
+    const int frc = has_f ? t + pi : p.kvpos0;
     bf16x8 kff[W::KS];
     uint2 vfraw[W::DB][4];
     if (any_f) {
 #pragma unroll
-        for (int s = 0; s < W::KS; ++s) kff[s] = *reinterpret_cast<const bf16x8 *>(kp + frc * sn + 16 * s + 8 * g);
+        for (int s = 0; s < W::KS; ++s) kff[s] = *reinterpret_cast<const bf16x8 *>(kp + frc * ksn + 16 * s + 8 * g);
 #pragma unroll
         for (int db = 0; db < W::DB; ++db)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                vfraw[db][i] = *reinterpret_cast<const uint2 *>(vp + frc * sn + 32 * db + 8 * i + 4 * g);
+                vfraw[db][i] = *reinterpret_cast<const uint2 *>(vp + frc * ksn + 32 * db + 8 * i + 4 * g);
     }
 #pragma unroll
     for (int s = 0; s < W::KS; ++s) ws.qf[s] = t_ok ? qraw[s] : bf16x8{};
@@ -383,11 +386,11 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
     // keys [j0, j0 + 32).
     auto block = [&](const unsigned char *kt, const unsigned char *vt, int j0, int blk) {
         // Wave-uniform: does the block meet the band, is it wholly inside it?
-        const bool act = BIDIR ? j0 < kend && q0 < N && j0 - (q0 + 31) <= kw && j0 + 31 >= q0 - kw
-                               : j0 < kend && q0 < N && j0 <= q0 + 31 && j0 + 31 >= q0 - kw;
+        const bool act = BIDIR ? j0 < kend && q0 < NQ && j0 - (q0 + 31) <= kw && j0 + 31 >= q0 - kw
+                               : j0 < kend && q0 < NQ && j0 <= q0 + 31 && j0 + 31 >= q0 - kw;
         if (!act) return;
-        const bool edge = BIDIR ? !(j0 + 31 - q0 <= kw && q0 + 31 - j0 <= kw) || q0 + 31 >= N || j0 + 31 >= N
-                                : !(j0 + 31 <= q0 && j0 >= q0 + 31 - kw) || q0 + 31 >= N;
+        const bool edge = BIDIR ? !(j0 + 31 - q0 <= kw && q0 + 31 - j0 <= kw) || q0 + 31 >= NQ || j0 + 31 >= NS
+                                : !(j0 + 31 <= q0 && j0 >= q0 + 31 - kw) || q0 + 31 >= NQ;
 
         // Fragment reads: the K rows (A operand of the scores) are issued
         // together ahead of the score MFMAs; the V^T reads (A operand of
@@ -424,7 +427,7 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
             }
         }
         bf16x8 pb[2];
-        softmax_block<D, CLAMP, BIDIR, LSE>(ws, sc, edge, j0, t, kw, N, t_ok, c2, p.scale, fb.local, p.clamp, g, pb);
+        softmax_block<D, CLAMP, BIDIR, LSE>(ws, sc, edge, j0, t, kw, NS, t_ok, c2, p.scale, fb.local, p.clamp, g, pb);
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc) {
 #pragma unroll
@@ -475,7 +478,7 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
     const float lb_tot = ws.lb + other_half(ws.lb);
     if (t_ok) {
         const float inv = 1.0f / lb_tot;
-        __bf16 *op = (__bf16 *)p.out + b * p.osb + h * p.osh + t * p.osn;
+        __bf16 *op = (__bf16 *)p.out + b * p.osb + h * p.osh + (int64_t)(t - p.qpos0) * p.osn;
 #pragma unroll
         for (int db = 0; db < W::DB; ++db) {
 #pragma unroll
@@ -488,7 +491,7 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
         }
         if constexpr (LSE) {
             const float l_tot = ws.l + other_half(ws.l);
-            if (g == 0) p.lse[bh * N + t] = (ws.m + __log2f(l_tot)) * kLn2 + fb.lse_shift;
+            if (g == 0) p.lse[bh * p.N + (t - p.qpos0)] = (ws.m + __log2f(l_tot)) * kLn2 + fb.lse_shift;
         }
     }
 }

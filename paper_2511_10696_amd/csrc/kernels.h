@@ -30,6 +30,11 @@ struct FwdParams {
     void *out;
     int64_t osb, osh, osn;
     float *lse;                     // [B][H][N] or nullptr
+    // Sequence shard (the banded bf16 forward only): q/out/lse/gate row i is
+    // absolute position qpos0 + i, k/v row i is kvpos0 + i, k/v rows end at
+    // kvend, the sequence has nseq positions.  A whole sequence: 0, 0, N, N.
+    int qpos0, kvpos0, kvend, nseq;
+    int64_t ksb, ksh, ksn;          // element strides of k and v (a whole sequence: sb, sh, sn)
 };
 
 struct DecodeParams {

@@ -157,6 +157,40 @@ def test_backward_empty_is_noop(lib, kw):
     assert bwd(lib, **kw) == 0
 
 
+def shard(lib, **kw):
+    # a valid-looking causal shard: queries [1024, 1536) of 4096, k/v from 512
+    a = dict(dtype=1, B=1, H=2, D=64, k=128, pi=512, causal=1, nseq=4096, qpos0=1024, nq=512, kvpos0=512, nkv=1024,
+             q=16, sb=65536, sh=32768, sn=64, kk=16, v=16, ksb=131072, ksh=65536, ksn=64, gate=16, gsb=0, gsh=1,
+             gsn=0, scale=0.125, clamp=0.0, out=16, osb=65536, osh=32768, osn=64, lse=None, stream=None)
+    a.update(kw)
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.pi_attn_forward_shard(a["dtype"], a["B"], a["H"], a["D"], a["k"], a["pi"], a["causal"], a["nseq"],
+                                     a["qpos0"], a["nq"], a["kvpos0"], a["nkv"], vp(a["q"]), a["sb"], a["sh"],
+                                     a["sn"], vp(a["kk"]), vp(a["v"]), a["ksb"], a["ksh"], a["ksn"], vp(a["gate"]),
+                                     a["gsb"], a["gsh"], a["gsn"], a["scale"], a["clamp"], vp(a["out"]), a["osb"],
+                                     a["osh"], a["osn"], vp(a["lse"]), vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=0), EUNSUP), (dict(D=32), EUNSUP), (dict(nseq=-1), EINVAL), (dict(qpos0=-1), EINVAL),
+    (dict(nq=4000), EINVAL),                       # queries past the sequence
+    (dict(kvpos0=544), EINVAL),                    # halo short of the partner t - pi of the first query
+    (dict(k=600, pi=0, kvpos0=448), EINVAL),       # halo short of the 32-aligned window start (424 -> 416)
+    (dict(nkv=1023), EINVAL),                      # k/v rows end before the last query
+    (dict(causal=0, nkv=1535), EINVAL),            # bidirectional: k/v must reach the last query + pi (2048)
+    (dict(kvpos0=3500, nkv=1000), EINVAL),         # k/v rows past the sequence
+    (dict(kk=None), EINVAL), (dict(v=8), EINVAL), (dict(ksn=4), EINVAL), (dict(gate=None), EINVAL),
+    (dict(q=None), EINVAL), (dict(out=8), EINVAL), (dict(scale=0.0), EINVAL), (dict(lse=2), EINVAL),
+])
+def test_forward_shard_rejects(lib, kw, code):
+    assert shard(lib, **kw) == code
+
+
+@pytest.mark.parametrize("kw", [dict(nq=0), dict(B=0), dict(H=0, q=None, kk=None)])
+def test_forward_shard_empty_is_noop(lib, kw):
+    assert shard(lib, **kw) == 0
+
+
 def ggh(lib, **kw):
     a = dict(B=2, H=3, N=100, dg=16, out=16, stream=None)
     a.update(kw)

@@ -38,3 +38,15 @@ def test_bidirectional_attended_keys_match_the_index_sets():
         idx = oracle.index_set(cfg.N, cfg.k, cfg.pi, causal=False)
         assert keys == int((idx >= 0).sum()) * cfg.B * cfg.H
         assert flops == 4 * cfg.D * keys
+
+
+def test_shard_accounting():
+    """One rank's share of fwd32k sharded eight ways: every query of the last
+    shard attends k + 1 window keys and its partner; the bytes are its q and
+    out plus the k/v rows held (shard and pi halo)."""
+    cfg = W.FORWARD["fwd32k"]
+    s0, lo = cfg.N - cfg.N // 8, cfg.N - cfg.N // 8 - cfg.pi
+    keys, flops, nbytes = bench.shard_algorithmic(cfg, s0, cfg.N, lo)
+    assert keys == (cfg.N - s0) * (cfg.k + 2) * cfg.B * cfg.H
+    assert flops == 4 * cfg.D * keys
+    assert nbytes == cfg.B * cfg.H * cfg.D * 2 * (2 * (cfg.N - s0) + 2 * (cfg.N - lo))
