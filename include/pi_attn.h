@@ -265,6 +265,54 @@ int pi_attn_forward_shard(int32_t dtype, int32_t B, int32_t H, int32_t D, int32_
                           void *stream);
 
 /*
+ * pi_attn_backward_shard_q, pi_attn_backward_shard_kv -- pi_attn_backward
+ * split into its two passes over one shard of a sequence of nseq positions
+ * (the gradients of Sec. 3.5 eq. jac and eqs. ddelta_da, dalpha_da, every
+ * working set taken by absolute position as in pi_attn_forward_shard).  A
+ * sequence-sharded run calls the query pass on its queries, exchanges the
+ * halo of query rows the key pass needs (q, dL/dy, lse, the row terms the
+ * neighbour's query pass wrote, and per-query gates), then calls the key
+ * pass on its keys.  bf16 only; the banded passes for every k.
+ *
+ * pi_attn_backward_shard_q: queries [qpos0, qpos0 + nq) with the k/v rows
+ * held from kvpos0 (nkv rows; the coverage pi_attn_forward_shard requires).
+ *   q [B][H][nq][D] (sb, sh, sn); kk, v [B][H][nkv][D] (ksb, ksh, ksn);
+ *   gate [H] or [B][H][nq]; lse [B][H][nq] (the forward's); out and dout
+ *   [B][H][nq][D] (osb, osh, osn); writes dq [B][H][nq][D], dgate and the
+ *   row terms [B][H][nq], all contiguous float32.
+ *
+ * pi_attn_backward_shard_kv: keys [kpos0, kpos0 + nk) (kk, v hold exactly
+ * these rows, [B][H][nk][D] through ksb, ksh, ksn) with the query rows held
+ * from qpos0 (nqh rows): q and dout [B][H][nqh][D] through (sb, sh, sn) and
+ * (osb, osh, osn), gate [H] or [B][H][nqh], lse and row terms [B][H][nqh]
+ * contiguous.  The query rows must cover every query whose working set
+ * holds one of the keys: qpos0 <= kpos0 (causal) or
+ * max(0, kpos0 - max(k, pi)) (bidirectional; k when pi <= k), and
+ * qpos0 + nqh >= min(nseq, kpos0 + nk + max(k, pi)) (k when pi <= k).
+ * Writes dk, dv [B][H][nk][D] contiguous float32.
+ *
+ * Results: the rows of pi_attn_backward's gradients (with k > 16, whose
+ * whole-sequence call also takes the banded passes) for the same absolute
+ * positions, bit-identical when qpos0 and kpos0 are multiples of 128.
+ * Errors: as pi_attn_backward; EUNSUPPORTED for float32; EINVAL for
+ * positions or rows held that do not satisfy the conditions above.
+ */
+int pi_attn_backward_shard_q(int32_t dtype, int32_t B, int32_t H, int32_t D, int32_t k, int32_t pi,
+                             int32_t causal, int32_t nseq, int32_t qpos0, int32_t nq, int32_t kvpos0, int32_t nkv,
+                             const void *q, int64_t sb, int64_t sh, int64_t sn, const void *kk, const void *v,
+                             int64_t ksb, int64_t ksh, int64_t ksn, const float *gate, int64_t gsb, int64_t gsh,
+                             int64_t gsn, float scale, float logit_clamp, const float *lse, const void *out,
+                             const void *dout, int64_t osb, int64_t osh, int64_t osn, float *dq, float *dgate,
+                             float *rowterm, void *stream);
+int pi_attn_backward_shard_kv(int32_t dtype, int32_t B, int32_t H, int32_t D, int32_t k, int32_t pi,
+                              int32_t causal, int32_t nseq, int32_t kpos0, int32_t nk, int32_t qpos0, int32_t nqh,
+                              const void *q, int64_t sb, int64_t sh, int64_t sn, const void *kk, const void *v,
+                              int64_t ksb, int64_t ksh, int64_t ksn, const float *gate, int64_t gsb, int64_t gsh,
+                              int64_t gsn, float scale, float logit_clamp, const float *lse, const float *rowterm,
+                              const void *dout, int64_t osb, int64_t osh, int64_t osn, float *dk, float *dv,
+                              void *stream);
+
+/*
  * pi_attn_gate_grad_per_head -- the gradient of a per-head gate logit g_h
  * shared by every b and t: out[h] = sum over b, t of dgate[b][h][t], the
  * per-query gradients pi_attn_backward writes (the gate enters each query's

@@ -22,13 +22,14 @@ import threading
 
 __all__ = ["pi_attn_index_set", "pi_attn_forward", "pi_attn_forward_gated", "pi_attn_backward",
            "pi_attn_decode_step", "pi_attn_ws_width",
-           "pi_attn_forward_shard", "pi_attn_strerror", "library", "LIB_PATH", "EXPORTED_SYMBOLS",
-           "PiAttnError"]
+           "pi_attn_forward_shard", "pi_attn_backward_shard_q", "pi_attn_backward_shard_kv",
+           "pi_attn_strerror", "library", "LIB_PATH", "EXPORTED_SYMBOLS", "PiAttnError"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpi_attn.so")
 EXPORTED_SYMBOLS = ("pi_attn_strerror", "pi_attn_ws_width", "pi_attn_index_set",
                     "pi_attn_forward", "pi_attn_forward_gated", "pi_attn_decode_step", "pi_attn_backward",
-                    "pi_attn_gate_grad_per_head", "pi_attn_forward_shard")
+                    "pi_attn_gate_grad_per_head", "pi_attn_forward_shard", "pi_attn_backward_shard_q",
+                    "pi_attn_backward_shard_kv")
 
 PI_ATTN_F32, PI_ATTN_BF16 = 0, 1
 
@@ -75,6 +76,14 @@ def library() -> ctypes.CDLL:
             lib.pi_attn_forward_shard.argtypes = ([i32] * 12 + [vp, i64, i64, i64, vp, vp, i64, i64, i64,
                                                                 vp, i64, i64, i64, f32, f32, vp, i64, i64, i64, vp, vp])
             lib.pi_attn_forward_shard.restype = ctypes.c_int
+            lib.pi_attn_backward_shard_q.argtypes = ([i32] * 12 + [vp, i64, i64, i64, vp, vp, i64, i64, i64,
+                                                                   vp, i64, i64, i64, f32, f32, vp, vp, vp, i64, i64,
+                                                                   i64, vp, vp, vp, vp])
+            lib.pi_attn_backward_shard_q.restype = ctypes.c_int
+            lib.pi_attn_backward_shard_kv.argtypes = ([i32] * 12 + [vp, i64, i64, i64, vp, vp, i64, i64, i64,
+                                                                    vp, i64, i64, i64, f32, f32, vp, vp, vp, i64, i64,
+                                                                    i64, vp, vp, vp])
+            lib.pi_attn_backward_shard_kv.restype = ctypes.c_int
             _lib = lib
     return _lib
 
@@ -239,6 +248,83 @@ def pi_attn_forward_shard(q, k, v, gate, k_window: int, pi: int, nseq: int, qpos
         _ptr(out), out.stride(0), out.stride(1), out.stride(2), _ptr(lse), _stream_handle(stream, q.device))
     _check(st, "pi_attn_forward_shard")
     return (out, lse) if return_lse else out
+
+
+def _shard_gate(torch, gate, B, H, n):
+    if gate.dtype != torch.float32:
+        raise TypeError("gate logits must be float32")
+    if tuple(gate.shape) == (H,):
+        return gate.view(1, H, 1).expand(B, H, n)
+    if tuple(gate.shape) == (B, H, n):
+        return gate
+    raise ValueError(f"gate must be [H] or [B, H, {n}], got {tuple(gate.shape)}")
+
+
+def pi_attn_backward_shard_q(q, k, v, gate, k_window: int, pi: int, nseq: int, qpos0: int, kvpos0: int, out, lse,
+                             dout, scale: float | None = None, logit_clamp: float = 0.0, stream=None,
+                             causal: bool = True):
+    """Query pass of the backward over one shard: q, out, dout [B, H, nq, D]
+    (bfloat16) at absolute positions [qpos0, qpos0 + nq), k and v
+    [B, H, nkv, D] from absolute position ``kvpos0`` (the forward shard's
+    rows), lse [B, H, nq].  Returns float32 dq [B, H, nq, D], the per-query
+    gate gradient and the row terms [B, H, nq]."""
+    torch = _torch()
+    _require_cuda(q, k, v, gate, out, dout, lse)
+    B, H, nq, D = q.shape
+    if out.shape != q.shape or dout.shape != q.shape or out.stride() != dout.stride():
+        raise ValueError("out and dout must match q's shape and share strides")
+    if k.shape != v.shape or k.stride() != v.stride() or k.shape[:2] != q.shape[:2] or k.shape[3] != D:
+        raise ValueError("k, v [B, H, nkv, D] with shared strides")
+    g = _shard_gate(torch, gate, B, H, nq)
+    f32 = dict(dtype=torch.float32, device=q.device)
+    dq = torch.empty((B, H, nq, D), **f32)
+    dg = torch.empty((B, H, nq), **f32)
+    rt = torch.empty((B, H, nq), **f32)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    st = library().pi_attn_backward_shard_q(
+        _dtype_code(q.dtype), B, H, D, int(k_window), int(pi), int(bool(causal)), int(nseq), int(qpos0), nq,
+        int(kvpos0), k.shape[2], _ptr(q), q.stride(0), q.stride(1), q.stride(2), _ptr(k), _ptr(v), k.stride(0),
+        k.stride(1), k.stride(2), _ptr(g), g.stride(0), g.stride(1), g.stride(2), float(scale), float(logit_clamp),
+        _ptr(lse), _ptr(out), _ptr(dout), dout.stride(0), dout.stride(1), dout.stride(2), _ptr(dq), _ptr(dg),
+        _ptr(rt), _stream_handle(stream, q.device))
+    _check(st, "pi_attn_backward_shard_q")
+    return dq, dg, rt
+
+
+def pi_attn_backward_shard_kv(q, k, v, gate, k_window: int, pi: int, nseq: int, kpos0: int, qpos0: int, lse, rowterm,
+                              dout, scale: float | None = None, logit_clamp: float = 0.0, stream=None,
+                              causal: bool = True):
+    """Key pass of the backward over one shard: k, v [B, H, nk, D] (bfloat16)
+    the keys at absolute positions [kpos0, kpos0 + nk); q, dout
+    [B, H, nqh, D], lse, rowterm [B, H, nqh] (contiguous float32) and gate
+    the query rows held from absolute position ``qpos0`` (the shard's own and
+    the halo rows).  Returns float32 dk, dv [B, H, nk, D]."""
+    torch = _torch()
+    _require_cuda(q, k, v, gate, dout, lse, rowterm)
+    B, H, nk, D = k.shape
+    if v.shape != k.shape or v.stride() != k.stride():
+        raise ValueError("k and v must share shape and strides")
+    if q.dim() != 4 or q.shape[:2] != k.shape[:2] or q.shape[3] != D or dout.shape != q.shape:
+        raise ValueError("q, dout [B, H, nqh, D]")
+    nqh = q.shape[2]
+    for name, x in (("lse", lse), ("rowterm", rowterm)):
+        if x.dtype != torch.float32 or tuple(x.shape) != (B, H, nqh) or not x.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous float32 [B, H, nqh] tensor")
+    g = _shard_gate(torch, gate, B, H, nqh)
+    f32 = dict(dtype=torch.float32, device=k.device)
+    dk = torch.empty((B, H, nk, D), **f32)
+    dv = torch.empty((B, H, nk, D), **f32)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    st = library().pi_attn_backward_shard_kv(
+        _dtype_code(k.dtype), B, H, D, int(k_window), int(pi), int(bool(causal)), int(nseq), int(kpos0), nk,
+        int(qpos0), nqh, _ptr(q), q.stride(0), q.stride(1), q.stride(2), _ptr(k), _ptr(v), k.stride(0),
+        k.stride(1), k.stride(2), _ptr(g), g.stride(0), g.stride(1), g.stride(2), float(scale), float(logit_clamp),
+        _ptr(lse), _ptr(rowterm), _ptr(dout), dout.stride(0), dout.stride(1), dout.stride(2), _ptr(dk), _ptr(dv),
+        _stream_handle(stream, k.device))
+    _check(st, "pi_attn_backward_shard_kv")
+    return dk, dv
 
 
 def pi_attn_forward_gated(q, k, v, u, w2, b2, k_window: int, pi: int, scale: float | None = None,

@@ -64,9 +64,30 @@ int check_sequence(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, in
     p.sb = sb; p.sh = sh; p.sn = sn;
     p.scale = scale;
     p.clamp = logit_clamp > 0.0f ? logit_clamp : 0.0f;
-    p.qpos0 = 0; p.kvpos0 = 0; p.kvend = N; p.nseq = N;
+    p.qpos0 = 0; p.kvpos0 = 0; p.kvend = N; p.nseq = N; p.qend = N;
     p.ksb = sb; p.ksh = sh; p.ksn = sn;
     return PI_ATTN_OK;
+}
+
+// Shard of a sequence of nseq positions: the queries [qpos0, qpos0 + nq)
+// and k/v rows held from kvpos0 (nkv of them).  True when the rows held
+// cover everything the query tiles stage or read: from the 32-aligned
+// window start of the first query (and its partner t - pi) to the last query
+// (causal) or max(k, pi) rows past it (bidirectional), within the sequence.
+bool shard_kv_covered(int32_t k, int32_t pi, bool causal, int32_t nseq, int32_t qpos0, int32_t nq, int32_t kvpos0,
+                      int32_t nkv) {
+    const bool par = pi > k;
+    int64_t lo = window_lo(qpos0, k) & ~31;
+    if (par) lo = std::min<int64_t>(lo, std::max(0, qpos0 - pi));
+    const int64_t qend = (int64_t)qpos0 + nq;
+    const int64_t hi = causal ? qend : std::min<int64_t>(nseq, qend + (par ? std::max(k, pi) : k));
+    return kvpos0 <= lo && (int64_t)kvpos0 + nkv >= hi;
+}
+
+// The positions of a shard call: non-negative and inside the sequence.
+bool shard_positions_ok(int32_t nseq, int32_t p0, int32_t n0, int32_t p1, int32_t n1) {
+    if (nseq < 0 || p0 < 0 || n0 < 0 || p1 < 0 || n1 < 0) return false;
+    return (int64_t)p0 + n0 <= nseq && (int64_t)p1 + n1 <= nseq;
 }
 
 }  // namespace
@@ -214,8 +235,7 @@ int pi_attn_forward_shard(int32_t dtype, int32_t B, int32_t H, int32_t D, int32_
                           float logit_clamp, void *out, int64_t osb, int64_t osh, int64_t osn, float *lse,
                           void *stream) {
     if (dtype != PI_ATTN_BF16) return PI_ATTN_EUNSUPPORTED;
-    if (nseq < 0 || qpos0 < 0 || nq < 0 || kvpos0 < 0 || nkv < 0) return PI_ATTN_EINVAL;
-    if ((int64_t)qpos0 + nq > nseq || (int64_t)kvpos0 + nkv > nseq) return PI_ATTN_EINVAL;
+    if (!shard_positions_ok(nseq, qpos0, nq, kvpos0, nkv)) return PI_ATTN_EINVAL;
     if (B < 0 || H < 0 || k < 0 || pi < 0) return PI_ATTN_EINVAL;
     if ((int64_t)B * H * nkv >= kMaxRows) return PI_ATTN_EINVAL;
     // the query checks of a whole-sequence forward over the nq query rows
@@ -229,16 +249,7 @@ int pi_attn_forward_shard(int32_t dtype, int32_t B, int32_t H, int32_t D, int32_
     if (!kk || !v || !aligned16(kk) || !aligned16(v)) return PI_ATTN_EINVAL;
     if (!stride16(ksb, es) || !stride16(ksh, es) || !stride16(ksn, es)) return PI_ATTN_EINVAL;
     if (!tile_span_ok(k, nseq, causal != 0, ksn, es)) return PI_ATTN_EUNSUPPORTED;
-    // the k/v rows held must cover every row the shard's tiles stage or read:
-    // from the 32-aligned window start of its first query (and the partner
-    // t - pi of its first query) to its last query (causal) or k and pi rows
-    // past it (bidirectional), within the sequence
-    const bool par = pi > k;
-    int64_t lo = window_lo(qpos0, k) & ~31;
-    if (par) lo = std::min<int64_t>(lo, std::max(0, qpos0 - pi));
-    const int64_t qend = (int64_t)qpos0 + nq;
-    const int64_t hi = causal ? qend : std::min<int64_t>(nseq, qend + (par ? std::max(k, pi) : k));
-    if (kvpos0 > lo || (int64_t)kvpos0 + nkv < hi) return PI_ATTN_EINVAL;
+    if (!shard_kv_covered(k, pi, causal != 0, nseq, qpos0, nq, kvpos0, nkv)) return PI_ATTN_EINVAL;
     if (!gate || !aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
     if (lse && !aligned4(lse)) return PI_ATTN_EINVAL;
     p.k_ptr = kk; p.v = v;
@@ -248,6 +259,87 @@ int pi_attn_forward_shard(int32_t dtype, int32_t B, int32_t H, int32_t D, int32_
     p.out = out; p.osb = osb; p.osh = osh; p.osn = osn;
     p.lse = lse;
     return from_hip(launch_forward_bf16(p, (hipStream_t)stream));
+}
+
+int pi_attn_backward_shard_q(int32_t dtype, int32_t B, int32_t H, int32_t D, int32_t k, int32_t pi,
+                             int32_t causal, int32_t nseq, int32_t qpos0, int32_t nq, int32_t kvpos0, int32_t nkv,
+                             const void *q, int64_t sb, int64_t sh, int64_t sn, const void *kk, const void *v,
+                             int64_t ksb, int64_t ksh, int64_t ksn, const float *gate, int64_t gsb, int64_t gsh,
+                             int64_t gsn, float scale, float logit_clamp, const float *lse, const void *out,
+                             const void *dout, int64_t osb, int64_t osh, int64_t osn, float *dq, float *dgate,
+                             float *rowterm, void *stream) {
+    if (dtype != PI_ATTN_BF16) return PI_ATTN_EUNSUPPORTED;
+    if (!shard_positions_ok(nseq, qpos0, nq, kvpos0, nkv)) return PI_ATTN_EINVAL;
+    if (B < 0 || H < 0 || k < 0 || pi < 0) return PI_ATTN_EINVAL;
+    if ((int64_t)B * H * nkv >= kMaxRows) return PI_ATTN_EINVAL;
+    BwdParams p{};
+    FwdParams &f = p.f;
+    bool empty;
+    const int status = check_sequence(dtype, B, H, nq, D, k, pi, causal, q, q, q, sb, sh, sn, scale, logit_clamp, out,
+                                      osb, osh, osn, f, empty);
+    if (status != PI_ATTN_OK || empty) return status;
+    if (!kk || !v || !aligned16(kk) || !aligned16(v)) return PI_ATTN_EINVAL;
+    if (!stride16(ksb, 2) || !stride16(ksh, 2) || !stride16(ksn, 2)) return PI_ATTN_EINVAL;
+    if (!tile_span_ok(k, nseq, causal != 0, ksn, 2)) return PI_ATTN_EUNSUPPORTED;
+    if (!shard_kv_covered(k, pi, causal != 0, nseq, qpos0, nq, kvpos0, nkv)) return PI_ATTN_EINVAL;
+    if (!gate || !lse || !dout || !dq || !dgate || !rowterm) return PI_ATTN_EINVAL;
+    if (!aligned16(dout) || !aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
+    if (!aligned4(lse) || !aligned16(dq) || !aligned4(dgate) || !aligned4(rowterm)) return PI_ATTN_EINVAL;
+    f.k_ptr = kk; f.v = v;
+    f.ksb = ksb; f.ksh = ksh; f.ksn = ksn;
+    f.qpos0 = qpos0; f.kvpos0 = kvpos0; f.kvend = kvpos0 + nkv; f.nseq = nseq; f.qend = qpos0 + nq;
+    f.gate = gate; f.gsb = gsb; f.gsh = gsh; f.gsn = gsn;
+    p.dtype = 1;
+    p.lse = lse;
+    p.out = out; p.dout = dout; p.osb = osb; p.osh = osh; p.osn = osn;
+    p.dq = dq; p.dgate = dgate; p.rowterm = rowterm;
+    return from_hip(launch_backward_q_bf16(p, (hipStream_t)stream));
+}
+
+int pi_attn_backward_shard_kv(int32_t dtype, int32_t B, int32_t H, int32_t D, int32_t k, int32_t pi,
+                              int32_t causal, int32_t nseq, int32_t kpos0, int32_t nk, int32_t qpos0, int32_t nqh,
+                              const void *q, int64_t sb, int64_t sh, int64_t sn, const void *kk, const void *v,
+                              int64_t ksb, int64_t ksh, int64_t ksn, const float *gate, int64_t gsb, int64_t gsh,
+                              int64_t gsn, float scale, float logit_clamp, const float *lse, const float *rowterm,
+                              const void *dout, int64_t osb, int64_t osh, int64_t osn, float *dk, float *dv,
+                              void *stream) {
+    if (dtype != PI_ATTN_BF16) return PI_ATTN_EUNSUPPORTED;
+    if (!shard_positions_ok(nseq, kpos0, nk, qpos0, nqh)) return PI_ATTN_EINVAL;
+    if (B < 0 || H < 0 || k < 0 || pi < 0) return PI_ATTN_EINVAL;
+    if ((int64_t)B * H * nqh >= kMaxRows) return PI_ATTN_EINVAL;
+    // the keys' checks through the whole-sequence ones over the nk key rows
+    // (their strides and pointers; q and dL/dy are checked below)
+    BwdParams p{};
+    FwdParams &f = p.f;
+    bool empty;
+    const int status = check_sequence(dtype, B, H, nk, D, k, pi, causal, kk, kk, v, ksb, ksh, ksn, scale,
+                                      logit_clamp, kk, ksb, ksh, ksn, f, empty);
+    if (status != PI_ATTN_OK || empty) return status;
+    if (!q || !dout || !aligned16(q) || !aligned16(dout)) return PI_ATTN_EINVAL;
+    if (!stride16(sb, 2) || !stride16(sh, 2) || !stride16(sn, 2)) return PI_ATTN_EINVAL;
+    if (!stride16(osb, 2) || !stride16(osh, 2) || !stride16(osn, 2)) return PI_ATTN_EINVAL;
+    if (!tile_span_ok(k, nseq, causal != 0, sn, 2) || !tile_span_ok(k, nseq, causal != 0, osn, 2))
+        return PI_ATTN_EUNSUPPORTED;
+    // the query rows held must include every query whose working set holds
+    // one of the keys: from max(k, pi) rows before the first key
+    // (bidirectional; the keys themselves when causal) to max(k, pi) rows
+    // past the last one (k when pi <= k), within the sequence
+    const int reach = pi > k ? std::max(k, pi) : k;
+    const int64_t lo = causal ? kpos0 : std::max(0, kpos0 - reach);
+    const int64_t hi = std::min<int64_t>(nseq, (int64_t)kpos0 + nk + reach);
+    if (qpos0 > lo || (int64_t)qpos0 + nqh < hi) return PI_ATTN_EINVAL;
+    if (!gate || !lse || !rowterm || !dk || !dv) return PI_ATTN_EINVAL;
+    if (!aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
+    if (!aligned4(lse) || !aligned4(rowterm) || !aligned16(dk) || !aligned16(dv)) return PI_ATTN_EINVAL;
+    f.q = q; f.sb = sb; f.sh = sh; f.sn = sn;
+    f.k_ptr = kk; f.v = v; f.ksb = ksb; f.ksh = ksh; f.ksn = ksn;
+    f.qpos0 = qpos0; f.kvpos0 = kpos0; f.kvend = kpos0 + nk; f.nseq = nseq; f.qend = qpos0 + nqh;
+    f.gate = gate; f.gsb = gsb; f.gsh = gsh; f.gsn = gsn;
+    p.dtype = 1;
+    p.lse = lse;
+    p.dout = dout; p.osb = osb; p.osh = osh; p.osn = osn;
+    p.dk = dk; p.dv = dv; p.rowterm = const_cast<float *>(rowterm);
+    return from_hip(launch_backward_kv_bf16(p, (hipStream_t)stream));
 }
 
 int pi_attn_gate_grad_per_head(int32_t B, int32_t H, int32_t N, const float *dgate, float *out, void *stream) {

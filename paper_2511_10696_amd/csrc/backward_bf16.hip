@@ -166,28 +166,31 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 5, c = lane & 31;
     const int N = p.N, kw = p.k, pi = p.pi;
-    const int t0 = qt * BM;
+    // absolute positions: queries [qpos0, NQ), keys and partners below NS
+    const int NQ = p.qpos0 + N, NS = p.nseq;
+    const int t0 = p.qpos0 + qt * BM;
     const int q0 = t0 + 32 * w;
     const int t = q0 + c;
-    const bool t_ok = t < N;
-    const int tq = t_ok ? t : 0;
-    const int64_t row = bh * N + tq;
+    const bool t_ok = t < NQ;
+    const int tq = t_ok ? t : p.qpos0;
+    const int64_t row = bh * N + (tq - p.qpos0);
 
-    const int64_t base = b * p.sb + h * p.sh;
-    const __bf16 *qp = (const __bf16 *)p.q + base;
-    const __bf16 *kp = (const __bf16 *)p.k_ptr + base;
-    const __bf16 *vp = (const __bf16 *)p.v + base;
-    const __bf16 *op = (const __bf16 *)bp.dout + b * bp.osb + h * bp.osh;
-    const int64_t sn = p.sn;
+    // row pointers indexed by absolute position (only rows held are read)
+    const int64_t sn = p.sn, ksn = p.ksn;
+    const __bf16 *qp = (const __bf16 *)p.q + b * p.sb + h * p.sh - (int64_t)p.qpos0 * sn;
+    const int64_t kvbase = b * p.ksb + h * p.ksh - (int64_t)p.kvpos0 * ksn;
+    const __bf16 *kp = (const __bf16 *)p.k_ptr + kvbase;
+    const __bf16 *vp = (const __bf16 *)p.v + kvbase;
+    const __bf16 *op = (const __bf16 *)bp.dout + b * bp.osb + h * bp.osh - (int64_t)p.qpos0 * bp.osn;
 
     const int kb0 = window_lo(t0, kw) & ~31;
-    const int kend = BIDIR ? (int)min((int64_t)t0 + BM + kw, (int64_t)N) : min(t0 + BM, N);
+    const int kend = min(BIDIR ? (int)min((int64_t)t0 + BM + kw, (int64_t)NS) : min(t0 + BM, NQ), p.kvend);
     const int ntiles = (kend - kb0 + TK - 1) / TK;
-    const int rowb = (int)(2 * sn);
+    const int rowb = (int)(2 * ksn);
     const __amdgpu_buffer_rsrc_t rk =
-        __builtin_amdgcn_make_buffer_rsrc((void *)(kp + (int64_t)kb0 * sn), (short)0, (kend - kb0) * rowb, 0x00020000);
+        __builtin_amdgcn_make_buffer_rsrc((void *)(kp + (int64_t)kb0 * ksn), (short)0, (kend - kb0) * rowb, 0x00020000);
     const __amdgpu_buffer_rsrc_t rv =
-        __builtin_amdgcn_make_buffer_rsrc((void *)(vp + (int64_t)kb0 * sn), (short)0, (kend - kb0) * rowb, 0x00020000);
+        __builtin_amdgcn_make_buffer_rsrc((void *)(vp + (int64_t)kb0 * ksn), (short)0, (kend - kb0) * rowb, 0x00020000);
     Stage<D> st;
     Stage<D> st0[BPT];
 #pragma unroll
@@ -202,10 +205,10 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
         qf[s] = t_ok ? qv : bf16x8{};
         of[s] = t_ok ? ov : bf16x8{};
     }
-    const float gl = p.gate[b * p.gsb + h * p.gsh + tq * p.gsn];
+    const float gl = p.gate[b * p.gsb + h * p.gsh + (tq - p.qpos0) * p.gsn];
     const FusionBias fb = fusion_bias(gl, CLAMP);
     // r_t = <dL/dy_t, y_t>: this lane's dims 16s + 8g + [0, 8), then the pair
-    const __bf16 *yp = (const __bf16 *)bp.out + b * bp.osb + h * bp.osh;
+    const __bf16 *yp = (const __bf16 *)bp.out + b * bp.osb + h * bp.osh - (int64_t)p.qpos0 * bp.osn;
     float rpart = 0.0f;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
@@ -233,12 +236,12 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
     // Partner row prow of this lane's query (has_p: it exists).
     auto partner = [&](int prow, bool has_p) {
         if (__builtin_amdgcn_ballot_w64(has_p) == 0) return;
-        const int prc = has_p ? prow : 0;
+        const int prc = has_p ? prow : p.kvpos0;
         bf16x8 kpf[KS], vpf[KS];
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
-            kpf[s] = *reinterpret_cast<const bf16x8 *>(kp + prc * sn + 16 * s + 8 * g);
-            vpf[s] = *reinterpret_cast<const bf16x8 *>(vp + prc * sn + 16 * s + 8 * g);
+            kpf[s] = *reinterpret_cast<const bf16x8 *>(kp + prc * ksn + 16 * s + 8 * g);
+            vpf[s] = *reinterpret_cast<const bf16x8 *>(vp + prc * ksn + 16 * s + 8 * g);
         }
         f32x16 sa = {}, da = {};
 #pragma unroll
@@ -268,7 +271,7 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
         for (int db = 0; db < DB; ++db) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const uint2 raw = *reinterpret_cast<const uint2 *>(kp + prc * sn + 32 * db + 8 * i + 4 * g);
+                const uint2 raw = *reinterpret_cast<const uint2 *>(kp + prc * ksn + 32 * db + 8 * i + 4 * g);
                 dq[db][4 * i + 0] += dd * __uint_as_float(raw.x << 16);
                 dq[db][4 * i + 1] += dd * __uint_as_float(raw.x & 0xffff0000u);
                 dq[db][4 * i + 2] += dd * __uint_as_float(raw.y << 16);
@@ -277,18 +280,18 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
         }
     };
     partner(t - pi, partner_enabled(kw, pi) && t - pi >= 0 && t_ok);
-    if constexpr (BIDIR) partner(t + pi, t_ok && partner_fwd_of(t, kw, pi, N) >= 0);
+    if constexpr (BIDIR) partner(t + pi, t_ok && partner_fwd_of(t, kw, pi, NS) >= 0);
 #pragma unroll
     for (int hf = 0; hf < BPT; ++hf) tile_store<D>(st0[hf], tA, hf, tid);
     __syncthreads();
 
     // ---- window band ---------------------------------------------------------
     auto block = [&](const TileBuf<D> &tb, int j0, int blk) {
-        const bool act = BIDIR ? j0 < kend && q0 < N && j0 - (q0 + 31) <= kw && j0 + 31 >= q0 - kw
-                               : j0 < kend && q0 < N && j0 <= q0 + 31 && j0 + 31 >= q0 - kw;
+        const bool act = BIDIR ? j0 < kend && q0 < NQ && j0 - (q0 + 31) <= kw && j0 + 31 >= q0 - kw
+                               : j0 < kend && q0 < NQ && j0 <= q0 + 31 && j0 + 31 >= q0 - kw;
         if (!act) return;
-        const bool edge = BIDIR ? !(j0 + 31 - q0 <= kw && q0 + 31 - j0 <= kw) || q0 + 31 >= N || j0 + 31 >= N
-                                : !(j0 + 31 <= q0 && j0 >= q0 + 31 - kw) || q0 + 31 >= N;
+        const bool edge = BIDIR ? !(j0 + 31 - q0 <= kw && q0 + 31 - j0 <= kw) || q0 + 31 >= NQ || j0 + 31 >= NS
+                                : !(j0 + 31 <= q0 && j0 >= q0 + 31 - kw) || q0 + 31 >= NQ;
         bf16x8 f[KS];
         read_rows<D>(f, tb.k, blk, c, g);
         f32x16 sc = {};
@@ -314,7 +317,7 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
             }
             if (edge) {
                 const int j = j0 + 8 * (e >> 2) + 4 * g + (e & 3);
-                const bool ok = BIDIR ? t_ok && j < N && j - t <= kw && t - j <= kw : t_ok && j <= t && j >= t - kw;
+                const bool ok = BIDIR ? t_ok && j < NS && j - t <= kw && t - j <= kw : t_ok && j <= t && j >= t - kw;
                 if (!ok) delta2 = -INFINITY;
             }
             const float wgt = __builtin_amdgcn_exp2f(delta2 - lse2);

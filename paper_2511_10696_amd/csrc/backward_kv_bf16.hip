@@ -104,19 +104,24 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 5, c = lane & 31;
     const int N = p.N, kw = p.k, pi = p.pi;
-    const int j0 = kt * BK;
+    // absolute positions: keys [kvpos0, NK) (this pass's keys), query rows
+    // held [QS, QE) (their q, dL/dy, lse, row terms and gate)
+    const int NK = p.kvpos0 + N, QS = p.qpos0, QE = min(p.qend, p.nseq);
+    const int j0 = p.kvpos0 + kt * BK;
     const int kq0 = j0 + 32 * w;
     const int j = kq0 + c;           // this lane's key
-    const bool j_ok = j < N;
-    const int jq = j_ok ? j : 0;
+    const bool j_ok = j < NK;
+    const int jq = j_ok ? j : p.kvpos0;
 
-    const int64_t base = b * p.sb + h * p.sh;
-    const __bf16 *qp = (const __bf16 *)p.q + base;
-    const __bf16 *kp = (const __bf16 *)p.k_ptr + base;
-    const __bf16 *vp = (const __bf16 *)p.v + base;
-    const __bf16 *op = (const __bf16 *)bp.dout + b * bp.osb + h * bp.osh;
-    const int64_t sn = p.sn, osn = bp.osn;
-    const int64_t rbase = bh * N;
+    // row pointers and per-row arrays indexed by absolute position
+    const int64_t sn = p.sn, ksn = p.ksn, osn = bp.osn;
+    const __bf16 *qp = (const __bf16 *)p.q + b * p.sb + h * p.sh - (int64_t)QS * sn;
+    const int64_t kvbase = b * p.ksb + h * p.ksh - (int64_t)p.kvpos0 * ksn;
+    const __bf16 *kp = (const __bf16 *)p.k_ptr + kvbase;
+    const __bf16 *vp = (const __bf16 *)p.v + kvbase;
+    const __bf16 *op = (const __bf16 *)bp.dout + b * bp.osb + h * bp.osh - (int64_t)QS * osn;
+    const int64_t rbase = bh * (int64_t)(p.qend - QS) - QS;   // lse, row terms [B][H][qend - qpos0]
+    const int64_t obase = bh * (int64_t)N - p.kvpos0;         // dk, dv [B][H][N]
     const bool exact = CLAMP;
     const float c2 = p.scale * kLog2e;
 
@@ -124,8 +129,8 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
     bf16x8 kf[KS], vf[KS];
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-        const bf16x8 kv = *reinterpret_cast<const bf16x8 *>(kp + jq * sn + 16 * s + 8 * g);
-        const bf16x8 vv = *reinterpret_cast<const bf16x8 *>(vp + jq * sn + 16 * s + 8 * g);
+        const bf16x8 kv = *reinterpret_cast<const bf16x8 *>(kp + jq * ksn + 16 * s + 8 * g);
+        const bf16x8 vv = *reinterpret_cast<const bf16x8 *>(vp + jq * ksn + 16 * s + 8 * g);
         kf[s] = j_ok ? kv : bf16x8{};
         vf[s] = j_ok ? vv : bf16x8{};
     }
@@ -141,15 +146,15 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
     // is): tiles [0, nband), [nband, nband + npar), then the rest.  Query
     // rows [lo, hi) of a stream; rows outside [0, N) are zero and masked.
     const int band_lo = BIDIR ? window_lo(j0, kw) & ~31 : j0;
-    const int band_hi = BIDIR ? (int)min((int64_t)j0 + BK + kw, (int64_t)N) : min(N, j0 + BK + kw);
+    const int band_hi = BIDIR ? (int)min((int64_t)j0 + BK + kw, (int64_t)QE) : min(QE, j0 + BK + kw);
     const int nband = band_hi > band_lo ? (band_hi - band_lo + TQ - 1) / TQ : 0;
-    const bool has_par = partner_enabled(kw, pi) && (int64_t)j0 + pi < N;
+    const bool has_par = partner_enabled(kw, pi) && (int64_t)j0 + pi < QE;
     const int par_lo = j0 + pi;
-    const int par_hi = has_par ? min(N, j0 + pi + BK) : par_lo;
+    const int par_hi = has_par ? min(QE, j0 + pi + BK) : par_lo;
     const int npar = has_par ? (par_hi - par_lo + TQ - 1) / TQ : 0;
     const bool has_par2 = BIDIR && partner_enabled(kw, pi) && j0 + BK > pi;
     const int par2_lo = j0 - pi;   // may be negative
-    const int par2_hi = has_par2 ? min(N, j0 + BK - pi) : par2_lo;
+    const int par2_hi = has_par2 ? min(QE, j0 + BK - pi) : par2_lo;
     const int npar2 = has_par2 ? (par2_hi - par2_lo + TQ - 1) / TQ : 0;
     const int ntiles = nband + npar + npar2;
 
@@ -162,13 +167,13 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
     auto tile_end = [&](int m) { return m < nband ? band_hi : (!BIDIR || m < nband + npar) ? par_hi : par2_hi; };
     auto load = [&](Stage<D> &st, int m) {
         const int q0m = tile_start(m), lim = tile_end(m);
-        const int tfirst = BIDIR && q0m < 0 ? 0 : q0m;   // an always-valid row of the stream
+        const int tfirst = min(max(q0m, QS), QE - 1);   // an always-held row
 #pragma unroll
         for (int u = 0; u < T::CH; ++u) {
             const int cid = tid + NT * u;
             const int row = cid / T::CPR, pc = cid % T::CPR;
             const int t = q0m + row;
-            const bool ok = BIDIR ? t >= 0 && t < lim : t < lim;   // causal streams start at row >= 0
+            const bool ok = t >= QS && t < lim;
             const int tc = ok ? t : tfirst;
             const uint4 qv = *reinterpret_cast<const uint4 *>(qp + tc * sn + 8 * pc);
             const uint4 ov = *reinterpret_cast<const uint4 *>(op + tc * osn + 8 * pc);
@@ -177,8 +182,8 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
         }
         if (tid < TQ) {
             const int t = q0m + tid;
-            const int tc = (BIDIR ? t >= 0 && t < lim : t < lim) ? t : tfirst;
-            const FusionBias fb = fusion_bias(p.gate[b * p.gsb + h * p.gsh + tc * p.gsn], exact);
+            const int tc = (t >= QS && t < lim) ? t : tfirst;
+            const FusionBias fb = fusion_bias(p.gate[b * p.gsb + h * p.gsh + (tc - QS) * p.gsn], exact);
             st.lse2 = (bp.lse[rbase + tc] - fb.lse_shift) * kLog2e;
             st.r = bp.rowterm[rbase + tc];
             st.bias = m < nband ? fb.local : fb.partner;
@@ -207,14 +212,15 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
         if (partner) {
             act = blk == (w & 1) && t0b == (BIDIR && kind == 2 ? kq0 - pi : kq0 + pi);
         } else if constexpr (BIDIR) {
-            act = t0b < lim && kq0 < N && t0b - (kq0 + 31) <= kw && t0b + 31 >= kq0 - kw;
+            act = t0b < lim && kq0 < NK && t0b - (kq0 + 31) <= kw && t0b + 31 >= kq0 - kw;
         } else {
-            act = t0b < lim && kq0 < N && t0b <= kq0 + 31 + kw && t0b + 31 >= kq0;
+            act = t0b < lim && kq0 < NK && t0b <= kq0 + 31 + kw && t0b + 31 >= kq0;
         }
         if (!act) return;
-        const bool edge = BIDIR ? partner || !(t0b + 31 - kq0 <= kw && kq0 + 31 - t0b <= kw) || t0b + 31 >= N ||
-                                      kq0 + 31 >= N
-                                : partner || !(t0b >= kq0 + 31 && t0b + 31 <= kq0 + kw) || t0b + 31 >= N || kq0 + 31 >= N;
+        const bool edge = BIDIR ? partner || !(t0b + 31 - kq0 <= kw && kq0 + 31 - t0b <= kw) || t0b + 31 >= QE ||
+                                      kq0 + 31 >= NK || t0b < QS
+                                : partner || !(t0b >= kq0 + 31 && t0b + 31 <= kq0 + kw) || t0b + 31 >= QE ||
+                                      kq0 + 31 >= NK;
         // rows of this block (A operands: query l%32, dims 16s + 8g): chunk
         // (2s + g) ^ x = 2(s ^ (x >> 1)) + (g ^ (x & 1)), x = chunk_x(row)
         const int xr = chunk_x(32 * blk + c);
@@ -254,9 +260,9 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
                     bool ok;
                     if constexpr (BIDIR) {
                         const bool is_par = kind == 2 ? j - t == pi : t - j == pi;
-                        ok = (partner ? is_par : t - j <= kw && j - t <= kw) && t >= 0 && t < N && j_ok;
+                        ok = (partner ? is_par : t - j <= kw && j - t <= kw) && t >= QS && t < QE && j_ok;
                     } else {
-                        ok = partner ? (t - j == pi && t < N && j_ok) : (t >= j && t - j <= kw && t < N && j_ok);
+                        ok = partner ? (t - j == pi && t < QE && j_ok) : (t >= j && t - j <= kw && t < QE && j_ok);
                     }
                     if (!ok) delta2 = -INFINITY;
                 }
@@ -330,7 +336,7 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
 
     // ---- store: lane (c, g) holds dims 32db + 8i + 4g + [0, 4) of key c ----
     if (j_ok) {
-        const int64_t row = rbase + j;
+        const int64_t row = obase + j;
         float *dkp = bp.dk + row * D, *dvp = bp.dv + row * D;
 #pragma unroll
         for (int d = 0; d < DB; ++d) {

@@ -34,6 +34,7 @@ struct FwdParams {
     // absolute position qpos0 + i, k/v row i is kvpos0 + i, k/v rows end at
     // kvend, the sequence has nseq positions.  A whole sequence: 0, 0, N, N.
     int qpos0, kvpos0, kvend, nseq;
+    int qend;                       // backward key pass: query rows held end at qend (a whole sequence: N)
     int64_t ksb, ksh, ksn;          // element strides of k and v (a whole sequence: sb, sh, sn)
 };
 

@@ -191,6 +191,66 @@ def test_forward_shard_empty_is_noop(lib, kw):
     assert shard(lib, **kw) == 0
 
 
+def shard_q(lib, **kw):
+    # a valid-looking causal query pass: queries [1024, 1536) of 4096, k/v from 512
+    a = dict(dtype=1, B=1, H=2, D=64, k=128, pi=512, causal=1, nseq=4096, qpos0=1024, nq=512, kvpos0=512, nkv=1024,
+             q=16, sb=65536, sh=32768, sn=64, kk=16, v=16, ksb=131072, ksh=65536, ksn=64, gate=16, gsb=0, gsh=1,
+             gsn=0, scale=0.125, clamp=0.0, lse=16, out=16, dout=16, osb=65536, osh=32768, osn=64, dq=16, dg=16,
+             rt=16, stream=None)
+    a.update(kw)
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.pi_attn_backward_shard_q(
+        a["dtype"], a["B"], a["H"], a["D"], a["k"], a["pi"], a["causal"], a["nseq"], a["qpos0"], a["nq"],
+        a["kvpos0"], a["nkv"], vp(a["q"]), a["sb"], a["sh"], a["sn"], vp(a["kk"]), vp(a["v"]), a["ksb"], a["ksh"],
+        a["ksn"], vp(a["gate"]), a["gsb"], a["gsh"], a["gsn"], a["scale"], a["clamp"], vp(a["lse"]), vp(a["out"]),
+        vp(a["dout"]), a["osb"], a["osh"], a["osn"], vp(a["dq"]), vp(a["dg"]), vp(a["rt"]), vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=0), EUNSUP), (dict(kvpos0=544), EINVAL), (dict(nq=4000), EINVAL), (dict(nkv=1023), EINVAL),
+    (dict(lse=None), EINVAL), (dict(out=None), EINVAL), (dict(dout=None), EINVAL), (dict(dq=None), EINVAL),
+    (dict(dg=None), EINVAL), (dict(rt=None), EINVAL), (dict(dq=20), EINVAL), (dict(kk=None), EINVAL),
+    (dict(gate=None), EINVAL), (dict(qpos0=-1), EINVAL),
+])
+def test_backward_shard_q_rejects(lib, kw, code):
+    assert shard_q(lib, **kw) == code
+
+
+def test_backward_shard_q_empty_is_noop(lib):
+    assert shard_q(lib, nq=0) == 0
+
+
+def shard_kv(lib, **kw):
+    # a valid-looking causal key pass: keys [1024, 1536) of 4096, query rows [1024, 2048) held
+    a = dict(dtype=1, B=1, H=2, D=64, k=128, pi=512, causal=1, nseq=4096, kpos0=1024, nk=512, qpos0=1024, nqh=1024,
+             q=16, sb=131072, sh=65536, sn=64, kk=16, v=16, ksb=65536, ksh=32768, ksn=64, gate=16, gsb=0, gsh=1,
+             gsn=0, scale=0.125, clamp=0.0, lse=16, rt=16, dout=16, osb=131072, osh=65536, osn=64, dk=16, dv=16,
+             stream=None)
+    a.update(kw)
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.pi_attn_backward_shard_kv(
+        a["dtype"], a["B"], a["H"], a["D"], a["k"], a["pi"], a["causal"], a["nseq"], a["kpos0"], a["nk"],
+        a["qpos0"], a["nqh"], vp(a["q"]), a["sb"], a["sh"], a["sn"], vp(a["kk"]), vp(a["v"]), a["ksb"], a["ksh"],
+        a["ksn"], vp(a["gate"]), a["gsb"], a["gsh"], a["gsn"], a["scale"], a["clamp"], vp(a["lse"]), vp(a["rt"]),
+        vp(a["dout"]), a["osb"], a["osh"], a["osn"], vp(a["dk"]), vp(a["dv"]), vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=0), EUNSUP), (dict(qpos0=1056, nqh=992), EINVAL),   # queries held start after the first key
+    (dict(nqh=1023), EINVAL),                                       # short of the last key + pi
+    (dict(causal=0), EINVAL),                                       # bidirectional: from the first key - pi
+    (dict(nk=4000), EINVAL), (dict(kk=None), EINVAL), (dict(q=None), EINVAL), (dict(dout=None), EINVAL),
+    (dict(lse=None), EINVAL), (dict(rt=None), EINVAL), (dict(dk=None), EINVAL), (dict(dv=8), EINVAL),
+    (dict(gate=None), EINVAL), (dict(osn=4), EINVAL),
+])
+def test_backward_shard_kv_rejects(lib, kw, code):
+    assert shard_kv(lib, **kw) == code
+
+
+def test_backward_shard_kv_empty_is_noop(lib):
+    assert shard_kv(lib, nk=0) == 0
+
+
 def ggh(lib, **kw):
     a = dict(B=2, H=3, N=100, dg=16, out=16, stream=None)
     a.update(kw)

@@ -1,11 +1,15 @@
-"""GPU tests of pi_attn_forward_shard: a sequence split into shards, each
-shard's forward run on its queries with its k/v rows plus the halo before
-(and, bidirectional, after) it, reproduces the whole-sequence forward.
+"""GPU tests of the sequence-shard calls: a sequence split into shards,
+each shard's forward run on its queries with its k/v rows plus the halo
+before (and, bidirectional, after) it, reproduces the whole-sequence
+forward; the backward split the same way (each shard's query pass, the row
+terms gathered as a neighbour would send them, each shard's key pass over
+its keys with the query rows that reach them) reproduces the whole-sequence
+gradients.
 
-Shards whose first query is a multiple of 128 and whose k/v rows start at a
-multiple of 32 run the same tiles in the same order as the whole-sequence
-call, so their outputs and lse must be bit-identical to its rows.  Other
-shard boundaries are held to the bf16 bar against the oracle.
+Shards whose first query (key) is a multiple of 128 run the same tiles in
+the same order as the whole-sequence call, so their results must be
+bit-identical to its rows.  Other shard boundaries are held to the bf16 bar
+against the oracle.
 """
 import numpy as np
 import pytest
@@ -109,3 +113,75 @@ def test_shard_of_the_benchmark_workload(device):
     full = pa.pi_attn_forward(q, k, v, gate, cfg.k, cfg.pi)
     torch.cuda.synchronize()
     assert torch.equal(out, full[:, :, s0:])
+
+
+# ---------------------------------------------------------------------------
+# backward over shards: the query pass per shard, the row terms gathered (the
+# halo a neighbour would send), then the key pass per shard
+# ---------------------------------------------------------------------------
+def q_rows_for_keys(nseq, k, pi, causal, kpos0, nk):
+    reach = max(k, pi) if pi > k else k
+    return (kpos0 if causal else max(0, kpos0 - reach)), min(nseq, kpos0 + nk + reach)
+
+
+def sharded_backward(q, k, v, gate, kw, pi, out, lse, dout, bounds, causal, pq):
+    B, H, N, D = q.shape
+    dqs, dgs, rts = [], [], []
+    for s0, s1 in bounds:
+        lo, hi = halo_rows(N, kw, pi, causal, s0, s1 - s0)
+        g = gate[:, :, s0:s1] if pq else gate
+        dq, dg, rt = pa.pi_attn_backward_shard_q(q[:, :, s0:s1], k[:, :, lo:hi], v[:, :, lo:hi], g, kw, pi, N, s0, lo,
+                                                 out[:, :, s0:s1], lse[:, :, s0:s1].contiguous(), dout[:, :, s0:s1],
+                                                 causal=causal)
+        dqs.append(dq)
+        dgs.append(dg)
+        rts.append(rt)
+    rowterm = torch.cat(rts, dim=2)
+    dks, dvs = [], []
+    for s0, s1 in bounds:
+        qlo, qhi = q_rows_for_keys(N, kw, pi, causal, s0, s1 - s0)
+        g = gate[:, :, qlo:qhi] if pq else gate
+        dk, dv = pa.pi_attn_backward_shard_kv(q[:, :, qlo:qhi], k[:, :, s0:s1], v[:, :, s0:s1], g, kw, pi, N, s0, qlo,
+                                              lse[:, :, qlo:qhi].contiguous(), rowterm[:, :, qlo:qhi].contiguous(),
+                                              dout[:, :, qlo:qhi], causal=causal)
+        dks.append(dk)
+        dvs.append(dv)
+    return tuple(torch.cat(x, dim=2) for x in (dqs, dks, dvs, dgs))
+
+
+@pytest.mark.parametrize("B,H,N,D,kw,pi,nshard", [
+    (1, 2, 4096, 128, 512, 1024, 4),
+    (2, 3, 2048, 64, 128, 256, 8),
+    (1, 2, 1536, 128, 40, 100, 3),
+    (1, 1, 1024, 64, 200, 150, 2),       # pi <= k: no partner
+])
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("pq", [False, True])
+def test_backward_shards_are_bit_identical(device, B, H, N, D, kw, pi, nshard, causal, pq):
+    cfg = W.ForwardConfig("custom", B, H, N, D, kw, pi, torch.bfloat16)
+    q, k, v, gate = W.forward_inputs(cfg, 6, device, per_query_gate=pq)
+    out, lse = pa.pi_attn_forward(q, k, v, gate, kw, pi, return_lse=True, causal=causal)
+    dout = W.cotangent(q.shape, q.dtype, 6, device)
+    whole = pa.pi_attn_backward(q, k, v, gate, kw, pi, out, lse, dout, gate_grad_per_query=True, causal=causal)
+    step = N // nshard
+    bounds = [(i * step, (i + 1) * step) for i in range(nshard)]
+    got = sharded_backward(q, k, v, gate, kw, pi, out, lse, dout, bounds, causal, pq)
+    torch.cuda.synchronize()
+    for name, a, b in zip(("dq", "dk", "dv", "dgate"), got, whole):
+        assert torch.equal(a, b), name
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_backward_unaligned_shards_against_the_oracle(device, causal):
+    from tests.test_gpu_backward import assert_grad
+    B, H, N, D, kw, pi = 1, 2, 700, 64, 40, 130
+    cfg = W.ForwardConfig("custom", B, H, N, D, kw, pi, torch.bfloat16)
+    q, k, v, gate = W.forward_inputs(cfg, 7, device, per_query_gate=True)
+    out, lse = pa.pi_attn_forward(q, k, v, gate, kw, pi, return_lse=True, causal=causal)
+    dout = W.cotangent(q.shape, q.dtype, 7, device)
+    bounds = [(0, 100), (100, 101), (101, 450), (450, 700)]
+    got = sharded_backward(q, k, v, gate, kw, pi, out, lse, dout, bounds, causal, True)
+    torch.cuda.synchronize()
+    refs = oracle.backward(q, k, v, gate, kw, pi, dout, causal=causal)
+    for name, a, ref in zip(("dq", "dk", "dv", "dgate"), got, refs):
+        assert_grad(np32(a), ref, name, torch.bfloat16)
