@@ -517,30 +517,53 @@ def bench_smallk(W, pa, torch, dev, stream, steps, warmup):
     return res
 
 
-def bench_shard(cfg, W, pa, torch, dev, stream, steps, warmup, nshard=8):
-    """The forward of one rank's share of the fwd32k sequence sharded
-    ``nshard`` ways: the last shard's queries and its k/v rows plus the pi
-    halo rows before it, held as contiguous tensors as a rank would hold
-    them."""
+def bench_shard(cfg, W, pa, torch, dev, stream, steps, warmup, nshard=8, rank=6):
+    """One rank's share of the fwd32k sequence sharded ``nshard`` ways (an
+    interior rank: halos on both sides), held as contiguous tensors as the
+    rank would hold them: the forward over its queries with the pi halo rows
+    of k/v before them, and the backward's two passes -- the query pass over
+    its queries, the key pass over its keys with the query rows that reach
+    them (its own and the max(k, pi) rows after them, whose lse and row terms
+    a neighbour would send)."""
     q, k, v, gate = W.forward_inputs(cfg, 0, dev)
     n = cfg.N
-    s0 = n - n // nshard
-    lo = max(0, s0 - max(cfg.k, cfg.pi))
-    qs, ks, vs = (x[:, :, a:].contiguous() for x, a in ((q, s0), (k, lo), (v, lo)))
-    del q, k, v
+    s0, s1 = rank * n // nshard, (rank + 1) * n // nshard
+    reach = max(cfg.k, cfg.pi)
+    lo = max(0, s0 - reach)              # k/v rows held by the forward and the query pass
+    qhi = min(n, s1 + reach)             # query rows held by the key pass
+    qs, ks, vs = (x[:, :, a:b].contiguous() for x, a, b in ((q, s0, s1), (k, lo, s1), (v, lo, s1)))
     out = torch.empty_like(qs)
     ms, _, _ = time_launches(
         torch, lambda: pa.pi_attn_forward_shard(qs, ks, vs, gate, cfg.k, cfg.pi, n, s0, lo, out=out),
         steps, warmup, stream)
-    keys, flops, nbytes = shard_algorithmic(cfg, s0, n, lo)
+    keys, flops, nbytes = shard_algorithmic(cfg, s0, s1, lo)
     rl, mf = roofline_of(flops, nbytes, ms / 1e3, "forward_bf16_kernel<128,false,false,false> (one shard)")
-    del qs, ks, vs, out
+    res = {"workload": (f"fwd32k sequence-sharded {nshard} ways, rank {rank}'s share: queries [{s0}, {s1}), "
+                        f"k/v rows [{lo}, {s1}) (its own and the pi = {cfg.pi} halo rows), B1 H32 D128 k512"),
+           "steps": steps, "us_per_step": round(ms * 1e3, 2),
+           "query_positions_per_s": round(cfg.B * (s1 - s0) / (ms / 1e3), 1),
+           "attended_keys_per_s": round(keys / (ms / 1e3), 1), "roofline": rl, "roofline_mfma": mf}
+    # backward: the forward's lse and output over the query rows the key pass
+    # holds, their row terms from a query pass over the same rows (what the
+    # neighbour's query pass and the halo exchange would deliver)
+    kv_lo = max(0, s0 - reach)
+    qh, kh, vh = (x[:, :, a:b].contiguous() for x, a, b in ((q, s0, qhi), (k, kv_lo, qhi), (v, kv_lo, qhi)))
+    outh, lseh = pa.pi_attn_forward_shard(qh, kh, vh, gate, cfg.k, cfg.pi, n, s0, kv_lo, return_lse=True)
+    douth = W.cotangent(qh.shape, qh.dtype, 0, dev)
+    _, _, rth = pa.pi_attn_backward_shard_q(qh, kh, vh, gate, cfg.k, cfg.pi, n, s0, kv_lo, outh, lseh, douth)
+    nq = s1 - s0
+    out_s, lse_s, dout_s = outh[:, :, :nq].contiguous(), lseh[:, :, :nq].contiguous(), douth[:, :, :nq].contiguous()
+    k_own, v_own = ks[:, :, s0 - lo:].contiguous(), vs[:, :, s0 - lo:].contiguous()
+
+    def backward():
+        pa.pi_attn_backward_shard_q(qs, ks, vs, gate, cfg.k, cfg.pi, n, s0, lo, out_s, lse_s, dout_s)
+        pa.pi_attn_backward_shard_kv(qh, k_own, v_own, gate, cfg.k, cfg.pi, n, s0, s0, lseh, rth, douth)
+    bms, _, _ = time_launches(torch, backward, max(1, steps // 5), 2, stream)
+    res["backward"] = {"us_per_step": round(bms * 1e3, 2),
+                       "note": "the query pass over the rank's queries and the key pass over its keys, one each"}
+    del q, k, v, qs, ks, vs, out, qh, kh, vh, outh, lseh, douth, rth
     torch.cuda.empty_cache()
-    return {"workload": (f"fwd32k sequence-sharded {nshard} ways, one rank's share: queries [{s0}, {n}), "
-                         f"k/v rows [{lo}, {n}) (its own and the pi = {cfg.pi} halo rows), B1 H32 D128 k512"),
-            "steps": steps, "us_per_step": round(ms * 1e3, 2),
-            "query_positions_per_s": round(cfg.B * (n - s0) / (ms / 1e3), 1),
-            "attended_keys_per_s": round(keys / (ms / 1e3), 1), "roofline": rl, "roofline_mfma": mf}
+    return res
 
 
 def bench_backward(cfg, W, pa, torch, dev, stream, steps, causal):
