@@ -279,10 +279,12 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
             }
         }
     };
-    partner(t - pi, partner_enabled(kw, pi) && t - pi >= 0 && t_ok);
-    if constexpr (BIDIR) partner(t + pi, t_ok && partner_fwd_of(t, kw, pi, NS) >= 0);
+    // the first tile goes to LDS before the partners are scored, so that its
+    // staging registers are free while the partner rows are held
 #pragma unroll
     for (int hf = 0; hf < BPT; ++hf) tile_store<D>(st0[hf], tA, hf, tid);
+    partner(t - pi, partner_enabled(kw, pi) && t - pi >= 0 && t_ok);
+    if constexpr (BIDIR) partner(t + pi, t_ok && partner_fwd_of(t, kw, pi, NS) >= 0);
     __syncthreads();
 
     // ---- window band ---------------------------------------------------------
@@ -301,8 +303,10 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
         f32x16 dp = {};
 #pragma unroll
         for (int s = 0; s < KS; ++s) dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[s], of[s], dp, 0, 0, 0);
+        // K^T for dQ: read before the softmax so the reads land during it,
+        // except with the clamp, whose extra terms leave no registers for it
         bf16x8 kt[2][DB];
-        read_cols<D>(kt, tb.k, blk, lane);
+        if constexpr (!CLAMP) read_cols<D>(kt, tb.k, blk, lane);
         float ds[16];
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
@@ -327,6 +331,7 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
             a_loc += cut ? 0.0f : pd;
             b_loc += cut ? 0.0f : wgt;
         }
+        if constexpr (CLAMP) read_cols<D>(kt, tb.k, blk, lane);
         bf16x8 dsb[2];
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc)

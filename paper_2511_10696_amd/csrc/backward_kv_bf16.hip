@@ -159,12 +159,17 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
     const int ntiles = nband + npar + npar2;
 
     // Stage tile m of the combined stream: 64 query rows starting at q0m.
-    auto tile_kind = [&](int m) { return m < nband ? 0 : (!BIDIR || m < nband + npar) ? 1 : 2; };
-    auto tile_start = [&](int m) {
-        return m < nband ? band_lo + TQ * m : (!BIDIR || m < nband + npar) ? par_lo + TQ * (m - nband)
-                                                                           : par2_lo + TQ * (m - nband - npar);
+    // Arithmetic with 0/1 weights rather than choices between variables: a
+    // choice between two memory locations (the captured values) compiles to a
+    // load through a chosen address, which keeps them in private memory.
+    auto in_par = [=](int m) { return m >= nband ? 1 : 0; };
+    auto in_par2 = [=](int m) { return BIDIR && m >= nband + npar ? 1 : 0; };
+    auto tile_kind = [=](int m) { return in_par(m) + in_par2(m); };
+    auto tile_start = [=](int m) {
+        const int s0 = band_lo + TQ * m, s1 = par_lo + TQ * (m - nband), s2 = par2_lo + TQ * (m - nband - npar);
+        return s0 + in_par(m) * (s1 - s0) + in_par2(m) * (s2 - s1);
     };
-    auto tile_end = [&](int m) { return m < nband ? band_hi : (!BIDIR || m < nband + npar) ? par_hi : par2_hi; };
+    auto tile_end = [=](int m) { return band_hi + in_par(m) * (par_hi - band_hi) + in_par2(m) * (par2_hi - par_hi); };
     auto load = [&](Stage<D> &st, int m) {
         const int q0m = tile_start(m), lim = tile_end(m);
         const int tfirst = min(max(q0m, QS), QE - 1);   // an always-held row
@@ -186,7 +191,8 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
             const FusionBias fb = fusion_bias(p.gate[b * p.gsb + h * p.gsh + (tc - QS) * p.gsn], exact);
             st.lse2 = (bp.lse[rbase + tc] - fb.lse_shift) * kLog2e;
             st.r = bp.rowterm[rbase + tc];
-            st.bias = m < nband ? fb.local : fb.partner;
+            const float bias_local = fb.local, bias_partner = fb.partner;
+            st.bias = m < nband ? bias_local : bias_partner;
         }
     };
     auto store = [&](const Stage<D> &st, QTile<D> &tb) {
