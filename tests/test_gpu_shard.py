@@ -185,3 +185,42 @@ def test_backward_unaligned_shards_against_the_oracle(device, causal):
     refs = oracle.backward(q, k, v, gate, kw, pi, dout, causal=causal)
     for name, a, ref in zip(("dq", "dk", "dv", "dgate"), got, refs):
         assert_grad(np32(a), ref, name, torch.bfloat16)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_clamped_shards_are_bit_identical(device, causal):
+    """A binding logit clamp through the sharded forward and both sharded
+    backward passes: equal to the whole-sequence results."""
+    B, H, N, D, kw, pi = 1, 2, 2048, 128, 96, 300
+    cfg = W.ForwardConfig("hh", B, H, N, D, kw, pi, torch.bfloat16, heavy_frac=0.05, heavy_mult=8.0)
+    q, k, v, gate = W.forward_inputs(cfg, 8, device, per_query_gate=True)
+    fw = dict(scale=0.5, logit_clamp=3.0)
+    out, lse = pa.pi_attn_forward(q, k, v, gate, kw, pi, return_lse=True, causal=causal, **fw)
+    bounds = [(0, 512), (512, 1024), (1024, 1536), (1536, 2048)]
+    sout, slse = run_shards(q, k, v, gate, kw, pi, bounds, causal, True, **fw)
+    dout = W.cotangent(q.shape, q.dtype, 8, device)
+    whole = pa.pi_attn_backward(q, k, v, gate, kw, pi, out, lse, dout, gate_grad_per_query=True, causal=causal, **fw)
+    dqs, dgs, rts = [], [], []
+    for s0, s1 in bounds:
+        lo, hi = halo_rows(N, kw, pi, causal, s0, s1 - s0)
+        dq, dg, rt = pa.pi_attn_backward_shard_q(q[:, :, s0:s1], k[:, :, lo:hi], v[:, :, lo:hi], gate[:, :, s0:s1],
+                                                 kw, pi, N, s0, lo, out[:, :, s0:s1], lse[:, :, s0:s1].contiguous(),
+                                                 dout[:, :, s0:s1], causal=causal, **fw)
+        dqs.append(dq)
+        dgs.append(dg)
+        rts.append(rt)
+    rowterm = torch.cat(rts, dim=2)
+    dks, dvs = [], []
+    for s0, s1 in bounds:
+        qlo, qhi = q_rows_for_keys(N, kw, pi, causal, s0, s1 - s0)
+        dk, dv = pa.pi_attn_backward_shard_kv(q[:, :, qlo:qhi], k[:, :, s0:s1], v[:, :, s0:s1], gate[:, :, qlo:qhi],
+                                              kw, pi, N, s0, qlo, lse[:, :, qlo:qhi].contiguous(),
+                                              rowterm[:, :, qlo:qhi].contiguous(), dout[:, :, qlo:qhi],
+                                              causal=causal, **fw)
+        dks.append(dk)
+        dvs.append(dv)
+    torch.cuda.synchronize()
+    assert torch.equal(sout, out) and torch.equal(slse, lse)
+    got = [torch.cat(x, dim=2) for x in (dqs, dks, dvs, dgs)]
+    for name, a, b in zip(("dq", "dk", "dv", "dgate"), got, whole):
+        assert torch.equal(a, b), name
