@@ -321,8 +321,8 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
             }
             if (edge) {
                 const int j = j0 + 8 * (e >> 2) + 4 * g + (e & 3);
-                const bool ok = BIDIR ? t_ok && j < NS && j - t <= kw && t - j <= kw : t_ok && j <= t && j >= t - kw;
-                if (!ok) delta2 = -INFINITY;
+                const bool ok = BIDIR ? t_ok & (j < NS) & (j - t <= kw) & (t - j <= kw) : t_ok & (j <= t) & (j >= t - kw);
+                delta2 = ok ? delta2 : -INFINITY;
             }
             const float wgt = __builtin_amdgcn_exp2f(delta2 - lse2);
             const float pd = wgt * dp[e];

@@ -232,49 +232,64 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
         const int xr = chunk_x(32 * blk + c);
         const int rb = (32 * blk + c) * T::ROW + 16 * (g ^ (xr & 1));
         const int rbo[2] = {rb + 32 * (xr >> 1), rb - 32 * (xr >> 1)};   // even, odd k-steps
+        bf16x8 qa[KS], oa[KS];
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            qa[s] = *reinterpret_cast<const bf16x8 *>(tb.q + rbo[s & 1] + 32 * s);
+            oa[s] = *reinterpret_cast<const bf16x8 *>(tb.o + rbo[s & 1] + 32 * s);
+        }
         f32x16 sc = {}, dp = {};
 #pragma unroll
-        for (int s = 0; s < KS; ++s)
-            sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                *reinterpret_cast<const bf16x8 *>(tb.q + rbo[s & 1] + 32 * s), kf[s], sc, 0, 0, 0);
+        for (int s = 0; s < KS; ++s) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[s], kf[s], sc, 0, 0, 0);
 #pragma unroll
-        for (int s = 0; s < KS; ++s)
-            dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                *reinterpret_cast<const bf16x8 *>(tb.o + rbo[s & 1] + 32 * s), vf[s], dp, 0, 0, 0);
-        // per-query terms of this lane's queries 8i + 4g + jj
+        for (int s = 0; s < KS; ++s) dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(oa[s], vf[s], dp, 0, 0, 0);
+        // logits (log2 units) of this lane's queries 8i + 4g + jj, slot 4i + jj
+        float dl2[16];
+        bool cut[16];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const f32x4 b4 = *reinterpret_cast<const f32x4 *>(tb.bias + 32 * blk + 8 * i + 4 * g);
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int e = 4 * i + jj;
+                cut[e] = false;
+                if constexpr (CLAMP) {
+                    const float dl = fminf(fmaxf(sc[e] * p.scale + b4[jj], -p.clamp), p.clamp);
+                    cut[e] = fabsf(dl) >= p.clamp;
+                    dl2[e] = dl * kLog2e;
+                } else {
+                    dl2[e] = __builtin_fmaf(sc[e], c2, b4[jj] * kLog2e);
+                }
+            }
+        }
+        // Edge blocks: entries outside the working set get -inf, by
+        // branch-free tests on d = t - j (window, or the partner offset of
+        // this stream) and on the held query range.
+        if (edge) {
+            const int tb0 = t0b + 4 * g;
+            const int ptgt = (BIDIR && kind == 2) ? -pi : pi;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int t = tb0 + 8 * (e >> 2) + (e & 3), d = t - j;
+                const bool in_w = BIDIR ? (d <= kw) & (d >= -kw) : (d >= 0) & (d <= kw);
+                const bool in_p = d == ptgt;
+                bool ok = ((partner & in_p) | (!partner & in_w)) & (t < QE) & j_ok;
+                if constexpr (BIDIR) ok = ok & (t >= QS);
+                dl2[e] = ok ? dl2[e] : -INFINITY;
+            }
+        }
         float pr[16], ds[16];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int qi = 32 * blk + 8 * i + 4 * g;
             const f32x4 l4 = *reinterpret_cast<const f32x4 *>(tb.lse2 + qi);
             const f32x4 r4 = *reinterpret_cast<const f32x4 *>(tb.r + qi);
-            const f32x4 b4 = *reinterpret_cast<const f32x4 *>(tb.bias + qi);
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
                 const int e = 4 * i + jj;
-                float delta2;
-                bool cut = false;
-                if constexpr (CLAMP) {
-                    const float dl = fminf(fmaxf(sc[e] * p.scale + b4[jj], -p.clamp), p.clamp);
-                    cut = fabsf(dl) >= p.clamp;
-                    delta2 = dl * kLog2e;
-                } else {
-                    delta2 = __builtin_fmaf(sc[e], c2, b4[jj] * kLog2e);
-                }
-                if (edge) {
-                    const int t = t0b + 8 * i + 4 * g + jj;
-                    bool ok;
-                    if constexpr (BIDIR) {
-                        const bool is_par = kind == 2 ? j - t == pi : t - j == pi;
-                        ok = (partner ? is_par : t - j <= kw && j - t <= kw) && t >= QS && t < QE && j_ok;
-                    } else {
-                        ok = partner ? (t - j == pi && t < QE && j_ok) : (t >= j && t - j <= kw && t < QE && j_ok);
-                    }
-                    if (!ok) delta2 = -INFINITY;
-                }
-                const float wgt = __builtin_amdgcn_exp2f(delta2 - l4[jj]);
+                const float wgt = __builtin_amdgcn_exp2f(dl2[e] - l4[jj]);
                 pr[e] = wgt;
-                ds[e] = cut ? 0.0f : wgt * (dp[e] - r4[jj]);
+                ds[e] = cut[e] ? 0.0f : wgt * (dp[e] - r4[jj]);
             }
         }
         bf16x8 pb[2], db8[2];
