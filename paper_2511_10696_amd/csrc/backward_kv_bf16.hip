@@ -71,7 +71,8 @@ template <int D>
 struct Stage {
     uint4 q[Tile<D>::CH];
     uint4 o[Tile<D>::CH];
-    float lse2, r, bias;
+    float gl, lse, r;   // raw per-row values: gate logit, lse, row term
+    bool band;          // a window-band row (else a partner-run row)
 };
 
 // LDS layout of the Q and dL/dy tiles: rows padded by 64 bytes, and the low
@@ -185,14 +186,16 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
             st.q[u] = ok ? qv : make_uint4(0, 0, 0, 0);
             st.o[u] = ok ? ov : make_uint4(0, 0, 0, 0);
         }
+        // Only loads here: the values derived from them are formed in store,
+        // after the tile's blocks, so that no wavefront waits for this
+        // tile's loads before it consumes the current one.
         if (tid < TQ) {
             const int t = q0m + tid;
             const int tc = (t >= QS && t < lim) ? t : tfirst;
-            const FusionBias fb = fusion_bias(p.gate[b * p.gsb + h * p.gsh + (tc - QS) * p.gsn], exact);
-            st.lse2 = (bp.lse[rbase + tc] - fb.lse_shift) * kLog2e;
+            st.gl = p.gate[b * p.gsb + h * p.gsh + (tc - QS) * p.gsn];
+            st.lse = bp.lse[rbase + tc];
             st.r = bp.rowterm[rbase + tc];
-            const float bias_local = fb.local, bias_partner = fb.partner;
-            st.bias = m < nband ? bias_local : bias_partner;
+            st.band = m < nband;
         }
     };
     auto store = [&](const Stage<D> &st, QTile<D> &tb) {
@@ -204,9 +207,11 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
             *reinterpret_cast<uint4 *>(tb.o + row * T::ROW + (pc ^ chunk_x(row)) * 16) = st.o[u];
         }
         if (tid < TQ) {
-            tb.lse2[tid] = st.lse2;
+            const FusionBias fb = fusion_bias(st.gl, exact);
+            tb.lse2[tid] = (st.lse - fb.lse_shift) * kLog2e;
             tb.r[tid] = st.r;
-            tb.bias[tid] = st.bias;
+            const float bias_local = fb.local, bias_partner = fb.partner;
+            tb.bias[tid] = st.band ? bias_local : bias_partner;
         }
     };
 
