@@ -307,9 +307,9 @@ def pmc_probe(W, pa, torch, dev):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
-              "(the operator shards over (b, h) with no communication; see the design notes)",
-              file=sys.stderr)
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: a multi-GPU run of this "
+              "operator is one process per GPU over its own (b, h) slice (no communication) or its own "
+              "sequence shard, so one GPU's throughput is the measured figure", file=sys.stderr)
         sys.exit(2)
     import torch
 
