@@ -29,6 +29,7 @@ the forward, inputs resident in HBM.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -79,6 +80,8 @@ def parse():
     ap.add_argument("--no-bidirectional", action="store_true")
     ap.add_argument("--no-smallk", action="store_true")
     ap.add_argument("--no-shard", action="store_true")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the fwd32k dense-causal and local-only comparisons and the fwd4k/fwd16k forwards")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pmc-probe", action="store_true",
                     help="run 3 launches of each timed kernel (forward, bidirectional forward, backward "
@@ -353,8 +356,40 @@ def main():
                  "query_positions_per_s": round(cfg.B * cfg.N / (bms / 1e3), 1),
                  "attended_keys_per_s": round(bkeys / (bms / 1e3), 1),
                  "roofline": brl, "roofline_mfma": bmf}
+    # ---- at the same shape: dense causal attention (k = N - 1) and the
+    # local window alone (pi = 0, no partner) -----------------------------------
+    variants = None
+    if not args.no_variants:
+        variants = {}
+        for name, kk, pp, steps in (("dense_causal", cfg.N - 1, 0, 5), ("local_only", cfg.k, 0, args.steps)):
+            vcfg = dataclasses.replace(cfg, name=name, k=kk, pi=pp)
+            vms, _, _ = time_launches(torch, lambda: pa.pi_attn_forward(q, k, v, gate, kk, pp, out=out), steps,
+                                      1, stream)
+            vkeys, vflops, vbytes = forward_algorithmic(vcfg)
+            vrl, vmf = roofline_of(vflops, vbytes, vms / 1e3, "forward_bf16_kernel<128,false,false,false>")
+            variants[name] = {"workload": f"fwd32k shape, causal, k={kk} pi={pp}", "steps": steps,
+                              "ms_per_step": round(vms, 5),
+                              "query_positions_per_s": round(cfg.B * cfg.N / (vms / 1e3), 1),
+                              "attended_keys_per_s": round(vkeys / (vms / 1e3), 1),
+                              "roofline": vrl, "roofline_mfma": vmf}
     del q, k, v, out
     torch.cuda.empty_cache()
+    if variants is not None:
+        for cname in ("fwd4k", "fwd16k"):
+            ccfg = W.FORWARD[cname]
+            cq, ck, cv, cg = W.forward_inputs(ccfg, 0, dev)
+            cout = torch.empty_like(cq)
+            cms, _, _ = time_launches(torch, lambda: pa.pi_attn_forward(cq, ck, cv, cg, ccfg.k, ccfg.pi, out=cout),
+                                      args.steps, args.warmup, stream)
+            ckeys, cflops, cbytes = forward_algorithmic(ccfg)
+            crl, cmf = roofline_of(cflops, cbytes, cms / 1e3, f"forward_bf16_kernel<{ccfg.D},false,false,false>")
+            variants[cname] = {"workload": f"{cname}: causal B{ccfg.B} H{ccfg.H} N{ccfg.N} D{ccfg.D} k{ccfg.k} "
+                                           f"pi{ccfg.pi} bf16", "steps": args.steps, "ms_per_step": round(cms, 5),
+                               "query_positions_per_s": round(ccfg.B * ccfg.N / (cms / 1e3), 1),
+                               "attended_keys_per_s": round(ckeys / (cms / 1e3), 1),
+                               "roofline": crl, "roofline_mfma": cmf}
+            del cq, ck, cv, cg, cout
+            torch.cuda.empty_cache()
 
     # ---- small window (the paper's default k = 4, pi = 16) -------------------
     smallk = None
@@ -457,6 +492,7 @@ def main():
                          "last-level cache; the headline value is the steady-state (hot) loop"},
         "device": device_info(torch, dev),
         "bidirectional": bidir,
+        "variants": variants,
         "smallk": smallk,
         "sequence_shard": shard,
         "decode": decode,
