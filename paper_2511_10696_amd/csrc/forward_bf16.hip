@@ -265,8 +265,10 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
     const int kend = min(BIDIR ? (int)min((int64_t)t0 + BM + kw, (int64_t)NS) : min(t0 + BM, NQ), p.kvend);
     const int ntiles = (kend - kb0 + TK - 1) / TK;
     // ---- prologue: every load is issued before any is waited for ----------
-    // (the first tile, the query fragments, the gate logit and the partner
-    // key/value rows), so the prologue costs one memory round trip.
+    // (the query fragments, the gate logit, the partner key/value rows, then
+    // the first tile), so the prologue costs one memory round trip; loads
+    // complete in issue order, so the partner scoring starts while the first
+    // tile is still in flight.
     // Buffer descriptors over rows [kb0, kend) of this head's keys and values
     // (word 3 is the gfx9 raw-buffer format: 32-bit data, range checked).
     const int rowb = (int)(2 * ksn);
@@ -276,8 +278,6 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
         __builtin_amdgcn_make_buffer_rsrc((void *)(vp + (int64_t)kb0 * ksn), (short)0, (kend - kb0) * rowb, 0x00020000);
     Stage<D> st;
     Stage<D> st0[BPT];
-#pragma unroll
-    for (int hf = 0; hf < BPT; ++hf) tile_load<D>(st0[hf], rk, rv, rowb, 0, hf, tid);
 
     // Loads use a clamped, always-readable row; lanes without a query or a
     // partner zero the data afterwards.
@@ -321,6 +321,8 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
             for (int i = 0; i < 4; ++i)
                 vfraw[db][i] = *reinterpret_cast<const uint2 *>(vp + frc * ksn + 32 * db + 8 * i + 4 * g);
     }
+#pragma unroll
+    for (int hf = 0; hf < BPT; ++hf) tile_load<D>(st0[hf], rk, rv, rowb, 0, hf, tid);
 #pragma unroll
     for (int s = 0; s < W::KS; ++s) ws.qf[s] = t_ok ? qraw[s] : bf16x8{};
 
