@@ -164,8 +164,9 @@ int pi_attn_forward_gated(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_
  *   S, H, D      sequences, heads, head dimension; cap = cache rows.
  *   len_in       device int32 [S]: current lengths (0 <= len_in[s] < cap).
  *   len_out      optional device int32 [S] (NULL to skip): receives
- *                len_in[s] + 1.  Must not alias len_in (other work-groups
- *                of the same step still read it).
+ *                len_in[s] + 1.  Must not overlap len_in (other work-groups
+ *                of the same step still read it): EINVAL if the two
+ *                S-element ranges share a byte.
  *   q_new, k_new, v_new   device [S][H][D] contiguous.
  *   k_cache, v_cache      device [S][H][cap][D] contiguous; row len_in[s]
  *                of every head is overwritten, nothing else is written.

@@ -468,6 +468,13 @@ def pi_attn_decode_step(len_in, q_new, k_new, v_new, k_cache, v_cache, gate, k: 
         raise ValueError("decode gate must be [H] or [S, H]")
     if out is None:
         out = torch.empty_like(q_new)
+    if tuple(out.shape) != (S, H, D) or out.dtype != k_cache.dtype or not out.is_contiguous():
+        raise ValueError("out must be a contiguous [S, H, D] tensor of the cache dtype")
+    if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (S, H) or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous float32 [S, H] tensor")
+    if len_out is not None and (len_out.dtype != torch.int32 or tuple(len_out.shape) != (S,)
+                                or not len_out.is_contiguous()):
+        raise ValueError("len_out must be a contiguous int32 [S] tensor")
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     st = library().pi_attn_decode_step(

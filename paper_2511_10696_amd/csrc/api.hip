@@ -207,7 +207,11 @@ int pi_attn_decode_step(int32_t dtype, int32_t S, int32_t H, int32_t D, int32_t 
     if (n >= kMaxRows) return PI_ATTN_EINVAL;
     if (n == 0) return PI_ATTN_OK;
     if (!len_in || !q_new || !k_new || !v_new || !k_cache || !v_cache || !gate || !out) return PI_ATTN_EINVAL;
-    if ((const void *)len_out == (const void *)len_in) return PI_ATTN_EINVAL;
+    if (len_out) {   // len_out must not overlap len_in: other work-groups of the step still read it
+        const uintptr_t a = reinterpret_cast<uintptr_t>(len_in), b = reinterpret_cast<uintptr_t>(len_out);
+        const uintptr_t bytes = (uintptr_t)S * sizeof(int32_t);
+        if (a < b + bytes && b < a + bytes) return PI_ATTN_EINVAL;
+    }
     if (!aligned4(len_in) || (len_out && !aligned4(len_out))) return PI_ATTN_EINVAL;
     if (!aligned16(q_new) || !aligned16(k_new) || !aligned16(v_new) || !aligned16(k_cache) ||
         !aligned16(v_cache) || !aligned16(out))

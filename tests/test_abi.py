@@ -286,6 +286,7 @@ def dec(lib, **kw):
 @pytest.mark.parametrize("kw,code", [
     (dict(dtype=3), EUNSUP), (dict(D=32), EUNSUP), (dict(S=-1), EINVAL), (dict(cap=0), EINVAL),
     (dict(k=-1), EINVAL), (dict(len_in=None), EINVAL), (dict(len_out=64), EINVAL), (dict(len_in=66), EINVAL),
+    (dict(len_out=68), EINVAL), (dict(len_out=60), EINVAL),    # partial overlaps of the two [S] ranges
     (dict(q=None), EINVAL), (dict(kc=None), EINVAL), (dict(vc=8), EINVAL), (dict(out=4), EINVAL),
     (dict(gate=None), EINVAL), (dict(gsh=-1), EINVAL), (dict(scale=0.0), EINVAL), (dict(lse=1), EINVAL),
 ])

@@ -12,7 +12,7 @@ import oracle
 import paper_2511_10696_amd as pa
 from paper_2511_10696_amd import workloads as W
 from tests.oracle_pins import BIDIR_IDX_CASES
-from tests.test_gpu_backward import assert_grad
+from tests.grad_check import check_backward
 from tests.test_gpu_parity import LSE_TOL, assert_close, np32
 
 pytestmark = pytest.mark.gpu
@@ -180,15 +180,7 @@ def test_forward_deterministic(device, dtype):
 # backward
 # ---------------------------------------------------------------------------
 def run_backward_case(q, k, v, gate, kw, pi, seed, clamp=0.0, scale=None):
-    out, lse = pa.pi_attn_forward(q, k, v, gate, kw, pi, return_lse=True, logit_clamp=clamp, scale=scale,
-                                  causal=False)
-    dout = W.cotangent(q.shape, q.dtype, seed, q.device)
-    dq, dk, dv, dg = pa.pi_attn_backward(q, k, v, gate, kw, pi, out, lse, dout, logit_clamp=clamp, scale=scale,
-                                         gate_grad_per_query=True, causal=False)
-    torch.cuda.synchronize()
-    rq, rk, rv, rg = oracle.backward(q, k, v, gate, kw, pi, dout, scale=scale, clamp=clamp, causal=False)
-    for name, got, ref in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv), ("dgate", dg, rg)):
-        assert_grad(np32(got), ref, name, q.dtype)
+    check_backward(q, k, v, gate, kw, pi, seed, causal=False, clamp=clamp, scale=scale)
 
 
 @pytest.mark.parametrize("seed", [0, 1])

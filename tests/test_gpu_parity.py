@@ -308,32 +308,60 @@ def test_decode_length_out_of_range(device, dtype):
     assert len_out.cpu().tolist() == [6, cap, -1, 8]
 
 
-def test_decode_config_sampled(device):
+def test_decode_config(device):
     """The decode workload (64 sequences, 32 heads, 32768 cached rows, k=512,
-    pi=1024): 1000 consecutive steps, checked on sampled steps and heads."""
+    pi=1024): 1000 consecutive steps.  Every appended cache row equals its
+    token bit for bit; at steps 0, 1, 499 and 999 every (s, h) pair, and at
+    16 seeded steps 64 seeded pairs, against the oracle.  The oracle's cache
+    for step i holds only rows [t - pi, t] (t = 32768 + i, all its working
+    set can reach), built from the seeded initial cache and the seeded
+    tokens of the earlier steps, never from the caches the kernel wrote."""
     cfg = W.DECODE["decode"]
     kc, vc, lens, gate = W.decode_state(cfg, 0, device)
     qs, ks, vs = W.decode_tokens(cfg, cfg.steps, 1, device)
+    L0, P = cfg.cache_len, cfg.pi
+    assert cfg.steps <= P    # every step's reach [t - pi, t) starts inside the initial cache
+    k0 = kc[:, :, L0 - P:L0].float().cpu().numpy()    # initial rows [L0 - pi, L0), fp32 (exact)
+    v0 = vc[:, :, L0 - P:L0].float().cpu().numpy()
     len_buf = [lens, torch.empty_like(lens)]
     rng = np.random.default_rng(3)
-    check_steps = sorted(set([0, 1, 499, cfg.steps - 1] + rng.choice(cfg.steps, 16, replace=False).tolist()))
+    full_steps = [0, 1, 499, cfg.steps - 1]
+    some_steps = sorted(set(rng.choice(cfg.steps, 16, replace=False).tolist()) - set(full_steps))
     outs = {}
     for step in range(cfg.steps):
         out = pa.pi_attn_decode_step(len_buf[step % 2], qs[step], ks[step], vs[step], kc, vc, gate,
                                      cfg.k, cfg.pi, len_out=len_buf[(step + 1) % 2])
-        if step in check_steps:
+        if step in full_steps or step in some_steps:
             outs[step] = out.clone()
     torch.cuda.synchronize()
-    assert (len_buf[cfg.steps % 2] == cfg.cache_len + cfg.steps).all()
-    pairs = [(int(s), int(h)) for s, h in zip(rng.choice(cfg.S, 6), rng.choice(cfg.H, 6))]
-    for s, h in pairs:
-        # rows < t of the final caches are exactly the rows present before step t
-        kslice = np32(kc[s:s + 1, h:h + 1])
-        vslice = np32(vc[s:s + 1, h:h + 1])
-        for step in check_steps:
-            t = cfg.cache_len + step
-            assert torch.equal(kc[s, h, t], ks[step, s, h]) and torch.equal(vc[s, h, t], vs[step, s, h])
-            ref = oracle.decode_step(np.array([t], np.int32), qs[step, s:s + 1, h:h + 1],
+    assert (len_buf[cfg.steps % 2] == L0 + cfg.steps).all()
+    assert torch.equal(kc[:, :, L0:L0 + cfg.steps], ks.permute(1, 2, 0, 3))
+    assert torch.equal(vc[:, :, L0:L0 + cfg.steps], vs.permute(1, 2, 0, 3))
+    ks_h, vs_h = ks.float().cpu().numpy(), vs.float().cpu().numpy()    # [steps, S, H, D]
+
+    def reach(step, s_idx, h_idx):
+        """Cache rows [t - pi, t) of the listed pairs as the step saw them:
+        [S', H', pi + 1, D], the last row left for the oracle's own write."""
+        a = P - step
+        kk = np.empty((len(s_idx), len(h_idx), P + 1, cfg.D), np.float32)
+        vv = np.empty_like(kk)
+        kk[:, :, :a] = k0[np.ix_(s_idx, h_idx)][:, :, step:]
+        vv[:, :, :a] = v0[np.ix_(s_idx, h_idx)][:, :, step:]
+        kk[:, :, a:P] = ks_h[:step][:, s_idx][:, :, h_idx].transpose(1, 2, 0, 3)
+        vv[:, :, a:P] = vs_h[:step][:, s_idx][:, :, h_idx].transpose(1, 2, 0, 3)
+        return kk, vv
+
+    all_s, all_h = np.arange(cfg.S), np.arange(cfg.H)
+    for step in full_steps:
+        kk, vv = reach(step, all_s, all_h)
+        t_rel = np.full(cfg.S, P, np.int32)   # t sits at row pi of the reach
+        ref = oracle.decode_step(t_rel, qs[step], ks[step], vs[step], kk, vv, gate, cfg.k, cfg.pi)
+        assert_close(np32(outs[step]), ref, torch.bfloat16, f"step {step}, all pairs")
+    for step in some_steps:
+        for s, h in zip(rng.choice(cfg.S, 64), rng.choice(cfg.H, 64)):
+            s, h = int(s), int(h)
+            kk, vv = reach(step, [s], [h])
+            ref = oracle.decode_step(np.array([P], np.int32), qs[step, s:s + 1, h:h + 1],
                                      ks[step, s:s + 1, h:h + 1], vs[step, s:s + 1, h:h + 1],
-                                     kslice, vslice, gate[h:h + 1], cfg.k, cfg.pi)
+                                     kk, vv, gate[h:h + 1], cfg.k, cfg.pi)
             assert_close(np32(outs[step][s:s + 1, h:h + 1]), ref, torch.bfloat16, f"step {step} s{s} h{h}")

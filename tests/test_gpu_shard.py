@@ -173,18 +173,18 @@ def test_backward_shards_are_bit_identical(device, B, H, N, D, kw, pi, nshard, c
 
 @pytest.mark.parametrize("causal", [True, False])
 def test_backward_unaligned_shards_against_the_oracle(device, causal):
-    from tests.test_gpu_backward import assert_grad
+    from tests.grad_check import assert_grad, expected_grads, forward_state
     B, H, N, D, kw, pi = 1, 2, 700, 64, 40, 130
     cfg = W.ForwardConfig("custom", B, H, N, D, kw, pi, torch.bfloat16)
     q, k, v, gate = W.forward_inputs(cfg, 7, device, per_query_gate=True)
-    out, lse = pa.pi_attn_forward(q, k, v, gate, kw, pi, return_lse=True, causal=causal)
+    out, lse, y = forward_state(q, k, v, gate, kw, pi, causal=causal)
     dout = W.cotangent(q.shape, q.dtype, 7, device)
     bounds = [(0, 100), (100, 101), (101, 450), (450, 700)]
     got = sharded_backward(q, k, v, gate, kw, pi, out, lse, dout, bounds, causal, True)
     torch.cuda.synchronize()
-    refs = oracle.backward(q, k, v, gate, kw, pi, dout, causal=causal)
-    for name, a, ref in zip(("dq", "dk", "dv", "dgate"), got, refs):
-        assert_grad(np32(a), ref, name, torch.bfloat16)
+    exp = expected_grads(q, k, v, gate, kw, pi, dout, out, y, causal=causal, row_term_from_out=True)
+    for name, a, e in zip(("dq", "dk", "dv", "dgate"), got, exp):
+        assert_grad(np32(a), e, name, torch.bfloat16)
 
 
 @pytest.mark.parametrize("causal", [True, False])

@@ -172,16 +172,19 @@ def test_gated_config_smallk8k(device):
 
 
 def test_gated_logits_feed_the_backward(device):
-    """The gate logits the gated forward writes are the per-query gate of
-    pi_attn_backward: gradients against the oracle on the same logits."""
-    from tests.test_gpu_backward import assert_grad
+    """The gate logits the gated forward writes are laid out as the per-query
+    gate of pi_attn_backward: they match the oracle's logits, and the
+    backward on those logits (rounded to float32 by the oracle side) meets
+    the gradient bar."""
+    from tests.grad_check import check_backward
     cfg = W.ForwardConfig("custom", 1, 2, 200, 64, 4, 16, torch.bfloat16)
     q, k, v, _ = W.forward_inputs(cfg, 6, device)
     u, w2, b2 = W.gate_mlp_inputs(cfg, 6, device)
-    out, g, lse = pa.pi_attn_forward_gated(q, k, v, u, w2, b2, 4, 16, return_lse=True)
-    dout = W.cotangent(q.shape, q.dtype, 6, device)
-    dq, dk, dv, dg = pa.pi_attn_backward(q, k, v, g, 4, 16, out, lse, dout)
+    _, g = pa.pi_attn_forward_gated(q, k, v, u, w2, b2, 4, 16)
     torch.cuda.synchronize()
-    rq, rk, rv, rg = oracle.backward(q, k, v, g, 4, 16, dout)
-    for name, got, ref in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv), ("dgate", dg, rg)):
-        assert_grad(np32(got), ref, name, q.dtype)
+    gref = oracle.gate_logits(u, w2, b2)
+    assert g.shape == gref.shape and g.is_contiguous()
+    bound = 1e-5 * (np.abs(np32(u)) @ np.abs(np32(w2)).T).transpose(0, 2, 1) + 1e-6
+    assert (np.abs(np32(g) - gref) <= bound).all()
+    gate = torch.from_numpy(gref.astype(np.float32)).to(device)
+    check_backward(q, k, v, gate, 4, 16, 6)

@@ -17,7 +17,7 @@ import torch
 import oracle
 import paper_2511_10696_amd as pa
 from paper_2511_10696_amd import workloads as W
-from tests.test_gpu_backward import assert_grad, np32
+from tests.grad_check import check_backward, forward_state, np32
 
 pytestmark = pytest.mark.gpu
 
@@ -25,20 +25,12 @@ TIGHT_RELL2 = 2e-3
 
 
 def run_case(q, k, v, gate, kw, pi, seed, causal, clamp=0.0, scale=None, tight=True):
-    out, lse = pa.pi_attn_forward(q, k, v, gate, kw, pi, return_lse=True, logit_clamp=clamp, scale=scale,
-                                  causal=causal)
-    dout = W.cotangent(q.shape, q.dtype, seed, q.device)
-    dq, dk, dv, dg = pa.pi_attn_backward(q, k, v, gate, kw, pi, out, lse, dout, logit_clamp=clamp, scale=scale,
-                                         gate_grad_per_query=True, causal=causal)
-    torch.cuda.synchronize()
-    refs = oracle.backward(q, k, v, gate, kw, pi, dout, scale=scale, clamp=clamp, causal=causal)
-    for name, got, ref in zip(("dq", "dk", "dv", "dgate"), (dq, dk, dv, dg), refs):
-        g = np32(got)
-        assert_grad(g, ref, name, q.dtype)
+    def tight_bar(name, g, ref):
         if tight:
             nr, ne = np.linalg.norm(ref), float(np.linalg.norm(g - ref))
             assert ne <= TIGHT_RELL2 * nr + 1e-5 * np.sqrt(ref.size), f"{name}: rel-L2 {ne / max(nr, 1e-300):.3g}"
-    return dq, dk, dv, dg
+    return check_backward(q, k, v, gate, kw, pi, seed, causal=causal, clamp=clamp, scale=scale, per_head_sum=False,
+                          extra=tight_bar)
 
 
 def inputs(B, H, N, D, seed, per_query_gate=False):
@@ -85,7 +77,7 @@ def test_backward_per_head_gate_sum(device, causal):
     oracle's per-query gradient summed, within the bf16 factor of the summed
     magnitudes."""
     q, k, v, gate = inputs(2, 3, 400, 64, 5)
-    out, lse = pa.pi_attn_forward(q, k, v, gate, 4, 16, return_lse=True, causal=causal)
+    out, lse, _ = forward_state(q, k, v, gate, 4, 16, causal=causal)
     dout = W.cotangent(q.shape, q.dtype, 5, device)
     *_, dgh = pa.pi_attn_backward(q, k, v, gate, 4, 16, out, lse, dout, causal=causal)
     torch.cuda.synchronize()

@@ -13,7 +13,7 @@ import torch
 import oracle
 import paper_2511_10696_amd as pa
 from paper_2511_10696_amd import workloads as W
-from tests.test_gpu_backward import assert_grad
+from tests.grad_check import assert_grad, check_backward, expected_grads, forward_state
 from tests.test_gpu_parity import LSE_TOL, assert_close, np32
 from tests.test_gpu_shard import run_shards, sharded_backward
 
@@ -60,14 +60,7 @@ def test_backward_sweep(device, c):
         pytest.skip("the clamp's gradient cut is a discontinuity; clamp cases are placed by hand elsewhere")
     cfg = W.ForwardConfig("custom", c["B"], c["H"], c["N"], c["D"], c["k"], c["pi"], torch.bfloat16)
     q, k, v, gate = W.forward_inputs(cfg, c["seed"], device, per_query_gate=c["pq"])
-    out, lse = pa.pi_attn_forward(q, k, v, gate, c["k"], c["pi"], return_lse=True, causal=c["causal"])
-    dout = W.cotangent(q.shape, q.dtype, c["seed"], device)
-    grads = pa.pi_attn_backward(q, k, v, gate, c["k"], c["pi"], out, lse, dout, gate_grad_per_query=True,
-                                causal=c["causal"])
-    torch.cuda.synchronize()
-    refs = oracle.backward(q, k, v, gate, c["k"], c["pi"], dout, causal=c["causal"])
-    for name, got, ref in zip(("dq", "dk", "dv", "dgate"), grads, refs):
-        assert_grad(np32(got), ref, f"{name} {ident(c)}", torch.bfloat16)
+    check_backward(q, k, v, gate, c["k"], c["pi"], c["seed"], causal=c["causal"], per_head_sum=False)
 
 
 @pytest.mark.parametrize("c", CASES, ids=ident)
@@ -121,8 +114,8 @@ def test_shard_sweep(device, c):
     full, lfull = pa.pi_attn_forward(q, k, v, gate, kw, pi, return_lse=True, causal=causal)
     out, lse = run_shards(q, k, v, gate, kw, pi, c["bounds"], causal, pq)
     dout = W.cotangent(q.shape, q.dtype, c["seed"], device)
-    got = sharded_backward(q, k, v, gate, kw, pi, full, lfull, dout, c["bounds"], causal, pq)
     if c["aligned"]:
+        got = sharded_backward(q, k, v, gate, kw, pi, full, lfull, dout, c["bounds"], causal, pq)
         whole = pa.pi_attn_backward(q, k, v, gate, kw, pi, full, lfull, dout, gate_grad_per_query=True,
                                     causal=causal)
         torch.cuda.synchronize()
@@ -134,9 +127,13 @@ def test_shard_sweep(device, c):
     ref, lref = oracle.forward(q, k, v, gate, kw, pi, want_lse=True, causal=causal)
     assert_close(np32(out), ref, torch.bfloat16, shard_ident(c))
     assert np.abs(np32(lse) - lref).max() <= LSE_TOL
-    refs = oracle.backward(q, k, v, gate, kw, pi, dout, causal=causal)
-    for name, a, r in zip(("dq", "dk", "dv", "dgate"), got, refs):
-        assert_grad(np32(a), r, f"{name} {shard_ident(c)}", torch.bfloat16)
+    # the gradients on the oracle's forward state
+    ostate, lstate, y = forward_state(q, k, v, gate, kw, pi, causal=causal)
+    got = sharded_backward(q, k, v, gate, kw, pi, ostate, lstate, dout, c["bounds"], causal, pq)
+    torch.cuda.synchronize()
+    exp = expected_grads(q, k, v, gate, kw, pi, dout, ostate, y, causal=causal, row_term_from_out=True)
+    for name, a, e in zip(("dq", "dk", "dv", "dgate"), got, exp):
+        assert_grad(np32(a), e, f"{name} {shard_ident(c)}", torch.bfloat16)
 
 
 # ---------------------------------------------------------------------------
