@@ -54,7 +54,8 @@ enum {
     PI_ATTN_OK = 0,
     PI_ATTN_EINVAL = -1,       /* null pointer, negative size, bad stride or alignment */
     PI_ATTN_EUNSUPPORTED = -2, /* valid request outside what is built (D, dtype)       */
-    PI_ATTN_EHIP = -3          /* the HIP runtime refused a launch                      */
+    PI_ATTN_EHIP = -3,         /* the HIP runtime refused a launch                      */
+    PI_ATTN_ESCRATCH = -4      /* too large for pi_attn_backward_noalloc's fixed array  */
 };
 
 /* Human-readable text for a status code (static storage, never NULL). */
@@ -226,6 +227,35 @@ int pi_attn_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D,
                      const void *dout, int64_t osb, int64_t osh, int64_t osn,
                      float *dq, float *dk, float *dv, float *dgate, float *rowterm,
                      void *stream);
+
+/*
+ * pi_attn_backward_noalloc -- pi_attn_backward for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving or
+ * training loops, harnesses that forbid hipMalloc): the same arguments,
+ * kernels and results without the rowterm workspace.  The row terms go to
+ * a fixed array of 4194304 float32 (16 MiB) that the library holds on every
+ * device it runs on until the process ends; the call uses the current
+ * device's array (hipGetDevice), so the buffers and the stream must be on
+ * that device.  It calls no allocating routine.
+ *   Arguments    as pi_attn_backward, without rowterm.
+ *   Results      bit-identical to pi_attn_backward's on the same inputs.
+ *   Sharing      every call on one device uses that device's array: calls
+ *                that overlap in time on one device (different streams,
+ *                threads without ordering) race on it and must be ordered by
+ *                the caller; calls in order on one stream are safe.  Each call
+ *                writes every row term it reads, so stale contents from an
+ *                earlier call never matter.
+ * Errors: as pi_attn_backward; ESCRATCH when B*H*N > 4194304 (nothing is
+ * enqueued); EHIP if the array's address cannot be obtained.
+ */
+int pi_attn_backward_noalloc(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D,
+                             int32_t k, int32_t pi, int32_t causal,
+                             const void *q, const void *kk, const void *v,
+                             int64_t sb, int64_t sh, int64_t sn,
+                             const float *gate, int64_t gsb, int64_t gsh, int64_t gsn,
+                             float scale, float logit_clamp, const float *lse, const void *out,
+                             const void *dout, int64_t osb, int64_t osh, int64_t osn,
+                             float *dq, float *dk, float *dv, float *dgate, void *stream);
 
 /*
  * pi_attn_forward_shard -- pi_attn_forward over one shard of a sequence:

@@ -21,6 +21,7 @@ import os
 import threading
 
 __all__ = ["pi_attn_index_set", "pi_attn_forward", "pi_attn_forward_gated", "pi_attn_backward",
+           "pi_attn_backward_noalloc",
            "pi_attn_decode_step", "pi_attn_ws_width",
            "pi_attn_forward_shard", "pi_attn_backward_shard_q", "pi_attn_backward_shard_kv",
            "pi_attn_strerror", "library", "LIB_PATH", "EXPORTED_SYMBOLS", "PiAttnError"]
@@ -29,7 +30,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpi_attn.
 EXPORTED_SYMBOLS = ("pi_attn_strerror", "pi_attn_ws_width", "pi_attn_index_set",
                     "pi_attn_forward", "pi_attn_forward_gated", "pi_attn_decode_step", "pi_attn_backward",
                     "pi_attn_gate_grad_per_head", "pi_attn_forward_shard", "pi_attn_backward_shard_q",
-                    "pi_attn_backward_shard_kv")
+                    "pi_attn_backward_shard_kv", "pi_attn_backward_noalloc")
 
 PI_ATTN_F32, PI_ATTN_BF16 = 0, 1
 
@@ -71,6 +72,10 @@ def library() -> ctypes.CDLL:
                                                          f32, f32, vp, vp, vp, i64, i64, i64,
                                                          vp, vp, vp, vp, vp, vp])
             lib.pi_attn_backward.restype = ctypes.c_int
+            lib.pi_attn_backward_noalloc.argtypes = ([i32] * 8 + [vp, vp, vp, i64, i64, i64, vp, i64, i64, i64,
+                                                                 f32, f32, vp, vp, vp, i64, i64, i64,
+                                                                 vp, vp, vp, vp, vp])
+            lib.pi_attn_backward_noalloc.restype = ctypes.c_int
             lib.pi_attn_gate_grad_per_head.argtypes = [i32, i32, i32, vp, vp, vp]
             lib.pi_attn_gate_grad_per_head.restype = ctypes.c_int
             lib.pi_attn_forward_shard.argtypes = ([i32] * 12 + [vp, i64, i64, i64, vp, vp, i64, i64, i64,
@@ -439,6 +444,53 @@ def pi_attn_backward(q, k, v, gate, k_window: int, pi: int, out, lse, dout, scal
                "pi_attn_gate_grad_per_head")
         dg = dgh
     return dq, dk, dv, dg
+
+
+def pi_attn_backward_noalloc(q, k, v, gate, k_window: int, pi: int, out, lse, dout, dq, dk, dv, dgate,
+                             scale: float | None = None, logit_clamp: float = 0.0, stream=None,
+                             causal: bool = True):
+    """pi_attn_backward into caller-owned outputs with no workspace: the row
+    terms live in the library's fixed per-device array (B*H*N <= 4194304;
+    calls that overlap in time on one device race on it).  dq, dk, dv
+    [B, H, N, D] and dgate [B, H, N] (per query) are contiguous float32
+    tensors that the call overwrites; out and dout must share strides.
+    Nothing is allocated here or in the library."""
+    torch = _torch()
+    _require_cuda(q, k, v, gate, out, dout, lse, dq, dk, dv, dgate)
+    if (q.dim() != 4 or k.shape != q.shape or v.shape != q.shape or dout.shape != q.shape
+            or out.shape != q.shape):
+        raise ValueError("q, k, v, out, dout must share one [B, H, N, D] shape")
+    if k.dtype != q.dtype or v.dtype != q.dtype or dout.dtype != q.dtype or out.dtype != q.dtype:
+        raise TypeError("q, k, v, out, dout must share one dtype")
+    if out.stride() != dout.stride() or k.stride() != q.stride() or v.stride() != q.stride():
+        raise ValueError("q, k, v must share strides, and out and dout must share strides")
+    if q.stride(3) != 1 or dout.stride(3) != 1:
+        raise ValueError("the head dimension must be contiguous")
+    B, H, N, D = q.shape
+    if gate.dtype != torch.float32:
+        raise TypeError("gate logits must be float32")
+    if tuple(gate.shape) == (H,):
+        gs = (0, gate.stride(0), 0)
+    elif tuple(gate.shape) == (B, H, N):
+        gs = gate.stride()
+    else:
+        raise ValueError(f"gate must be [H] or [B, H, N], got {tuple(gate.shape)}")
+    if lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, N) or not lse.is_contiguous():
+        raise ValueError("lse must be the contiguous float32 [B, H, N] lse of the forward")
+    for name, t, shape in (("dq", dq, (B, H, N, D)), ("dk", dk, (B, H, N, D)), ("dv", dv, (B, H, N, D)),
+                           ("dgate", dgate, (B, H, N))):
+        if t.dtype != torch.float32 or tuple(t.shape) != shape or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous float32 {list(shape)} tensor")
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    st = library().pi_attn_backward_noalloc(
+        _dtype_code(q.dtype), B, H, N, D, int(k_window), int(pi), int(bool(causal)),
+        _ptr(q), _ptr(k), _ptr(v), q.stride(0), q.stride(1), q.stride(2),
+        _ptr(gate), gs[0], gs[1], gs[2], float(scale), float(logit_clamp), _ptr(lse),
+        _ptr(out), _ptr(dout), dout.stride(0), dout.stride(1), dout.stride(2),
+        _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dgate), _stream_handle(stream, q.device))
+    _check(st, "pi_attn_backward_noalloc")
+    return dq, dk, dv, dgate
 
 
 def pi_attn_decode_step(len_in, q_new, k_new, v_new, k_cache, v_cache, gate, k: int, pi: int,

@@ -2,6 +2,7 @@
 // Nothing here allocates; every launch goes on the caller's stream.
 #include <math.h>
 #include <algorithm>
+#include <mutex>
 #include <stdint.h>
 
 #include "../../include/pi_attn.h"
@@ -90,6 +91,32 @@ bool shard_positions_ok(int32_t nseq, int32_t p0, int32_t n0, int32_t p1, int32_
     return (int64_t)p0 + n0 <= nseq && (int64_t)p1 + n1 <= nseq;
 }
 
+// Row terms of pi_attn_backward_noalloc: one fixed array per device in
+// place of the caller's workspace.  Host code never uses its name as an
+// address; the device address comes from hipGetSymbolAddress.
+constexpr int64_t kScratchRows = (int64_t)1 << 22;   // float32 row terms: 16 MiB
+static __device__ __align__(256) float scratch[kScratchRows];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float *g_scratch[kMaxDevices];   // address of `scratch` on each device (null until looked up)
+
+// The address of the current device's copy of `scratch`, looked up on the
+// first call on that device (with it current) and kept.
+int scratch_of_current_device(float **ptr) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return PI_ATTN_EHIP;
+    if (dev < 0 || dev >= kMaxDevices) return PI_ATTN_EUNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void *addr = nullptr;
+        if (hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch)) != hipSuccess || !addr) return PI_ATTN_EHIP;
+        g_scratch[dev] = static_cast<float *>(addr);
+    }
+    *ptr = g_scratch[dev];
+    return PI_ATTN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -102,6 +129,8 @@ const char *pi_attn_strerror(int status) {
             return "unsupported configuration (head dimension must be 64 or 128; dtype f32/bf16; bf16: "
                    "(k + 256) rows of keys, (2k + 256) bidirectional, must span under 2 GiB)";
         case PI_ATTN_EHIP: return "HIP runtime refused the launch";
+        case PI_ATTN_ESCRATCH:
+            return "problem too large for the no-allocation backward's fixed row-term array (B*H*N > 4194304)";
         default: return "unknown status";
     }
 }
@@ -168,6 +197,38 @@ int pi_attn_forward_gated(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_
     return from_hip(dtype == PI_ATTN_BF16 ? launch_forward_bf16(p, st) : launch_forward_f32(p, st));
 }
 
+}  // extern "C"
+
+namespace {
+
+// Validation of pi_attn_backward's arguments other than the row-term
+// workspace; fills p on PI_ATTN_OK (empty: nothing to do).
+int prepare_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, int32_t k, int32_t pi,
+                     int32_t causal, const void *q, const void *kk, const void *v, int64_t sb, int64_t sh,
+                     int64_t sn, const float *gate, int64_t gsb, int64_t gsh, int64_t gsn, float scale,
+                     float logit_clamp, const float *lse, const void *out, const void *dout, int64_t osb, int64_t osh,
+                     int64_t osn, float *dq, float *dk, float *dv, float *dgate, BwdParams &p, bool &empty) {
+    FwdParams &f = p.f;
+    // out shares dout's strides; it stands in for the forward output in the shared checks
+    const int status = check_sequence(dtype, B, H, N, D, k, pi, causal, q, kk, v, sb, sh, sn, scale, logit_clamp,
+                                      out, osb, osh, osn, f, empty);
+    if (status != PI_ATTN_OK || empty) return status;
+    if (!gate || !lse || !dout || !dq || !dk || !dv || !dgate) return PI_ATTN_EINVAL;
+    if (!aligned16(dout) || !aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
+    if (!aligned4(lse) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv) || !aligned4(dgate))
+        return PI_ATTN_EINVAL;
+    f.gate = gate; f.gsb = gsb; f.gsh = gsh; f.gsn = gsn;
+    p.dtype = dtype == PI_ATTN_BF16 ? 1 : 0;
+    p.lse = lse;
+    p.out = out; p.dout = dout; p.osb = osb; p.osh = osh; p.osn = osn;
+    p.dq = dq; p.dk = dk; p.dv = dv; p.dgate = dgate;
+    return PI_ATTN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 int pi_attn_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, int32_t k, int32_t pi,
                      int32_t causal, const void *q, const void *kk, const void *v, int64_t sb, int64_t sh, int64_t sn,
                      const float *gate, int64_t gsb, int64_t gsh, int64_t gsn, float scale, float logit_clamp,
@@ -175,22 +236,31 @@ int pi_attn_backward(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, 
                      int64_t osn, float *dq,
                      float *dk, float *dv, float *dgate, float *rowterm, void *stream) {
     BwdParams p{};
-    FwdParams &f = p.f;
     bool empty;
-    // out shares dout's strides; it stands in for the forward output in the shared checks
-    const int status = check_sequence(dtype, B, H, N, D, k, pi, causal, q, kk, v, sb, sh, sn, scale, logit_clamp,
-                                      out, osb, osh, osn, f, empty);
+    const int status = prepare_backward(dtype, B, H, N, D, k, pi, causal, q, kk, v, sb, sh, sn, gate, gsb, gsh, gsn,
+                                        scale, logit_clamp, lse, out, dout, osb, osh, osn, dq, dk, dv, dgate, p,
+                                        empty);
     if (status != PI_ATTN_OK || empty) return status;
-    if (!gate || !lse || !dout || !dq || !dk || !dv || !dgate || !rowterm) return PI_ATTN_EINVAL;
-    if (!aligned16(dout) || !aligned4(gate) || gsb < 0 || gsh < 0 || gsn < 0) return PI_ATTN_EINVAL;
-    if (!aligned4(lse) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv) || !aligned4(dgate) ||
-        !aligned4(rowterm))
-        return PI_ATTN_EINVAL;
-    f.gate = gate; f.gsb = gsb; f.gsh = gsh; f.gsn = gsn;
-    p.dtype = dtype == PI_ATTN_BF16 ? 1 : 0;
-    p.lse = lse;
-    p.out = out; p.dout = dout; p.osb = osb; p.osh = osh; p.osn = osn;
-    p.dq = dq; p.dk = dk; p.dv = dv; p.dgate = dgate; p.rowterm = rowterm;
+    if (!rowterm || !aligned4(rowterm)) return PI_ATTN_EINVAL;
+    p.rowterm = rowterm;
+    return from_hip(launch_backward(p, (hipStream_t)stream));
+}
+
+int pi_attn_backward_noalloc(int32_t dtype, int32_t B, int32_t H, int32_t N, int32_t D, int32_t k, int32_t pi,
+                             int32_t causal, const void *q, const void *kk, const void *v, int64_t sb, int64_t sh,
+                             int64_t sn, const float *gate, int64_t gsb, int64_t gsh, int64_t gsn, float scale,
+                             float logit_clamp, const float *lse, const void *out, const void *dout, int64_t osb,
+                             int64_t osh, int64_t osn, float *dq, float *dk, float *dv, float *dgate, void *stream) {
+    if (B < 0 || H < 0 || N < 0) return PI_ATTN_EINVAL;
+    if ((int64_t)B * H * N > kScratchRows) return PI_ATTN_ESCRATCH;
+    BwdParams p{};
+    bool empty;
+    int status = prepare_backward(dtype, B, H, N, D, k, pi, causal, q, kk, v, sb, sh, sn, gate, gsb, gsh, gsn, scale,
+                                  logit_clamp, lse, out, dout, osb, osh, osn, dq, dk, dv, dgate, p, empty);
+    if (status != PI_ATTN_OK || empty) return status;
+    status = scratch_of_current_device(&p.rowterm);
+    if (status != PI_ATTN_OK) return status;
+    // every path writes each row term before it reads it: nothing to clear
     return from_hip(launch_backward(p, (hipStream_t)stream));
 }
 

@@ -12,7 +12,7 @@ import paper_2511_10696_amd as pa
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "pi_attn.h")
 
-EINVAL, EUNSUP = -1, -2
+EINVAL, EUNSUP, ESCRATCH = -1, -2, -4
 
 
 @pytest.fixture(scope="module")
@@ -40,7 +40,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_strerror(lib):
-    for st in (0, -1, -2, -3, -99):
+    for st in (0, -1, -2, -3, -4, -99):
         assert isinstance(pa.pi_attn_strerror(st), str) and pa.pi_attn_strerror(st)
 
 
@@ -155,6 +155,37 @@ def test_backward_rejects(lib, kw, code):
 @pytest.mark.parametrize("kw", [dict(N=0), dict(B=0), dict(N=0, lse=None, dq=None)])
 def test_backward_empty_is_noop(lib, kw):
     assert bwd(lib, **kw) == 0
+
+
+def bwd_noalloc(lib, **kw):
+    a = dict(dtype=1, B=1, H=2, N=256, D=64, k=32, pi=64, causal=1, q=16, kk=16, v=16, sb=32768, sh=16384,
+             sn=64, gate=16, gsb=0, gsh=1, gsn=0, scale=0.125, clamp=0.0, lse=16, out=16, dout=16, osb=32768,
+             osh=16384, osn=64, dq=16, dk=16, dv=16, dg=16, stream=None)
+    a.update(kw)
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.pi_attn_backward_noalloc(a["dtype"], a["B"], a["H"], a["N"], a["D"], a["k"], a["pi"], a["causal"],
+                                        vp(a["q"]), vp(a["kk"]), vp(a["v"]), a["sb"], a["sh"], a["sn"],
+                                        vp(a["gate"]), a["gsb"], a["gsh"], a["gsn"], a["scale"], a["clamp"],
+                                        vp(a["lse"]), vp(a["out"]), vp(a["dout"]), a["osb"], a["osh"], a["osn"],
+                                        vp(a["dq"]), vp(a["dk"]), vp(a["dv"]), vp(a["dg"]), vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=5), EUNSUP), (dict(D=32), EUNSUP), (dict(B=-1), EINVAL), (dict(N=-3), EINVAL),
+    (dict(k=-1), EINVAL), (dict(lse=None), EINVAL), (dict(out=8), EINVAL), (dict(dq=None), EINVAL),
+    (dict(dg=None), EINVAL), (dict(dq=20), EINVAL), (dict(scale=0.0), EINVAL), (dict(gsh=-1), EINVAL),
+    # B*H*N above the fixed row-term array (4194304 entries): rejected before anything else
+    (dict(B=1, H=1, N=(1 << 22) + 1), ESCRATCH), (dict(B=2, H=1024, N=2049), ESCRATCH),
+    (dict(B=1, H=32, N=(1 << 17) + 1, q=None), ESCRATCH),
+    (dict(B=1, H=32, N=1 << 17, q=None), EINVAL),     # exactly the maximum: past the size check
+])
+def test_backward_noalloc_rejects(lib, kw, code):
+    assert bwd_noalloc(lib, **kw) == code
+
+
+@pytest.mark.parametrize("kw", [dict(N=0), dict(B=0, H=1 << 20), dict(N=0, lse=None, dq=None)])
+def test_backward_noalloc_empty_is_noop(lib, kw):
+    assert bwd_noalloc(lib, **kw) == 0
 
 
 def shard(lib, **kw):
