@@ -41,18 +41,18 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
-PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "forward_bf16_fwd32k_hbm_traffic.txt")
-DECODE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_bf16_s64_hbm_traffic.txt")
-BIDIR_TRAFFIC = os.path.join(ROOT, "profiles", "forward_bf16_bidir_fwd32k_hbm_traffic.txt")
-BACKWARD_TRAFFIC = {True: os.path.join(ROOT, "profiles", "backward_bf16_fwd32k_hbm_traffic.txt"),
-                    False: os.path.join(ROOT, "profiles", "backward_bf16_bidir_fwd32k_hbm_traffic.txt")}
-SMALLK_TRAFFIC = {"gated": os.path.join(ROOT, "profiles", "smallk_bf16_gated_smallk8k_hbm_traffic.txt"),
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "forward_bf16_fwd32k_counters.txt")
+DECODE_TRAFFIC = os.path.join(ROOT, "profiles", "decode_bf16_s64_counters.txt")
+BIDIR_TRAFFIC = os.path.join(ROOT, "profiles", "forward_bf16_bidir_fwd32k_counters.txt")
+BACKWARD_TRAFFIC = {True: os.path.join(ROOT, "profiles", "backward_bf16_fwd32k_counters.txt"),
+                    False: os.path.join(ROOT, "profiles", "backward_bf16_bidir_fwd32k_counters.txt")}
+SMALLK_TRAFFIC = {"gated": os.path.join(ROOT, "profiles", "smallk_bf16_gated_smallk8k_counters.txt"),
                   "gated_bidirectional": os.path.join(ROOT, "profiles",
-                                                      "smallk_bf16_gated_bidir_smallk8k_hbm_traffic.txt"),
-                  "per_head_gate": os.path.join(ROOT, "profiles", "smallk_bf16_smallk8k_hbm_traffic.txt"),
-                  "backward": os.path.join(ROOT, "profiles", "smallk_bwd_bf16_smallk8k_hbm_traffic.txt"),
+                                                      "smallk_bf16_gated_bidir_smallk8k_counters.txt"),
+                  "per_head_gate": os.path.join(ROOT, "profiles", "smallk_bf16_smallk8k_counters.txt"),
+                  "backward": os.path.join(ROOT, "profiles", "smallk_bwd_bf16_smallk8k_counters.txt"),
                   "backward_bidirectional": os.path.join(ROOT, "profiles",
-                                                         "smallk_bwd_bf16_bidir_smallk8k_hbm_traffic.txt")}
+                                                         "smallk_bwd_bf16_bidir_smallk8k_counters.txt")}
 FORWARD_SOURCES = ("forward_bf16.hip", "pi_common.h", "kernels.h")
 SMALLK_SOURCES = ("smallk_bf16.hip", "smallk_common.h", "smallk.h", "pi_common.h", "kernels.h")
 SMALLK_BWD_SOURCES = ("smallk_bwd_bf16.hip", "smallk_common.h", "smallk.h", "backward.hip", "pi_common.h",
@@ -160,10 +160,32 @@ def time_launches(torch, fn, steps, warmup, stream):
 FLUSH_BYTES = 1 << 30    # written between cold launches: 4x the 256 MB last-level cache plus the L2s
 
 
+def hip_clocks(dev_index):
+    """Peak shader and memory clocks (MHz) the HIP runtime reports for the device."""
+    import ctypes
+    try:
+        hip = ctypes.CDLL("libamdhip64.so")
+    except OSError:
+        return {}
+    out = {}
+    for name, attr in (("sclk_peak_mhz", "hipDeviceAttributeClockRate"),
+                       ("mclk_peak_mhz", "hipDeviceAttributeMemoryClockRate")):
+        code = HIP_DEVICE_ATTRIBUTES[attr]
+        val = ctypes.c_int(0)
+        if hip.hipDeviceGetAttribute(ctypes.byref(val), code, dev_index) == 0:
+            out[name] = round(val.value / 1e3, 1)   # kHz -> MHz
+    return out
+
+
+# hipDeviceAttribute_t values of the two clock queries (hip/hip_runtime_api.h, ROCm 7)
+HIP_DEVICE_ATTRIBUTES = {"hipDeviceAttributeClockRate": 5, "hipDeviceAttributeMemoryClockRate": 60}
+
+
 def device_info(torch, dev):
     pr = torch.cuda.get_device_properties(dev)
     return {"name": pr.name, "arch": getattr(pr, "gcnArchName", None), "compute_units": pr.multi_processor_count,
-            "hbm_bytes": pr.total_memory, "hbm_peak_gbs": HBM_PEAK_GBS, "mfma_bf16_peak_tflops": MFMA_BF16_PEAK_TFLOPS}
+            "hbm_bytes": pr.total_memory, "hbm_peak_gbs": HBM_PEAK_GBS, "mfma_bf16_peak_tflops": MFMA_BF16_PEAK_TFLOPS,
+            **hip_clocks(dev.index or 0)}
 
 
 def time_cold(torch, fn, reps, stream):
@@ -185,9 +207,11 @@ def time_cold(torch, fn, reps, stream):
     return times[len(times) // 2], times[0]
 
 
-def roofline_of(flops, nbytes, sec, kernel, traffic=None):
+def roofline_of(flops, nbytes, sec, kernel, traffic=None, counters=None):
     """Roofline record of one launch: the bound is whichever of the HBM and
-    MFMA times of its algorithmic work is larger."""
+    MFMA times of its algorithmic work is larger; `counters` (from the
+    committed counter summary of the same kernel sources) adds the measured
+    MFMA busy fraction, DRAM rate and clock."""
     tflops, gbs = flops / sec / 1e12, nbytes / sec / 1e9
     hbm = nbytes / (HBM_PEAK_GBS * 1e9) >= flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
     r = {"bound": "hbm" if hbm else "mfma", "kernel": kernel,
@@ -196,6 +220,8 @@ def roofline_of(flops, nbytes, sec, kernel, traffic=None):
          "unit": "GB/s" if hbm else "TFLOP/s",
          "frac": round((gbs / HBM_PEAK_GBS) if hbm else (tflops / MFMA_BF16_PEAK_TFLOPS), 4),
          "traffic": traffic}
+    if counters:
+        r.update(counters)
     mf = {"achieved": round(tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
           "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "flops_per_launch": flops,
           "bytes_per_launch": nbytes}
@@ -230,10 +256,10 @@ def source_digest(paths):
     return h.hexdigest()[:16]
 
 
-def measured_traffic(digest, path=PROFILE_TRAFFIC):
-    """HBM bytes per launch (calibrated FETCH_SIZE + WRITE_SIZE) from the
-    committed rocprofv3 counter summary; valid only for the kernel source it
-    was taken on, so None once the source digest differs."""
+def read_profile(digest, path):
+    """The key = value fields of a committed rocprofv3 counter summary, or
+    None when it is missing or was taken on other kernel sources (its
+    source_digest differs from `digest`)."""
     if not os.path.exists(path):
         return None
     rec = {}
@@ -241,9 +267,36 @@ def measured_traffic(digest, path=PROFILE_TRAFFIC):
         if "=" in line and not line.lstrip().startswith("#"):
             key, val = line.split("=", 1)
             rec[key.strip()] = val.strip()
-    if rec.get("source_digest") != digest or "hbm_bytes_per_launch" not in rec:
+    return rec if rec.get("source_digest") == digest else None
+
+
+def measured_traffic(digest, path=PROFILE_TRAFFIC):
+    """HBM bytes per launch (calibrated FETCH_SIZE + WRITE_SIZE) from the
+    committed rocprofv3 counter summary; valid only for the kernel source it
+    was taken on, so None once the source digest differs."""
+    rec = read_profile(digest, path)
+    if rec is None or "hbm_bytes_per_launch" not in rec:
         return None
     return int(float(rec["hbm_bytes_per_launch"]))
+
+
+def measured_counters(digest, path, sec):
+    """Counter figures of the same summary for the bench line: the MFMA busy
+    fraction (SQ_VALU_MFMA_BUSY_CYCLES over the SIMD-cycles of the kernel's
+    active time), the LDS bank-conflict fraction, the shader clock the
+    kernel ran at (GRBM_GUI_ACTIVE cycles over its traced duration), and the
+    measured DRAM rate (the counted HBM bytes over this run's launch time).
+    Empty when the summary does not match the kernel sources."""
+    rec = read_profile(digest, path)
+    if rec is None:
+        return {}
+    out = {}
+    for key in ("mfma_busy", "lds_bank_conflict", "sclk_mhz"):
+        if key in rec:
+            out[key] = float(rec[key])
+    if "hbm_bytes_per_launch" in rec:
+        out["dram_gbs"] = round(float(rec["hbm_bytes_per_launch"]) / sec / 1e9, 2)
+    return out
 
 
 def pmc_probe(W, pa, torch, dev):
@@ -339,7 +392,8 @@ def main():
     keys, flops, nbytes = forward_algorithmic(cfg)
     digest = csrc_digest(FORWARD_SOURCES)
     roofline, roofline_mfma = roofline_of(flops, nbytes, sec, "forward_bf16_kernel<128,false,false,false>",
-                                          measured_traffic(digest))
+                                          measured_traffic(digest), measured_counters(digest, PROFILE_TRAFFIC, sec))
+    host_inputs = [x.cpu() for x in (q, k, v, gate)]   # the exact bytes the kernel consumed, for the CPU baseline
 
     # ---- bidirectional forward, same shape ----------------------------------
     bidir = None
@@ -349,7 +403,8 @@ def main():
             args.steps, args.warmup, stream)
         bkeys, bflops, bbytes = forward_algorithmic(cfg, causal=False)
         brl, bmf = roofline_of(bflops, bbytes, bms / 1e3, "forward_bf16_kernel<128,false,true,false>",
-                               measured_traffic(digest, BIDIR_TRAFFIC))
+                               measured_traffic(digest, BIDIR_TRAFFIC),
+                               measured_counters(digest, BIDIR_TRAFFIC, bms / 1e3))
         bidir = {"workload": "fwd32k bidirectional: B1 H32 N32768 D128 k512 pi1024 bf16 (window |j-t|<=k, "
                              "partners t-pi and t+pi)",
                  "steps": args.steps, "ms_per_step": round(bms, 5),
@@ -379,15 +434,19 @@ def main():
             ccfg = W.FORWARD[cname]
             cq, ck, cv, cg = W.forward_inputs(ccfg, 0, dev)
             cout = torch.empty_like(cq)
-            cms, _, _ = time_launches(torch, lambda: pa.pi_attn_forward(cq, ck, cv, cg, ccfg.k, ccfg.pi, out=cout),
-                                      args.steps, args.warmup, stream)
+            cfn = lambda: pa.pi_attn_forward(cq, ck, cv, cg, ccfg.k, ccfg.pi, out=cout)
+            cms, _, _ = time_launches(torch, cfn, args.steps, args.warmup, stream)
+            ccold, ccold_min = time_cold(torch, cfn, args.cold_reps, stream)
             ckeys, cflops, cbytes = forward_algorithmic(ccfg)
             crl, cmf = roofline_of(cflops, cbytes, cms / 1e3, f"forward_bf16_kernel<{ccfg.D},false,false,false>")
             variants[cname] = {"workload": f"{cname}: causal B{ccfg.B} H{ccfg.H} N{ccfg.N} D{ccfg.D} k{ccfg.k} "
                                            f"pi{ccfg.pi} bf16", "steps": args.steps, "ms_per_step": round(cms, 5),
                                "query_positions_per_s": round(ccfg.B * ccfg.N / (cms / 1e3), 1),
                                "attended_keys_per_s": round(ckeys / (cms / 1e3), 1),
-                               "roofline": crl, "roofline_mfma": cmf}
+                               "roofline": crl, "roofline_mfma": cmf,
+                               "cold": {"ms_per_step_median": round(ccold, 5), "ms_per_step_min": round(ccold_min, 5),
+                                        "reps": args.cold_reps,
+                                        "roofline_frac_median": round(cbytes / (ccold / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}}
             del cq, ck, cv, cg, cout
             torch.cuda.empty_cache()
 
@@ -402,12 +461,16 @@ def main():
         shard = bench_shard(cfg, W, pa, torch, dev, stream, args.steps, args.warmup)
 
     # ---- decode step --------------------------------------------------------
-    decode = None
+    decode = decode_host = None
     if not args.no_decode:
         dcfg = W.DECODE["decode"]
         nsteps = args.decode_steps
         kc, vc, lens, dgate = W.decode_state(dcfg, 0, dev)
         qs, ks, vs = W.decode_tokens(dcfg, nsteps, 1, dev)
+        if not args.no_cpu_baseline:   # the rows the oracle's first ten steps can reach, as the GPU holds them
+            L0, P = dcfg.cache_len, dcfg.pi
+            decode_host = (kc[:, :, L0 - P:L0].cpu(), vc[:, :, L0 - P:L0].cpu(), qs[:10].cpu(), ks[:10].cpu(),
+                           vs[:10].cpu(), dgate.cpu())
         lbuf = [lens, torch.empty_like(lens)]
         dout = torch.empty((dcfg.S, dcfg.H, dcfg.D), dtype=dcfg.dtype, device=dev)
         # settle and warm up on a scratch copy of the lengths (row cache_len is
@@ -446,6 +509,7 @@ def main():
         ddigest = source_digest([os.path.join(ROOT, "paper_2511_10696_amd", "csrc", f)
                                  for f in ("decode_bf16.hip", "pi_common.h", "kernels.h")])
         dtraffic = measured_traffic(ddigest, DECODE_TRAFFIC)
+        dcounters = measured_counters(ddigest, DECODE_TRAFFIC, dms / 1e3)
         dgbs = dbytes / (dms / 1e3) / 1e9
         decode = {"workload": "decode S64 H32 D128 k512 pi1024 cache32768 bf16", "steps": nsteps,
                   "ms_per_step": round(dms, 5), "us_per_step": round(dms * 1e3, 2),
@@ -455,7 +519,7 @@ def main():
                   "roofline": {"bound": "hbm", "kernel": "decode_bf16_kernel<128>",
                                "achieved": round(dgbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                "frac": round(dgbs / HBM_PEAK_GBS, 4), "bytes_per_step": dbytes,
-                               "traffic": dtraffic}}
+                               "traffic": dtraffic, **dcounters}}
         del kc, vc, qs, ks, vs
         torch.cuda.empty_cache()
 
@@ -468,7 +532,8 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, W)
+        cpu = cpu_baseline(cfg, host_inputs, W.DECODE["decode"], decode_host)
+    del host_inputs
 
     rec = {
         "metric": "pi-Attn fwd queries/s at N=32K + decode step latency; % HBM/MFMA roofline",
@@ -527,7 +592,8 @@ def bench_smallk(W, pa, torch, dev, stream, steps, warmup):
         mode = "false" if causal else "true"
         rl, mf = roofline_of(flops, nbytes, ms / 1e3,
                              f"smallk_bf16_kernel<64,{mode},{'true' if gated else 'false'},4>",
-                             measured_traffic(csrc_digest(SMALLK_SOURCES), SMALLK_TRAFFIC[name]))
+                             measured_traffic(csrc_digest(SMALLK_SOURCES), SMALLK_TRAFFIC[name]),
+                             measured_counters(csrc_digest(SMALLK_SOURCES), SMALLK_TRAFFIC[name], ms / 1e3))
         res[name] = {"us_per_step": round(ms * 1e3, 2),
                      "query_positions_per_s": round(cfg.B * cfg.N / (ms / 1e3), 1),
                      "attended_keys_per_s": round(keys / (ms / 1e3), 1),
@@ -543,7 +609,8 @@ def bench_smallk(W, pa, torch, dev, stream, steps, warmup):
         mode = "false" if causal else "true"
         rl, _ = roofline_of(flops, nbytes, ms / 1e3,
                             f"smallk_bwd_q_kernel<64,{mode},4> + smallk_bwd_kv_kernel<64,{mode},4>",
-                            measured_traffic(csrc_digest(SMALLK_BWD_SOURCES), SMALLK_TRAFFIC[name]))
+                            measured_traffic(csrc_digest(SMALLK_BWD_SOURCES), SMALLK_TRAFFIC[name]),
+                            measured_counters(csrc_digest(SMALLK_BWD_SOURCES), SMALLK_TRAFFIC[name], ms / 1e3))
         res[name] = {"us_per_step": round(ms * 1e3, 2),
                      "query_positions_per_s": round(cfg.B * cfg.N / (ms / 1e3), 1),
                      "bytes_per_step": nbytes, "roofline": rl}
@@ -617,27 +684,82 @@ def bench_backward(cfg, W, pa, torch, dev, stream, steps, causal):
     mode = "false" if causal else "true"
     kernels = f"backward_q_bf16_kernel<128,false,{mode}> + backward_kv_bf16_kernel<128,false,{mode}>"
     rl, mf = roofline_of(flops, nbytes, ms / 1e3, kernels,
-                         measured_traffic(csrc_digest(BACKWARD_SOURCES), BACKWARD_TRAFFIC[causal]))
+                         measured_traffic(csrc_digest(BACKWARD_SOURCES), BACKWARD_TRAFFIC[causal]),
+                         measured_counters(csrc_digest(BACKWARD_SOURCES), BACKWARD_TRAFFIC[causal], ms / 1e3))
     return {"workload": ("backward of fwd32k" + ("" if causal else " bidirectional")
                          + ": B1 H32 N32768 D128 k512 pi1024 bf16 in, fp32 gradients"),
             "steps": steps, "ms_per_step": round(ms, 4), "roofline": rl, "roofline_mfma": mf}
 
 
-def cpu_baseline(cfg, W):
-    """The fp64 oracle, as it stands, on the forward workload (fresh CPU
-    inputs of the same shape and distribution, every head and query; a few
-    seconds on the host's cores), in query positions/s of the full problem."""
-    import torch
+ONE_THREAD_CHILD = """
+import sys, time
+import numpy as np
+sys.path.insert(0, sys.argv[1])
+import oracle
+d = np.load(sys.argv[2])
+t = time.perf_counter()
+oracle.forward(d["q"], d["k"], d["v"], d["gate"], int(d["kw"]), int(d["pi"]))
+print(time.perf_counter() - t)
+"""
+
+
+def cpu_baseline(cfg, host_inputs, dcfg=None, decode_host=None):
+    """The fp64 oracle, as it stands, on the host's cores, fed host copies of
+    exactly the bytes the GPU consumed: (1) the whole fwd32k forward on all
+    cores, in query positions/s; (2) one (b, h) slice on one thread,
+    scaled by B*H and labelled extrapolated; (3) ten consecutive decode
+    steps of the decode workload on all cores, per step, over the rows each
+    step's working set can reach (pi + 1 per (s, h))."""
+    import subprocess
+    import tempfile
+
+    import numpy as np
 
     import oracle
-    q, k, v, gate = W.forward_inputs(cfg, 0, "cpu")
+    q, k, v, gate = host_inputs
     t = time.perf_counter()
     oracle.forward(q, k, v, gate, cfg.k, cfg.pi)
     dt = time.perf_counter() - t
-    return {"value": round(cfg.B * cfg.N / dt, 1), "unit": "query positions/s",
-            "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"the whole fwd32k forward ({cfg.B * cfg.H} heads x {cfg.N} queries), fp64, {dt:.2f} s",
-            "head_rows_per_s": round(cfg.B * cfg.H * cfg.N / dt, 1)}
+    res = {"value": round(cfg.B * cfg.N / dt, 1), "unit": "query positions/s",
+           "cores": oracle.num_threads(), "kind": "oracle",
+           "sample": f"the whole fwd32k forward ({cfg.B * cfg.H} heads x {cfg.N} queries), fp64, {dt:.2f} s, "
+                     "on a device-to-host copy of the kernel's inputs",
+           "head_rows_per_s": round(cfg.B * cfg.H * cfg.N / dt, 1)}
+    with tempfile.TemporaryDirectory() as td:
+        path = os.path.join(td, "slice.npz")
+        np.savez(path, q=q[:1, :1].float().numpy(), k=k[:1, :1].float().numpy(), v=v[:1, :1].float().numpy(),
+                 gate=gate[:1].double().numpy(), kw=cfg.k, pi=cfg.pi)
+        env = dict(os.environ, OMP_NUM_THREADS="1")
+        r = subprocess.run([sys.executable, "-c", ONE_THREAD_CHILD, ROOT, path], env=env, capture_output=True,
+                           text=True, timeout=600)
+    if r.returncode == 0:
+        dt1 = float(r.stdout.strip().splitlines()[-1])
+        res["single_thread_extrapolated"] = {
+            "value": round(cfg.N / (dt1 * cfg.B * cfg.H) * cfg.B, 1), "unit": "query positions/s", "cores": 1,
+            "sample": f"one (b, h) slice of fwd32k ({cfg.N} queries) on one thread in {dt1:.2f} s, "
+                      f"extrapolated to all {cfg.B * cfg.H} heads"}
+    if decode_host is not None:
+        k0, v0, qs, ks, vs, gate_d = decode_host
+        steps = qs.shape[0]
+        P = dcfg.pi
+        shape = (dcfg.S, dcfg.H, P + steps, dcfg.D)
+        kk = np.zeros(shape, np.float32)
+        vv = np.zeros(shape, np.float32)
+        kk[:, :, :P] = k0.float().numpy()
+        vv[:, :, :P] = v0.float().numpy()
+        per = []
+        for i in range(steps):
+            lens = np.full(dcfg.S, P + i, np.int32)
+            t = time.perf_counter()
+            oracle.decode_step(lens, qs[i], ks[i], vs[i], kk, vv, gate_d, dcfg.k, dcfg.pi)
+            per.append(time.perf_counter() - t)
+        us = sum(per) / steps * 1e6
+        res["decode"] = {"us_per_step": round(us, 1), "queries_per_s": round(dcfg.S / (us / 1e6), 1),
+                         "steps": steps, "cores": oracle.num_threads(),
+                         "sample": f"{steps} consecutive steps of the decode workload from 32768 cached rows, "
+                                   f"{dcfg.S} sequences x {dcfg.H} heads, fp64, over the pi + 1 rows each "
+                                   "(s, h) can reach"}
+    return res
 
 
 if __name__ == "__main__":

@@ -50,3 +50,22 @@ def test_shard_accounting():
     assert keys == (cfg.N - s0) * (cfg.k + 2) * cfg.B * cfg.H
     assert flops == 4 * cfg.D * keys
     assert nbytes == cfg.B * cfg.H * cfg.D * 2 * (2 * (cfg.N - s0) + 2 * (cfg.N - lo))
+
+
+def test_cpu_baseline_legs_on_a_small_problem():
+    """The CPU-baseline leg on small stand-ins: the all-core forward, the
+    one-thread slice extrapolated to every head, and ten decode steps over
+    the rows each step can reach."""
+    import dataclasses
+    import torch
+    cfg = W.ForwardConfig("small", 1, 2, 300, 64, 32, 64, torch.bfloat16)
+    host = W.forward_inputs(cfg, 0, "cpu")
+    dcfg = dataclasses.replace(W.DECODE["decode"], S=2, H=2, D=64, k=16, pi=40, cache_len=100, steps=10)
+    g = torch.Generator().manual_seed(0)
+    k0, v0 = (torch.randn(2, 2, 40, 64, generator=g).to(torch.bfloat16) for _ in range(2))
+    qs, ks, vs = (torch.randn(10, 2, 2, 64, generator=g).to(torch.bfloat16) for _ in range(3))
+    res = bench.cpu_baseline(cfg, host, dcfg, (k0, v0, qs, ks, vs, torch.zeros(2)))
+    assert res["kind"] == "oracle" and res["value"] > 0 and res["cores"] >= 1
+    st = res["single_thread_extrapolated"]
+    assert st["cores"] == 1 and st["value"] > 0 and "extrapolated" in st["sample"]
+    assert res["decode"]["steps"] == 10 and res["decode"]["us_per_step"] > 0
