@@ -9,6 +9,7 @@ from __future__ import annotations
 
 import glob
 import os
+import re
 import subprocess
 import sys
 from concurrent.futures import ThreadPoolExecutor
@@ -43,13 +44,35 @@ def sources() -> list[str]:
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
+# The compiler's per-kernel resource remarks; the build fails if any kernel
+# needs private (scratch) memory, i.e. spills registers.
+RESOURCE_REMARKS = ["-Rpass-analysis=kernel-resource-usage"]
+
+
+def scratch_users(remarks: str) -> list[str]:
+    """Kernels whose resource remark reports a nonzero ScratchSize."""
+    users, name = [], None
+    for line in remarks.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            continue
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and int(m.group(1)) > 0:
+            users.append(f"{name} ({m.group(1)} bytes/lane)")
+    return users
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
     form = [] if os.path.basename(src) in AGPR_FORM else VGPR_FORM
-    cmd = [hipcc(), *COMMON, *form, "-c", src, "-o", obj]
+    cmd = [hipcc(), *COMMON, *form, *RESOURCE_REMARKS, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
+    spills = scratch_users(r.stderr)
+    if spills:
+        raise RuntimeError(f"{src}: kernels use scratch memory (register spills): " + ", ".join(spills))
     return obj
 
 

@@ -24,8 +24,9 @@
 // A = sum alpha^ dP and B = sum alpha^ over the unclamped entries of each
 // prior, dg = sum_prior d(log omega)/dg (A - r* B).  r* is also written out
 // as the row term of the key pass.  The partner
-// row (Sec. 3.4, eq. Npi) is the diagonal of one 32x32 block per product,
-// read straight from global memory as in the forward; the bidirectional mode
+// row (Sec. 3.4, eq. Npi) is read straight from global memory in the layout
+// of the query fragments, and its score and dP are per-lane dot products
+// (then the other half's), as in the forward; the bidirectional mode
 // (window |j - t| <= k, band up to t0 + 127 + k) adds the second partner
 // t + pi the same way.
 //
@@ -106,14 +107,16 @@ __device__ inline float other_half(float x) {
     return __uint_as_float(__lane_id() < 32 ? p[1] : p[0]);
 }
 
-// Diagonal (row c, column c) of a 32x32 accumulator block, for lane (c, g).
-__device__ inline float diagonal(const f32x16 &acc, int c, int g) {
-    const int slot = 4 * (c >> 3) + (c & 3);
-    float mine = 0.0f;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) mine = (e == slot) ? acc[e] : mine;
-    const float theirs = other_half(mine);
-    return (g == ((c >> 2) & 1)) ? mine : theirs;
+// acc + <a, b> over eight bf16 pairs (packed products, fp32 sums).
+__device__ inline float dot_bf16x8(const bf16x8 &a, const bf16x8 &b, float acc) {
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 0, 1), __builtin_shufflevector(b, b, 0, 1),
+                                          acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 2, 3), __builtin_shufflevector(b, b, 2, 3),
+                                          acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 4, 5), __builtin_shufflevector(b, b, 4, 5),
+                                          acc, false);
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 6, 7), __builtin_shufflevector(b, b, 6, 7),
+                                           acc, false);
 }
 
 // Row fragments (A operand, row l%32, dims 16s + 8(l/32)) of 32-row block
@@ -232,7 +235,7 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
     // exact row term and per-prior sums for the gate gradient
     float r_all = 0.0f, a_loc = 0.0f, b_loc = 0.0f, a_par = 0.0f, b_par = 0.0f;
 
-    // ---- partners: the diagonal of K_p Q^T and V_p dO^T ----------------------
+    // ---- partners: scores and dP of the partner rows ------------------------
     // Partner row prow of this lane's query (has_p: it exists).
     auto partner = [&](int prow, bool has_p) {
         if (__builtin_amdgcn_ballot_w64(has_p) == 0) return;
@@ -243,13 +246,15 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
             kpf[s] = *reinterpret_cast<const bf16x8 *>(kp + prc * ksn + 16 * s + 8 * g);
             vpf[s] = *reinterpret_cast<const bf16x8 *>(vp + prc * ksn + 16 * s + 8 * g);
         }
-        f32x16 sa = {}, da = {};
+        // score and dP of the partner: per-lane dot products of the query and
+        // dL/dy fragments with the partner rows (same layout), then the pair
+        float sa = 0.0f, da = 0.0f;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
-            sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(has_p ? kpf[s] : bf16x8{}, qf[s], sa, 0, 0, 0);
-            da = __builtin_amdgcn_mfma_f32_32x32x16_bf16(has_p ? vpf[s] : bf16x8{}, of[s], da, 0, 0, 0);
+            sa = dot_bf16x8(qf[s], has_p ? kpf[s] : bf16x8{}, sa);
+            da = dot_bf16x8(of[s], has_p ? vpf[s] : bf16x8{}, da);
         }
-        const float sd = diagonal(sa, c, g), dpd = diagonal(da, c, g);
+        const float sd = sa + other_half(sa), dpd = da + other_half(da);
         float delta2;
         bool cut = false;
         if constexpr (CLAMP) {

@@ -32,8 +32,8 @@
 //
 // The long-range partner (Sec. 3.4, eq. Npi; Sec. 3.5, eq. online_ws): the
 // partner rows of a wavefront's 32 queries are 32 consecutive rows shifted by
-// pi, read straight from global memory into the MFMA operand layout.  Its
-// score (the diagonal of one 32x32 MFMA block) seeds the online softmax:
+// pi, read straight from global memory in the layout of the query fragments.
+// Its score (a per-lane dot product of the two) seeds the online softmax:
 // running max = partner logit, running sum = 1, accumulator = partner value.
 // The bidirectional mode scores the second partner t + pi the same way and
 // seeds the state with both.
@@ -169,6 +169,18 @@ __device__ inline float sum_bf16x8(const bf16x8 &p, float s) {
     s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 4, 5), one, s, false);
     s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 6, 7), one, s, false);
     return s;
+}
+
+// acc + <a, b> over eight bf16 pairs (packed products, fp32 sums).
+__device__ inline float dot_bf16x8(const bf16x8 &a, const bf16x8 &b, float acc) {
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 0, 1), __builtin_shufflevector(b, b, 0, 1),
+                                          acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 2, 3), __builtin_shufflevector(b, b, 2, 3),
+                                          acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 4, 5), __builtin_shufflevector(b, b, 4, 5),
+                                          acc, false);
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 6, 7), __builtin_shufflevector(b, b, 6, 7),
+                                           acc, false);
 }
 
 // Scores of one 32-key block -> log2-unit logits (masked to -inf on edge
@@ -329,19 +341,14 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
     const FusionBias fb = fusion_bias(gl, CLAMP);
     const float c2 = p.scale * kLog2e;
     // Partner logit (log2 units) of this lane's query from the partner rows
-    // kf: the diagonal of one 32x32 score block, whose entry (row c, column
-    // c) sits in half (c/4)%2 at slot 4(c/8) + c%4.
+    // kf: lane (c, g) holds dims 16s + 8g + [0, 8) of query c and of its
+    // partner row, so the score is a per-lane dot product (packed bf16
+    // pairs, fp32 sums) plus the other half's.
     auto partner_logit = [&](const bf16x8 (&kf)[W::KS], bool has) {
-        f32x16 acc = {};
+        float part = 0.0f;
 #pragma unroll
-        for (int s = 0; s < W::KS; ++s)
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(has ? kf[s] : bf16x8{}, ws.qf[s], acc, 0, 0, 0);
-        const int slot = 4 * (c >> 3) + (c & 3);
-        float mine = 0.0f;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) mine = (e == slot) ? acc[e] : mine;
-        const float theirs = other_half(mine);
-        const float diag = (g == ((c >> 2) & 1)) ? mine : theirs;
+        for (int s = 0; s < W::KS; ++s) part = dot_bf16x8(ws.qf[s], has ? kf[s] : bf16x8{}, part);
+        const float diag = part + other_half(part);
         float sp;
         if constexpr (CLAMP) {
             sp = fminf(fmaxf(diag * p.scale + fb.partner, -p.clamp), p.clamp) * kLog2e;

@@ -359,3 +359,13 @@ def test_product_does_not_import_oracle():
                 text = open(os.path.join(dirpath, f)).read()
                 assert not re.search(r"^\s*(import|from)\s+oracle\b", text, flags=re.M), f
                 assert "pi_oracle" not in text and "liboracle" not in text, f
+
+
+def test_build_rejects_scratch_users():
+    """The build's spill check reads the compiler's resource remarks."""
+    from paper_2511_10696_amd import build
+    ok = ("x.hip:1:1: remark: Function Name: _Z1kv [-Rpass-analysis=kernel-resource-usage]\n"
+          "x.hip:1:1: remark:     ScratchSize [bytes/lane]: 0 [-Rpass-analysis=kernel-resource-usage]\n")
+    bad = ok.replace("_Z1kv", "_Z1jv").replace("]: 0 ", "]: 28 ")
+    assert build.scratch_users(ok) == []
+    assert build.scratch_users(ok + bad) == ["_Z1jv (28 bytes/lane)"]
