@@ -132,6 +132,16 @@ def _require_cuda(*ts):
             raise RuntimeError("pi_attn tensors must be on the GPU (no CPU path exists)")
 
 
+def _out_f32(torch, given, shape, device, name):
+    """A caller's float32 output buffer (checked: contiguous, the shape), or a new one."""
+    if given is None:
+        return torch.empty(shape, dtype=torch.float32, device=device)
+    _require_cuda(given)
+    if given.dtype != torch.float32 or tuple(given.shape) != tuple(shape) or not given.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous float32 tensor of shape {tuple(shape)}")
+    return given
+
+
 def _check(status: int, where: str):
     if status != 0:
         raise PiAttnError(status, where)
@@ -267,7 +277,7 @@ def _shard_gate(torch, gate, B, H, n):
 
 def pi_attn_backward_shard_q(q, k, v, gate, k_window: int, pi: int, nseq: int, qpos0: int, kvpos0: int, out, lse,
                              dout, scale: float | None = None, logit_clamp: float = 0.0, stream=None,
-                             causal: bool = True):
+                             causal: bool = True, dq=None, dgate=None, rowterm=None):
     """Query pass of the backward over one shard: q, out, dout [B, H, nq, D]
     (bfloat16) at absolute positions [qpos0, qpos0 + nq), k and v
     [B, H, nkv, D] from absolute position ``kvpos0`` (the forward shard's
@@ -281,10 +291,9 @@ def pi_attn_backward_shard_q(q, k, v, gate, k_window: int, pi: int, nseq: int, q
     if k.shape != v.shape or k.stride() != v.stride() or k.shape[:2] != q.shape[:2] or k.shape[3] != D:
         raise ValueError("k, v [B, H, nkv, D] with shared strides")
     g = _shard_gate(torch, gate, B, H, nq)
-    f32 = dict(dtype=torch.float32, device=q.device)
-    dq = torch.empty((B, H, nq, D), **f32)
-    dg = torch.empty((B, H, nq), **f32)
-    rt = torch.empty((B, H, nq), **f32)
+    dq = _out_f32(torch, dq, (B, H, nq, D), q.device, "dq")
+    dg = _out_f32(torch, dgate, (B, H, nq), q.device, "dgate")
+    rt = _out_f32(torch, rowterm, (B, H, nq), q.device, "rowterm")
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     st = library().pi_attn_backward_shard_q(
@@ -299,7 +308,7 @@ def pi_attn_backward_shard_q(q, k, v, gate, k_window: int, pi: int, nseq: int, q
 
 def pi_attn_backward_shard_kv(q, k, v, gate, k_window: int, pi: int, nseq: int, kpos0: int, qpos0: int, lse, rowterm,
                               dout, scale: float | None = None, logit_clamp: float = 0.0, stream=None,
-                              causal: bool = True):
+                              causal: bool = True, dk=None, dv=None):
     """Key pass of the backward over one shard: k, v [B, H, nk, D] (bfloat16)
     the keys at absolute positions [kpos0, kpos0 + nk); q, dout
     [B, H, nqh, D], lse, rowterm [B, H, nqh] (contiguous float32) and gate
@@ -317,9 +326,8 @@ def pi_attn_backward_shard_kv(q, k, v, gate, k_window: int, pi: int, nseq: int, 
         if x.dtype != torch.float32 or tuple(x.shape) != (B, H, nqh) or not x.is_contiguous():
             raise ValueError(f"{name} must be a contiguous float32 [B, H, nqh] tensor")
     g = _shard_gate(torch, gate, B, H, nqh)
-    f32 = dict(dtype=torch.float32, device=k.device)
-    dk = torch.empty((B, H, nk, D), **f32)
-    dv = torch.empty((B, H, nk, D), **f32)
+    dk = _out_f32(torch, dk, (B, H, nk, D), k.device, "dk")
+    dv = _out_f32(torch, dv, (B, H, nk, D), k.device, "dv")
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     st = library().pi_attn_backward_shard_kv(
@@ -389,7 +397,7 @@ def pi_attn_forward_gated(q, k, v, u, w2, b2, k_window: int, pi: int, scale: flo
 
 def pi_attn_backward(q, k, v, gate, k_window: int, pi: int, out, lse, dout, scale: float | None = None,
                      logit_clamp: float = 0.0, gate_grad_per_query: bool = False, stream=None,
-                     causal: bool = True):
+                     causal: bool = True, dq=None, dk=None, dv=None, dgate=None, rowterm=None):
     """Gradients of the pi-Attention forward for dL/dy = ``dout``.
 
     q, k, v, gate, k_window, pi, scale, logit_clamp and causal as passed to
@@ -398,7 +406,8 @@ def pi_attn_backward(q, k, v, gate, k_window: int, pi: int, out, lse, dout, scal
     dtype and strides.  Returns float32
     (dq, dk, dv) [B, H, N, D] and dgate shaped like ``gate`` (summed over
     b and t for a per-head gate), or [B, H, N] per query when
-    ``gate_grad_per_query``.
+    ``gate_grad_per_query``.  dq, dk, dv, dgate (per query) and the row-term
+    workspace rowterm may be passed as contiguous float32 buffers to fill.
     """
     torch = _torch()
     _require_cuda(q, k, v, gate, out, dout, lse)
@@ -426,9 +435,9 @@ def pi_attn_backward(q, k, v, gate, k_window: int, pi: int, out, lse, dout, scal
     if lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, N) or not lse.is_contiguous():
         raise ValueError("lse must be the contiguous float32 [B, H, N] lse of the forward")
     f32 = dict(dtype=torch.float32, device=q.device)
-    dq, dk, dv = (torch.empty((B, H, N, D), **f32) for _ in range(3))
-    dg = torch.empty((B, H, N), **f32)
-    rowterm = torch.empty((B, H, N), **f32)
+    dq, dk, dv = (_out_f32(torch, x, (B, H, N, D), q.device, n) for x, n in ((dq, "dq"), (dk, "dk"), (dv, "dv")))
+    dg = _out_f32(torch, dgate, (B, H, N), q.device, "dgate")
+    rowterm = _out_f32(torch, rowterm, (B, H, N), q.device, "rowterm")
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     st = library().pi_attn_backward(
