@@ -61,11 +61,17 @@ enum {
 /* Human-readable text for a status code (static storage, never NULL). */
 const char *pi_attn_strerror(int status);
 
-/* Slots per query in the index-set layout: causal, k+1 window slots plus one
- * partner slot iff pi > k; bidirectional, 2k+1 window slots plus two
- * partner slots iff pi > k.  Returns -1 for k < 0, pi < 0 or a width beyond
- * int32. */
+/* Slots per query in the index-set layout, the largest |W_t| (Sec. 3.5, eq.
+ * online_ws: the window of eq. Nr, radius k with self, plus the partners of
+ * eq. Npi, not counted twice when they lie in the window, App. A offset
+ * list): causal, k+1 window slots plus one partner slot iff pi > k;
+ * bidirectional, 2k+1 window slots plus two partner slots iff pi > k.
+ * Returns -1 for k < 0, pi < 0 or a width beyond int32. */
 int32_t pi_attn_ws_width(int32_t k, int32_t pi, int32_t causal);
+
+/* The paper's score scale 1/sqrt(D) (Sec. 3.2, eq. z), the value to pass as
+ * `scale` for the paper's operator; 0 for D < 1. */
+float pi_attn_default_scale(int32_t D);
 
 /*
  * pi_attn_index_set -- the working sets W_t of a length-n sequence

@@ -16,7 +16,6 @@ bidirectional mode, window |j - t| <= k and partners t -/+ pi):
 from __future__ import annotations
 
 import ctypes
-import math
 import os
 import threading
 
@@ -27,7 +26,7 @@ __all__ = ["pi_attn_index_set", "pi_attn_forward", "pi_attn_forward_gated", "pi_
            "pi_attn_strerror", "library", "LIB_PATH", "EXPORTED_SYMBOLS", "PiAttnError"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpi_attn.so")
-EXPORTED_SYMBOLS = ("pi_attn_strerror", "pi_attn_ws_width", "pi_attn_index_set",
+EXPORTED_SYMBOLS = ("pi_attn_strerror", "pi_attn_ws_width", "pi_attn_default_scale", "pi_attn_index_set",
                     "pi_attn_forward", "pi_attn_forward_gated", "pi_attn_decode_step", "pi_attn_backward",
                     "pi_attn_gate_grad_per_head", "pi_attn_forward_shard", "pi_attn_backward_shard_q",
                     "pi_attn_backward_shard_kv", "pi_attn_backward_noalloc")
@@ -57,6 +56,8 @@ def library() -> ctypes.CDLL:
             lib.pi_attn_strerror.restype = ctypes.c_char_p
             lib.pi_attn_ws_width.argtypes = [i32, i32, i32]
             lib.pi_attn_ws_width.restype = i32
+            lib.pi_attn_default_scale.argtypes = [i32]
+            lib.pi_attn_default_scale.restype = f32
             lib.pi_attn_index_set.argtypes = [i32, i32, i32, i32, vp, vp]
             lib.pi_attn_index_set.restype = ctypes.c_int
             lib.pi_attn_forward.argtypes = ([i32] * 8 + [vp, vp, vp, i64, i64, i64, vp, i64, i64, i64,
@@ -142,6 +143,11 @@ def _out_f32(torch, given, shape, device, name):
     return given
 
 
+def _scale(scale, D: int) -> float:
+    """The given score scale, or the library's default 1/sqrt(D)."""
+    return float(library().pi_attn_default_scale(int(D))) if scale is None else float(scale)
+
+
 def _check(status: int, where: str):
     if status != 0:
         raise PiAttnError(status, where)
@@ -203,8 +209,7 @@ def pi_attn_forward(q, k, v, gate, k_window: int, pi: int, scale: float | None =
     if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, N)
                             or not lse.is_contiguous()):
         raise ValueError("lse must be a contiguous float32 [B, H, N] tensor")
-    if scale is None:
-        scale = 1.0 / math.sqrt(D)
+    scale = _scale(scale, D)
     st = library().pi_attn_forward(
         _dtype_code(q.dtype), B, H, N, D, int(k_window), int(pi), int(bool(causal)),
         _ptr(q), _ptr(k), _ptr(v), q.stride(0), q.stride(1), q.stride(2),
@@ -254,8 +259,7 @@ def pi_attn_forward_shard(q, k, v, gate, k_window: int, pi: int, nseq: int, qpos
     if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, nq)
                             or not lse.is_contiguous()):
         raise ValueError("lse must be a contiguous float32 [B, H, nq] tensor")
-    if scale is None:
-        scale = 1.0 / math.sqrt(D)
+    scale = _scale(scale, D)
     st = library().pi_attn_forward_shard(
         PI_ATTN_BF16, B, H, D, int(k_window), int(pi), int(bool(causal)), int(nseq), int(qpos0), nq, int(kvpos0),
         nkv, _ptr(q), q.stride(0), q.stride(1), q.stride(2), _ptr(k), _ptr(v), k.stride(0), k.stride(1),
@@ -294,8 +298,7 @@ def pi_attn_backward_shard_q(q, k, v, gate, k_window: int, pi: int, nseq: int, q
     dq = _out_f32(torch, dq, (B, H, nq, D), q.device, "dq")
     dg = _out_f32(torch, dgate, (B, H, nq), q.device, "dgate")
     rt = _out_f32(torch, rowterm, (B, H, nq), q.device, "rowterm")
-    if scale is None:
-        scale = 1.0 / math.sqrt(D)
+    scale = _scale(scale, D)
     st = library().pi_attn_backward_shard_q(
         _dtype_code(q.dtype), B, H, D, int(k_window), int(pi), int(bool(causal)), int(nseq), int(qpos0), nq,
         int(kvpos0), k.shape[2], _ptr(q), q.stride(0), q.stride(1), q.stride(2), _ptr(k), _ptr(v), k.stride(0),
@@ -328,8 +331,7 @@ def pi_attn_backward_shard_kv(q, k, v, gate, k_window: int, pi: int, nseq: int, 
     g = _shard_gate(torch, gate, B, H, nqh)
     dk = _out_f32(torch, dk, (B, H, nk, D), k.device, "dk")
     dv = _out_f32(torch, dv, (B, H, nk, D), k.device, "dv")
-    if scale is None:
-        scale = 1.0 / math.sqrt(D)
+    scale = _scale(scale, D)
     st = library().pi_attn_backward_shard_kv(
         _dtype_code(k.dtype), B, H, D, int(k_window), int(pi), int(bool(causal)), int(nseq), int(kpos0), nk,
         int(qpos0), nqh, _ptr(q), q.stride(0), q.stride(1), q.stride(2), _ptr(k), _ptr(v), k.stride(0),
@@ -383,8 +385,7 @@ def pi_attn_forward_gated(q, k, v, u, w2, b2, k_window: int, pi: int, scale: flo
     if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, N)
                             or not lse.is_contiguous()):
         raise ValueError("lse must be a contiguous float32 [B, H, N] tensor")
-    if scale is None:
-        scale = 1.0 / math.sqrt(D)
+    scale = _scale(scale, D)
     st = library().pi_attn_forward_gated(
         _dtype_code(q.dtype), B, H, N, D, int(k_window), int(pi), int(bool(causal)),
         _ptr(q), _ptr(k), _ptr(v), q.stride(0), q.stride(1), q.stride(2),
@@ -438,8 +439,7 @@ def pi_attn_backward(q, k, v, gate, k_window: int, pi: int, out, lse, dout, scal
     dq, dk, dv = (_out_f32(torch, x, (B, H, N, D), q.device, n) for x, n in ((dq, "dq"), (dk, "dk"), (dv, "dv")))
     dg = _out_f32(torch, dgate, (B, H, N), q.device, "dgate")
     rowterm = _out_f32(torch, rowterm, (B, H, N), q.device, "rowterm")
-    if scale is None:
-        scale = 1.0 / math.sqrt(D)
+    scale = _scale(scale, D)
     st = library().pi_attn_backward(
         _dtype_code(q.dtype), B, H, N, D, int(k_window), int(pi), int(bool(causal)),
         _ptr(q), _ptr(k), _ptr(v), q.stride(0), q.stride(1), q.stride(2),
@@ -490,8 +490,7 @@ def pi_attn_backward_noalloc(q, k, v, gate, k_window: int, pi: int, out, lse, do
                            ("dgate", dgate, (B, H, N))):
         if t.dtype != torch.float32 or tuple(t.shape) != shape or not t.is_contiguous():
             raise ValueError(f"{name} must be a contiguous float32 {list(shape)} tensor")
-    if scale is None:
-        scale = 1.0 / math.sqrt(D)
+    scale = _scale(scale, D)
     st = library().pi_attn_backward_noalloc(
         _dtype_code(q.dtype), B, H, N, D, int(k_window), int(pi), int(bool(causal)),
         _ptr(q), _ptr(k), _ptr(v), q.stride(0), q.stride(1), q.stride(2),
@@ -536,8 +535,7 @@ def pi_attn_decode_step(len_in, q_new, k_new, v_new, k_cache, v_cache, gate, k: 
     if len_out is not None and (len_out.dtype != torch.int32 or tuple(len_out.shape) != (S,)
                                 or not len_out.is_contiguous()):
         raise ValueError("len_out must be a contiguous int32 [S] tensor")
-    if scale is None:
-        scale = 1.0 / math.sqrt(D)
+    scale = _scale(scale, D)
     st = library().pi_attn_decode_step(
         _dtype_code(k_cache.dtype), S, H, D, cap, int(k), int(pi), _ptr(len_in), _ptr(len_out),
         _ptr(q_new), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(gate), gss, gsh,

@@ -141,6 +141,8 @@ int32_t pi_attn_ws_width(int32_t k, int32_t pi, int32_t causal) {
     return m > INT32_MAX ? -1 : (int32_t)m;
 }
 
+float pi_attn_default_scale(int32_t D) { return D < 1 ? 0.0f : 1.0f / sqrtf((float)D); }
+
 int pi_attn_index_set(int32_t n, int32_t k, int32_t pi, int32_t causal, int32_t *idx, void *stream) {
     if (n < 0 || k < 0 || pi < 0) return PI_ATTN_EINVAL;
     if ((int64_t)n * ws_width(k, pi, causal != 0) >= kMaxRows) return PI_ATTN_EINVAL;

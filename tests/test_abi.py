@@ -369,3 +369,12 @@ def test_build_rejects_scratch_users():
     bad = ok.replace("_Z1kv", "_Z1jv").replace("]: 0 ", "]: 28 ")
     assert build.scratch_users(ok) == []
     assert build.scratch_users(ok + bad) == ["_Z1jv (28 bytes/lane)"]
+
+
+@pytest.mark.parametrize("D", [64, 128, 1, 0, -3])
+def test_default_scale(lib, D):
+    """1/sqrt(D) (Sec. 3.2, eq. z), rounded to float32; 0 for D < 1."""
+    import math
+    import numpy as np
+    got = pa.library().pi_attn_default_scale(D)
+    assert got == (float(np.float32(1.0 / math.sqrt(D))) if D >= 1 else 0.0)
