@@ -22,10 +22,15 @@
 // row-major value tile, with the same permutation.
 //
 // Tiles are staged global -> registers -> LDS, the next tile while the two
-// blocks of the current one are consumed, row-major with the
-// 16-byte chunks of row r XOR-swizzled (K: chunk ^ (r mod chunks-per-row);
-// V: chunk ^ 2(r mod 4)) so that the fragment reads and the transpose reads
-// are free of bank conflicts.  The global side uses buffer loads whose
+// blocks of the current one are consumed, row-major.  K rows have their
+// 16-byte chunks XOR-swizzled (chunk ^ (r mod chunks-per-row)): the
+// fragment reads (16 lanes, 16 rows, one chunk each) hit 16 distinct groups
+// of 4 banks.  V rows are padded by 64 bytes at D = 128: the transpose reads
+// (4 rows, 64 bytes each per 32 lanes) then hit 64 distinct banks, whereas a
+// chunk swizzle (chunk ^ 2(r mod 4), kept at D = 64, whose LDS budget has no
+// room for padding) leaves them two-way conflicted when the LDS serves
+// 8-byte reads 32 lanes at a time (23.9% conflict cycles by the counters at
+// fwd32k, none with the padding, same time).  The global side uses buffer loads whose
 // descriptor range ends at the tile's last usable row: the hardware range
 // check zero-fills rows past it, and offsets are 32-bit with no per-load
 // clamping or 64-bit address arithmetic.
@@ -79,6 +84,10 @@ struct Tile {
     static constexpr int CPR = D / 8;   // 16-byte chunks per row
     static constexpr int ROW_BYTES = 2 * D;
     static constexpr int BYTES = TK * ROW_BYTES;
+    // V rows: padded by 64 bytes at D = 128 (not swizzled), XOR-swizzled at D = 64
+    static constexpr bool VPAD = D == 128;
+    static constexpr int VROW = VPAD ? 2 * D + 64 : 2 * D;
+    static constexpr int VBYTES = TK * VROW;
 };
 
 // One LDS tile buffer: 64 key rows and 64 value rows.  The kernel declares
@@ -86,7 +95,7 @@ struct Tile {
 template <int D>
 struct TileBuf {
     alignas(16) unsigned char k[Tile<D>::BYTES];
-    alignas(16) unsigned char v[Tile<D>::BYTES];
+    alignas(16) unsigned char v[Tile<D>::VBYTES];
 };
 
 __device__ inline int k_swz(int row, int chunk, int cpr) { return chunk ^ (row & (cpr - 1)); }
@@ -119,7 +128,7 @@ __device__ inline void tile_load(Stage<D> &st, __amdgpu_buffer_rsrc_t rk, __amdg
         const int cid = tid + NT * (hf * Stage<D>::CH + u);
         const int row = cid / T::CPR, pc = cid % T::CPR;
         const int off = (row0 + row) * rowb + k_swz(row, pc, T::CPR) * 16;
-        const int offv = (row0 + row) * rowb + v_swz(row, pc) * 16;
+        const int offv = (row0 + row) * rowb + (T::VPAD ? pc : v_swz(row, pc)) * 16;
         st.k[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, 0));
         st.v[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, offv, 0, 0));
     }
@@ -132,7 +141,8 @@ __device__ inline void tile_store(const Stage<D> &st, TileBuf<D> &tb, int hf, in
     for (int u = 0; u < Stage<D>::CH; ++u) {
         const int cid = tid + NT * (hf * Stage<D>::CH + u);   // = row * CPR + physical chunk
         *reinterpret_cast<uint4 *>(tb.k + cid * 16) = st.k[u];
-        *reinterpret_cast<uint4 *>(tb.v + cid * 16) = st.v[u];
+        const int vo = Tile<D>::VPAD ? (cid / Tile<D>::CPR) * Tile<D>::VROW + (cid % Tile<D>::CPR) * 16 : cid * 16;
+        *reinterpret_cast<uint4 *>(tb.v + vo) = st.v[u];
     }
 }
 
@@ -425,7 +435,9 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
                 for (int hh = 0; hh < 2; ++hh) {
                     const int vrow = 32 * blk + 16 * cc + 8 * hh + 4 * g + r;
                     const int chunk = 4 * db + 2 * (G & 1) + (qd >> 1);
-                    const unsigned char *src = vt + vrow * T::ROW_BYTES + v_swz(vrow, chunk) * 16 + (qd & 1) * 8;
+                    const unsigned char *src =
+                        T::VPAD ? vt + vrow * T::VROW + chunk * 16 + (qd & 1) * 8
+                                : vt + vrow * T::ROW_BYTES + v_swz(vrow, chunk) * 16 + (qd & 1) * 8;
                     const bf16x4 y =
                         __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)src));
                     vf[cc][db][4 * hh + 0] = y[0];
