@@ -24,12 +24,9 @@ ARCH = "gfx950"
 # Packed-FP32 VALU instructions are disabled for every kernel (hipcc would
 # otherwise form them from float2-style code).  MFMA accumulators are kept in
 # ordinary VGPRs (the softmax rescales them with VALU instructions; the AGPR
-# form would copy them back and forth) -- except in the files listed in
-# AGPR_FORM, whose accumulators are only read at the end and need the
-# accumulation registers for room.
+# form would copy them back and forth).
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
-AGPR_FORM = {"backward_kv_bf16.hip"}
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
           "-I", os.path.join(ROOT, "include")] + DEVICE_FLAGS
 
@@ -65,8 +62,7 @@ def scratch_users(remarks: str) -> list[str]:
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    form = [] if os.path.basename(src) in AGPR_FORM else VGPR_FORM
-    cmd = [hipcc(), *COMMON, *form, *RESOURCE_REMARKS, "-c", src, "-o", obj]
+    cmd = [hipcc(), *COMMON, *VGPR_FORM, *RESOURCE_REMARKS, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")

@@ -1,33 +1,38 @@
 // backward_kv_bf16.hip -- MFMA key pass of the backward for bf16 inputs:
 // dk and dv (D = 64 or 128), fp32 accumulation.
 //
-// A work-group of 4 wavefronts owns 128 keys [j0, j0 + 128) of one (b, h);
-// wavefront w the 32 keys kq0 = j0 + 32w + [0, 32), whose K and V rows stay
-// in registers as B operands.  The queries that hold these keys in their
+// A work-group of 8 wavefronts owns 128 keys [j0, j0 + 128) of one (b, h),
+// as 4 pairs: pair w (wavefronts w and w + 4) the 32 keys
+// kq0 = j0 + 32w + [0, 32).  The queries that hold these keys in their
 // working set stream through LDS in 64-row tiles of Q and dL/dy, with the
 // per-query lse, row term r_t = <dL/dy_t, y_t> and prior bias: first the
 // window band, queries [j0, j0 + 127 + k] (key j is in W_t iff
 // j <= t <= j + k, Sec. 3.2 eq. Nr), then the partner run
 // [j0 + pi, j0 + pi + 128) (key j is the partner of query j + pi when
-// pi > k, Sec. 3.4 eq. Npi), in which wavefront w meets its partners on
-// the diagonal of block w.  The bidirectional mode streams the band
+// pi > k, Sec. 3.4 eq. Npi), in which pair w meets its partners on the
+// diagonal of block w.  The bidirectional mode streams the band
 // [j0 - k, j0 + 127 + k] (|t - j| <= k) and a second partner run
 // [j0 - pi, j0 - pi + 128) (key j is the partner t + pi of query j - pi);
-// rows of a run outside [0, N) are zero and masked.  Per 32-query block, on
-// v_mfma_f32_32x32x16_bf16:
-//   S   = Q K^T      A = Q rows (LDS), B = K^T (registers)
-//   dP  = dO V^T     A = dO rows (LDS), B = V^T (registers)
-// both with lane l holding key l%32 and queries 8i + 4(l/32) + j at slot
-// 4i + j; then alpha^ = exp(delta - lse_t), dS = alpha^ (dP - r_t) (Sec.
-// 3.5 eq. jac; 0 where the clamp saturates), and
-//   dV^T += dO^T alpha^   A = dO^T by LDS transpose reads
-//   dK^T += Q^T dS        A = Q^T by LDS transpose reads
-// with the query order permuted inside each 16-query chunk as the forward
-// permutes V^T against P^T.  dk carries the factor scale.
+// rows of a run outside [0, N) are zero and masked.
 //
-// The dK^T and dV^T accumulators (128 registers at D = 128) are only read
-// at the end, so this file keeps MFMA accumulators in accumulation
-// registers; one work-group per CU.
+// The two wavefronts of a pair split each 32-query block between them, on
+// v_mfma_f32_32x32x16_bf16 with lane l holding key l%32 and queries
+// 8i + 4(l/32) + j at slot 4i + j:
+//   value wavefront (K^T in registers, dV^T accumulator)
+//     S = Q K^T (A = Q rows from LDS), alpha^ = exp(delta - lse_t),
+//     alpha^ to LDS for its partner, then dV^T += dO^T alpha^
+//   key wavefront (V^T in registers, dK^T accumulator)
+//     dP = dO V^T, then with alpha^ from LDS dS = alpha^ (dP - r_t)
+//     (Sec. 3.5 eq. jac; 0 where the clamp saturates), dK^T += Q^T dS
+// The transposed A operands are LDS transpose reads, with the query order
+// permuted inside each 16-query chunk as the forward permutes V^T against
+// P^T.  dk carries the factor scale.  The alpha^ handed over is the float32
+// value the value wavefront computed (sign bit set where the clamp
+// saturates), so the split changes no result.  Each wavefront holds one
+// accumulator (64 registers at D = 128) and one operand block, so two
+// wavefronts fit each SIMD and one's exponentials and conversions run while
+// the other's MFMAs do.  Every block is two phases split by a work-group
+// barrier: S and dP, then dV and dK; alpha^ is double-buffered by block.
 #include "kernels.h"
 #include "pi_common.h"
 
@@ -42,11 +47,10 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr int WAVES = 4;
-constexpr int NT = 64 * WAVES;
-constexpr int BK = 32 * WAVES;   // keys per work-group
+constexpr int PAIRS = 4;
+constexpr int NT = 64 * 2 * PAIRS;
+constexpr int BK = 32 * PAIRS;   // keys per work-group
 constexpr int TQ = 64;           // query rows per LDS tile
-constexpr int BPT = TQ / 32;
 
 template <int D>
 struct Tile {
@@ -62,9 +66,17 @@ template <int D>
 struct QTile {
     alignas(16) unsigned char q[Tile<D>::BYTES];
     alignas(16) unsigned char o[Tile<D>::BYTES];
-    alignas(16) float lse2[TQ];   // (lse_t - lse_shift_t) * log2 e
+    alignas(16) float lse2[TQ];   // (lse_t - lse_shift_t) * log2 e (with the clamp)
     alignas(16) float r[TQ];      // row term
-    alignas(16) float bias[TQ];   // prior bias of this stream (natural log)
+    alignas(16) float bias[TQ];   // with the clamp: prior bias of this stream (natural log);
+                                  // without: that bias * log2 e - lse2, the exponent offset
+};
+
+// alpha^ of one block, handed from each pair's value wavefront to its key
+// wavefront: slot group i (slots 4i..4i+3) of lane l at [i][l], so each
+// 16-byte access of a wavefront covers consecutive addresses.
+struct PBuf {
+    alignas(16) float v[2][PAIRS][4][64][4];   // [block parity][pair][i][lane]
 };
 
 template <int D>
@@ -83,17 +95,13 @@ struct Stage {
 // the k-step (two bases, even and odd steps) and in the dimension block.
 __device__ inline int chunk_x(int row) { return (row >> 2) & 3; }
 
-__device__ inline float other_half(float x) {
-    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return __uint_as_float(__lane_id() < 32 ? p[1] : p[0]);
-}
-
 template <int D, bool CLAMP, bool BIDIR>
-__global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, int n_kt, int64_t n_logical) {
+__global__ __launch_bounds__(NT) void backward_kv_bf16_kernel(BwdParams bp, int n_kt, int64_t n_logical) {
     using T = Tile<D>;
     constexpr int KS = T::KS, DB = T::DB;
     const FwdParams &p = bp.f;
     __shared__ QTile<D> tA, tB;
+    __shared__ PBuf pbuf;
     const int64_t logical = xcd_remap(blockIdx.x, n_logical);
     if (logical < 0) return;
     const int kt = (int)(logical % n_kt);
@@ -102,7 +110,9 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
 
     const int tid = threadIdx.x;
     const int lane = __lane_id();
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int w = wv % PAIRS;               // pair
+    const bool keyw = wv >= PAIRS;          // key wavefront (else value wavefront)
     const int g = lane >> 5, c = lane & 31;
     const int N = p.N, kw = p.k, pi = p.pi;
     // absolute positions: keys [kvpos0, NK) (this pass's keys), query rows
@@ -118,29 +128,24 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
     const int64_t sn = p.sn, ksn = p.ksn, osn = bp.osn;
     const __bf16 *qp = (const __bf16 *)p.q + b * p.sb + h * p.sh - (int64_t)QS * sn;
     const int64_t kvbase = b * p.ksb + h * p.ksh - (int64_t)p.kvpos0 * ksn;
-    const __bf16 *kp = (const __bf16 *)p.k_ptr + kvbase;
-    const __bf16 *vp = (const __bf16 *)p.v + kvbase;
     const __bf16 *op = (const __bf16 *)bp.dout + b * bp.osb + h * bp.osh - (int64_t)QS * osn;
     const int64_t rbase = bh * (int64_t)(p.qend - QS) - QS;   // lse, row terms [B][H][qend - qpos0]
     const int64_t obase = bh * (int64_t)N - p.kvpos0;         // dk, dv [B][H][N]
     const bool exact = CLAMP;
     const float c2 = p.scale * kLog2e;
 
-    // K^T and V^T B operands of this wavefront's keys (zero past N).
-    bf16x8 kf[KS], vf[KS];
+    // B operand of this wavefront's keys: K^T (value wavefront) or V^T (key
+    // wavefront), zero past N; and its accumulator, dV^T or dK^T.
+    const __bf16 *kvp = (const __bf16 *)(keyw ? p.v : p.k_ptr) + kvbase;
+    bf16x8 kvf[KS];
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-        const bf16x8 kv = *reinterpret_cast<const bf16x8 *>(kp + jq * ksn + 16 * s + 8 * g);
-        const bf16x8 vv = *reinterpret_cast<const bf16x8 *>(vp + jq * ksn + 16 * s + 8 * g);
-        kf[s] = j_ok ? kv : bf16x8{};
-        vf[s] = j_ok ? vv : bf16x8{};
+        const bf16x8 x = *reinterpret_cast<const bf16x8 *>(kvp + jq * ksn + 16 * s + 8 * g);
+        kvf[s] = j_ok ? x : bf16x8{};
     }
-    f32x16 dk[DB], dv[DB];
+    f32x16 acc[DB];
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
-        dk[db] = f32x16{};
-        dv[db] = f32x16{};
-    }
+    for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
 
     // Query streams (kind 0 band, 1 the run of queries whose partner t - pi
     // is one of these keys, 2 (bidirectional) the run whose partner t + pi
@@ -208,106 +213,144 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
         }
         if (tid < TQ) {
             const FusionBias fb = fusion_bias(st.gl, exact);
-            tb.lse2[tid] = (st.lse - fb.lse_shift) * kLog2e;
+            const float l2 = (st.lse - fb.lse_shift) * kLog2e;
+            tb.lse2[tid] = l2;
             tb.r[tid] = st.r;
             const float bias_local = fb.local, bias_partner = fb.partner;
-            tb.bias[tid] = st.band ? bias_local : bias_partner;
+            const float bias = st.band ? bias_local : bias_partner;
+            tb.bias[tid] = CLAMP ? bias : bias * kLog2e - l2;
         }
     };
 
-    // One 32-query block (rows 32 blk.. of tile tb, first query t0b) of a
-    // stream of the given kind.
-    auto block = [&](const QTile<D> &tb, int t0b, int blk, int kind, int lim) {
+    // Whether pair w meets the 32-query block starting at t0b, and whether
+    // the block needs masking.
+    auto active = [&](int t0b, int blk, int kind, int lim) {
+        if (kind != 0) return blk == (w & 1) && t0b == (BIDIR && kind == 2 ? kq0 - pi : kq0 + pi);
+        if constexpr (BIDIR) return t0b < lim && kq0 < NK && t0b - (kq0 + 31) <= kw && t0b + 31 >= kq0 - kw;
+        return t0b < lim && kq0 < NK && t0b <= kq0 + 31 + kw && t0b + 31 >= kq0;
+    };
+    auto edge_block = [&](int t0b, int kind) {
         const bool partner = kind != 0;
-        bool act;
-        if (partner) {
-            act = blk == (w & 1) && t0b == (BIDIR && kind == 2 ? kq0 - pi : kq0 + pi);
-        } else if constexpr (BIDIR) {
-            act = t0b < lim && kq0 < NK && t0b - (kq0 + 31) <= kw && t0b + 31 >= kq0 - kw;
-        } else {
-            act = t0b < lim && kq0 < NK && t0b <= kq0 + 31 + kw && t0b + 31 >= kq0;
-        }
-        if (!act) return;
-        const bool edge = BIDIR ? partner || !(t0b + 31 - kq0 <= kw && kq0 + 31 - t0b <= kw) || t0b + 31 >= QE ||
-                                      kq0 + 31 >= NK || t0b < QS
-                                : partner || !(t0b >= kq0 + 31 && t0b + 31 <= kq0 + kw) || t0b + 31 >= QE ||
-                                      kq0 + 31 >= NK;
+        return BIDIR ? partner || !(t0b + 31 - kq0 <= kw && kq0 + 31 - t0b <= kw) || t0b + 31 >= QE ||
+                           kq0 + 31 >= NK || t0b < QS
+                     : partner || !(t0b >= kq0 + 31 && t0b + 31 <= kq0 + kw) || t0b + 31 >= QE || kq0 + 31 >= NK;
+    };
+
+    // First phase of a block (rows 32 blk.. of tile tb, first query t0b):
+    // the value wavefront forms alpha^ (to pb for dV, to LDS for its
+    // partner), the key wavefront dP (to dp).
+    auto phase1 = [&](const QTile<D> &tb, int t0b, int blk, int kind, bool edge, int par, bf16x8 (&pb)[2],
+                      f32x16 &dp) {
         // rows of this block (A operands: query l%32, dims 16s + 8g): chunk
         // (2s + g) ^ x = 2(s ^ (x >> 1)) + (g ^ (x & 1)), x = chunk_x(row)
         const int xr = chunk_x(32 * blk + c);
         const int rb = (32 * blk + c) * T::ROW + 16 * (g ^ (xr & 1));
         const int rbo[2] = {rb + 32 * (xr >> 1), rb - 32 * (xr >> 1)};   // even, odd k-steps
-        bf16x8 qa[KS], oa[KS];
+        const unsigned char *src = keyw ? tb.o : tb.q;
+        bf16x8 ra[KS];
 #pragma unroll
-        for (int s = 0; s < KS; ++s) {
-            qa[s] = *reinterpret_cast<const bf16x8 *>(tb.q + rbo[s & 1] + 32 * s);
-            oa[s] = *reinterpret_cast<const bf16x8 *>(tb.o + rbo[s & 1] + 32 * s);
+        for (int s = 0; s < KS; ++s) ra[s] = *reinterpret_cast<const bf16x8 *>(src + rbo[s & 1] + 32 * s);
+        f32x16 sc = {};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ra[s], kvf[s], sc, 0, 0, 0);
+        if (keyw) {
+            dp = sc;
+            return;
         }
-        f32x16 sc = {}, dp = {};
-#pragma unroll
-        for (int s = 0; s < KS; ++s) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[s], kf[s], sc, 0, 0, 0);
-#pragma unroll
-        for (int s = 0; s < KS; ++s) dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(oa[s], vf[s], dp, 0, 0, 0);
-        // logits (log2 units) of this lane's queries 8i + 4g + jj, slot 4i + jj
-        float dl2[16];
+        // alpha^ of this lane's queries 8i + 4g + jj, slot 4i + jj
         bool cut[16];
+        float pr[16];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const f32x4 b4 = *reinterpret_cast<const f32x4 *>(tb.bias + 32 * blk + 8 * i + 4 * g);
+            if constexpr (CLAMP) {
+                const f32x4 l4 = *reinterpret_cast<const f32x4 *>(tb.lse2 + 32 * blk + 8 * i + 4 * g);
 #pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-                const int e = 4 * i + jj;
-                cut[e] = false;
-                if constexpr (CLAMP) {
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int e = 4 * i + jj;
                     const float dl = fminf(fmaxf(sc[e] * p.scale + b4[jj], -p.clamp), p.clamp);
                     cut[e] = fabsf(dl) >= p.clamp;
-                    dl2[e] = dl * kLog2e;
-                } else {
-                    dl2[e] = __builtin_fmaf(sc[e], c2, b4[jj] * kLog2e);
+                    pr[e] = __builtin_amdgcn_exp2f(dl * kLog2e - l4[jj]);
+                }
+            } else {
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int e = 4 * i + jj;
+                    cut[e] = false;
+                    pr[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[e], c2, b4[jj]));
                 }
             }
         }
-        // Edge blocks: entries outside the working set get -inf, by
-        // branch-free tests on d = t - j (window, or the partner offset of
-        // this stream) and on the held query range.
+        // Edge blocks: the working-set entries of this lane's key j among the
+        // block's queries are one run of rows, the window [j, j + k] (|t - j|
+        // <= k bidirectionally) or the single partner query of this stream,
+        // cut to the held rows [QS, QE) and to the block; bit r of keep marks
+        // row 4g + r of the block (this lane's rows 4g + 8i + jj at bit
+        // 8i + jj), and alpha^ of the other entries is cleared.  The empty
+        // asm keeps this a branch that interior blocks skip.
         if (edge) {
-            const int tb0 = t0b + 4 * g;
-            const int ptgt = (BIDIR && kind == 2) ? -pi : pi;
+            asm volatile("" ::: "memory");
+            int lo, hi;
+            if (kind == 0) {
+                lo = BIDIR ? j - kw : j;
+                hi = j + kw;
+            } else {
+                lo = hi = j + ((BIDIR && kind == 2) ? -pi : pi);
+            }
+            lo = max(lo, max(QS, t0b));
+            hi = min(hi, min(QE - 1, t0b + 31));
+            const int n = hi - lo + 1;
+            uint32_t keep = !j_ok || n <= 0 ? 0u : n >= 32 ? ~0u : ((1u << n) - 1u) << (lo - t0b);
+            keep >>= 4 * g;
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int t = tb0 + 8 * (e >> 2) + (e & 3), d = t - j;
-                const bool in_w = BIDIR ? (d <= kw) & (d >= -kw) : (d >= 0) & (d <= kw);
-                const bool in_p = d == ptgt;
-                bool ok = ((partner & in_p) | (!partner & in_w)) & (t < QE) & j_ok;
-                if constexpr (BIDIR) ok = ok & (t >= QS);
-                dl2[e] = ok ? dl2[e] : -INFINITY;
+            for (int e = 0; e < 16; ++e) {   // all bits of pr[e], or none
+                const int bit = __builtin_amdgcn_sbfe((int)keep, 8 * (e >> 2) + (e & 3), 1);
+                pr[e] = __int_as_float(__float_as_int(pr[e]) & bit);
             }
         }
-        float pr[16], ds[16];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int qi = 32 * blk + 8 * i + 4 * g;
-            const f32x4 l4 = *reinterpret_cast<const f32x4 *>(tb.lse2 + qi);
-            const f32x4 r4 = *reinterpret_cast<const f32x4 *>(tb.r + qi);
+            f32x4 h4;
 #pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-                const int e = 4 * i + jj;
-                const float wgt = __builtin_amdgcn_exp2f(dl2[e] - l4[jj]);
-                pr[e] = wgt;
-                ds[e] = cut[e] ? 0.0f : wgt * (dp[e] - r4[jj]);
-            }
+            for (int jj = 0; jj < 4; ++jj) h4[jj] = cut[4 * i + jj] ? -pr[4 * i + jj] : pr[4 * i + jj];
+            *reinterpret_cast<f32x4 *>(&pbuf.v[par][w][i][lane][0]) = h4;
         }
-        bf16x8 pb[2], db8[2];
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                pb[cc][e] = (__bf16)pr[8 * cc + e];
-                db8[cc][e] = (__bf16)ds[8 * cc + e];
+            for (int e = 0; e < 8; ++e) pb[cc][e] = (__bf16)pr[8 * cc + e];
+        }
+    };
+
+    // Second phase: dV^T += dO^T alpha^ (value wavefront) or, with alpha^
+    // from LDS, dK^T += Q^T dS (key wavefront).
+    auto phase2 = [&](const QTile<D> &tb, int blk, int par, const bf16x8 (&pb)[2], const f32x16 &dp) {
+        bf16x8 bop[2];
+        if (keyw) {
+            float ds[16];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const f32x4 a4 = *reinterpret_cast<const f32x4 *>(&pbuf.v[par][w][i][lane][0]);
+                const f32x4 r4 = *reinterpret_cast<const f32x4 *>(tb.r + 32 * blk + 8 * i + 4 * g);
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int e = 4 * i + jj;
+                    const float d = a4[jj] * (dp[e] - r4[jj]);
+                    ds[e] = CLAMP && a4[jj] < 0.0f ? 0.0f : d;
+                }
             }
+#pragma unroll
+            for (int cc = 0; cc < 2; ++cc) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) bop[cc][e] = (__bf16)ds[8 * cc + e];
+            }
+        } else {
+            bop[0] = pb[0];
+            bop[1] = pb[1];
         }
         // transposed tiles (A operands: dim 32db + l%32, queries permuted)
         // rows 32 blk + 4g + rr + 8hh + 16cc, chunks 4d + (j ^ (g + 2hh))
+        const unsigned char *src = keyw ? tb.q : tb.o;
         const int G = lane >> 4, rr = (lane >> 2) & 3, qd = lane & 3;
         const int jq = 2 * (G & 1) + (qd >> 1);
         const int toff[2] = {(32 * blk + 4 * g + rr) * T::ROW + 16 * (jq ^ g) + (qd & 1) * 8,
@@ -316,66 +359,66 @@ __global__ __launch_bounds__(NT, 1) void backward_kv_bf16_kernel(BwdParams bp, i
         for (int cc = 0; cc < 2; ++cc) {
 #pragma unroll
             for (int d = 0; d < DB; ++d) {
-                bf16x8 ao, aq;
+                bf16x8 at;
 #pragma unroll
                 for (int hh = 0; hh < 2; ++hh) {
                     const int off = toff[hh] + 16 * cc * T::ROW + 64 * d;
-                    const bf16x4 yo = __builtin_bit_cast(
-                        bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(tb.o + off)));
-                    const bf16x4 yq = __builtin_bit_cast(
-                        bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(tb.q + off)));
+                    const bf16x4 y = __builtin_bit_cast(
+                        bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(src + off)));
 #pragma unroll
-                    for (int x = 0; x < 4; ++x) {
-                        ao[4 * hh + x] = yo[x];
-                        aq[4 * hh + x] = yq[x];
-                    }
+                    for (int x = 0; x < 4; ++x) at[4 * hh + x] = y[x];
                 }
-                dv[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ao, pb[cc], dv[d], 0, 0, 0);
-                dk[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, db8[cc], dk[d], 0, 0, 0);
+                acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(at, bop[cc], acc[d], 0, 0, 0);
             }
         }
     };
 
+    // One 64-row tile (cur) of the combined stream; the staged next tile goes
+    // into nxt between the two blocks (nxt's last reader, the previous
+    // tile's second block, finished before this tile's first barrier).
+    Stage<D> st;
+    auto tile = [&](const QTile<D> &cur, QTile<D> &nxt, int m) {
+        const int t0 = tile_start(m), kind = tile_kind(m), lim = tile_end(m);
+        bf16x8 pb[2];
+        f32x16 dp;
+        const bool a0 = active(t0, 0, kind, lim), a1 = active(t0 + 32, 1, kind, lim);
+        if (a0) phase1(cur, t0, 0, kind, edge_block(t0, kind), 0, pb, dp);
+        __syncthreads();
+        if (a0) phase2(cur, 0, 0, pb, dp);
+        if (a1) phase1(cur, t0 + 32, 1, kind, edge_block(t0 + 32, kind), 1, pb, dp);
+        if (m + 1 < ntiles) {
+            store(st, nxt);
+            if (m + 2 < ntiles) load(st, m + 2);
+        }
+        __syncthreads();
+        if (a1) phase2(cur, 1, 1, pb, dp);
+    };
+
     if (ntiles > 0) {
-        Stage<D> st;
         load(st, 0);
         store(st, tA);
+        if (ntiles > 1) load(st, 1);
         __syncthreads();
         for (int m = 0; m < ntiles; m += 2) {
-            // tile m in tA; stage m+1 into tB while it is consumed
-            if (m + 1 < ntiles) load(st, m + 1);
-#pragma unroll
-            for (int blk = 0; blk < BPT; ++blk)
-                block(tA, tile_start(m) + 32 * blk, blk, tile_kind(m), tile_end(m));
+            tile(tA, tB, m);
             if (m + 1 >= ntiles) break;
-            store(st, tB);
-            __syncthreads();
-            if (m + 2 < ntiles) load(st, m + 2);
-#pragma unroll
-            for (int blk = 0; blk < BPT; ++blk)
-                block(tB, tile_start(m + 1) + 32 * blk, blk, tile_kind(m + 1), tile_end(m + 1));
-            if (m + 2 >= ntiles) break;
-            store(st, tA);
-            __syncthreads();
+            tile(tB, tA, m + 1);
         }
     }
 
     // ---- store: lane (c, g) holds dims 32db + 8i + 4g + [0, 4) of key c ----
     if (j_ok) {
         const int64_t row = obase + j;
-        float *dkp = bp.dk + row * D, *dvp = bp.dv + row * D;
+        float *dst = (keyw ? bp.dk : bp.dv) + row * D;
+        const float f = keyw ? p.scale : 1.0f;
 #pragma unroll
         for (int d = 0; d < DB; ++d) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                f32x4 a, v4;
+                f32x4 a;
 #pragma unroll
-                for (int x = 0; x < 4; ++x) {
-                    a[x] = dk[d][4 * i + x] * p.scale;
-                    v4[x] = dv[d][4 * i + x];
-                }
-                *reinterpret_cast<f32x4 *>(dkp + 32 * d + 8 * i + 4 * g) = a;
-                *reinterpret_cast<f32x4 *>(dvp + 32 * d + 8 * i + 4 * g) = v4;
+                for (int x = 0; x < 4; ++x) a[x] = acc[d][4 * i + x] * f;
+                *reinterpret_cast<f32x4 *>(dst + 32 * d + 8 * i + 4 * g) = a;
             }
         }
     }
@@ -394,12 +437,10 @@ template <int D, bool BIDIR>
 hipError_t launch_kvc(const BwdParams &p, hipStream_t stream) {
     return p.f.clamp > 0.0f ? launch_kv<D, true, BIDIR>(p, stream) : launch_kv<D, false, BIDIR>(p, stream);
 }
-
 }  // namespace
 
 hipError_t launch_backward_kv_bf16(const BwdParams &p, hipStream_t stream) {
     if (p.f.D == 64) return p.f.causal ? launch_kvc<64, false>(p, stream) : launch_kvc<64, true>(p, stream);
     return p.f.causal ? launch_kvc<128, false>(p, stream) : launch_kvc<128, true>(p, stream);
 }
-
 }  // namespace pi_attn
