@@ -283,15 +283,17 @@ def measured_traffic(digest, path=PROFILE_TRAFFIC):
 def measured_counters(digest, path, sec):
     """Counter figures of the same summary for the bench line: the MFMA busy
     fraction (SQ_VALU_MFMA_BUSY_CYCLES over the SIMD-cycles of the kernel's
-    active time), the LDS bank-conflict fraction, the shader clock the
-    kernel ran at (GRBM_GUI_ACTIVE cycles over its traced duration), and the
-    measured DRAM rate (the counted HBM bytes over this run's launch time).
-    Empty when the summary does not match the kernel sources."""
+    active time), the LDS bank-conflict fraction, an upper bound on the
+    shader clock the kernel ran at (GRBM_GUI_ACTIVE cycles, whose counting
+    window can extend past the dispatch, over its traced duration; taken
+    from dispatches of at least 300 us only), and the measured DRAM rate
+    (the counted HBM bytes over this run's launch time).  Empty when the
+    summary does not match the kernel sources."""
     rec = read_profile(digest, path)
     if rec is None:
         return {}
     out = {}
-    for key in ("mfma_busy", "lds_bank_conflict", "sclk_mhz"):
+    for key in ("mfma_busy", "lds_bank_conflict", "sclk_mhz_max"):
         if key in rec:
             out[key] = float(rec[key])
     if "hbm_bytes_per_launch" in rec:
