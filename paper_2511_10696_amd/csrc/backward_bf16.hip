@@ -271,12 +271,27 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
             a_par += cut ? 0.0f : wgt * dpd;
             b_par += cut ? 0.0f : wgt;
         }
-        // dq += dd * k_p over this lane's dims 32db + 8i + 4g + [0, 4)
+        // dq += dd * k_p over this lane's dims 32db + 8i + 4g + [0, 4): the
+        // 8-dim group m = 4db + i, whose half 4g..4g+3 this lane needs, is
+        // held whole by lane (c, m & 1) in kpf[m >> 1]; each lane keeps its
+        // own half of its groups and takes the other half from the other
+        // half of the wavefront
+        const auto kh = [&](int s2) { return __builtin_bit_cast(uint4, has_p ? kpf[s2] : bf16x8{}); };
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
+        for (int s2 = 0; s2 < KS; ++s2) {
+            const uint4 own = kh(s2);
+            // lane g = 0 sends dims 4..7 of its group, lane g = 1 dims 0..3
+            const uint2 send = g == 0 ? make_uint2(own.z, own.w) : make_uint2(own.x, own.y);
+            const uint2 recv = make_uint2(__float_as_uint(other_half(__uint_as_float(send.x))),
+                                          __float_as_uint(other_half(__uint_as_float(send.y))));
+            // groups 2 s2 (held by g = 0) and 2 s2 + 1 (held by g = 1)
+            const uint2 lo = g == 0 ? make_uint2(own.x, own.y) : recv;   // group 2 s2, dims 4g..4g+3
+            const uint2 hi = g == 0 ? recv : make_uint2(own.z, own.w);   // group 2 s2 + 1
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const uint2 raw = *reinterpret_cast<const uint2 *>(kp + prc * ksn + 32 * db + 8 * i + 4 * g);
+            for (int half = 0; half < 2; ++half) {
+                const int m = 2 * s2 + half;
+                const uint2 raw = half ? hi : lo;
+                const int db = m >> 2, i = m & 3;
                 dq[db][4 * i + 0] += dd * __uint_as_float(raw.x << 16);
                 dq[db][4 * i + 1] += dd * __uint_as_float(raw.x & 0xffff0000u);
                 dq[db][4 * i + 2] += dd * __uint_as_float(raw.y << 16);

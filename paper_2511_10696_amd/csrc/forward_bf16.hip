@@ -312,36 +312,33 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
 
     // Partner rows: A-operand row c of the wavefront is row q0 + c - pi, the
     // partner of query q0 + c; the accumulator seed is that row's value, of
-    // which lane (c, g) holds dims 32db + 8i + 4g + [0, 4).
+    // which lane (c, g) holds dims 32db + 8i + 4g + [0, 4).  Both rows are
+    // read in the layout of the query fragments (dims 16s + 8g + [0, 8));
+    // the value row is then regrouped by an exchange between the two halves
+    // of the wavefront (seed_layout).
     const int prow = t - pi;
     const bool has_p = partner_enabled(kw, pi) && prow >= 0 && t_ok;   // depends on c only
     const bool any_p = __builtin_amdgcn_ballot_w64(has_p) != 0;       // wave-uniform
     const int prc = has_p ? prow : p.kvpos0;
-    bf16x8 kpf[W::KS];
-    uint2 vraw[W::DB][4];
+    bf16x8 kpf[W::KS], vpf[W::KS];
     if (any_p) {
 #pragma unroll
-        for (int s = 0; s < W::KS; ++s) kpf[s] = *reinterpret_cast<const bf16x8 *>(kp + prc * ksn + 16 * s + 8 * g);
-#pragma unroll
-        for (int db = 0; db < W::DB; ++db)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                vraw[db][i] = *reinterpret_cast<const uint2 *>(vp + prc * ksn + 32 * db + 8 * i + 4 * g);
+        for (int s = 0; s < W::KS; ++s) {
+            kpf[s] = *reinterpret_cast<const bf16x8 *>(kp + prc * ksn + 16 * s + 8 * g);
+            vpf[s] = *reinterpret_cast<const bf16x8 *>(vp + prc * ksn + 16 * s + 8 * g);
+        }
     }
     // Bidirectional: the second partner t + pi, loaded the same way.
     const bool has_f = BIDIR && t_ok && partner_fwd_of(t, kw, pi, NS) >= 0;
     const bool any_f = BIDIR && __builtin_amdgcn_ballot_w64(has_f) != 0;
     const int frc = has_f ? t + pi : p.kvpos0;
-    bf16x8 kff[W::KS];
-    uint2 vfraw[W::DB][4];
+    bf16x8 kff[W::KS], vff[W::KS];
     if (any_f) {
 #pragma unroll
-        for (int s = 0; s < W::KS; ++s) kff[s] = *reinterpret_cast<const bf16x8 *>(kp + frc * ksn + 16 * s + 8 * g);
-#pragma unroll
-        for (int db = 0; db < W::DB; ++db)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                vfraw[db][i] = *reinterpret_cast<const uint2 *>(vp + frc * ksn + 32 * db + 8 * i + 4 * g);
+        for (int s = 0; s < W::KS; ++s) {
+            kff[s] = *reinterpret_cast<const bf16x8 *>(kp + frc * ksn + 16 * s + 8 * g);
+            vff[s] = *reinterpret_cast<const bf16x8 *>(vp + frc * ksn + 16 * s + 8 * g);
+        }
     }
 #pragma unroll
     for (int hf = 0; hf < BPT; ++hf) tile_load<D>(st0[hf], rk, rv, rowb, 0, hf, tid);
@@ -378,6 +375,23 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
     ws.lb = ws.l;   // the partner weights enter the accumulator unrounded
     // Lanes without that partner contribute exactly 0 (their loads read a
     // clamped row whose data is not used, not even multiplied by 0).
+    // The value row in the accumulator layout: the 8-dim group m = 4db + i,
+    // of which this lane needs dims 4g..4g+3, is held whole by lane
+    // (c, m & 1) in vf[m >> 1]; each lane keeps its own half of its groups
+    // and takes the other half from the other half of the wavefront.
+    auto seed_layout = [&](const bf16x8 (&vf)[W::KS], uint2 (&vr)[W::DB][4]) {
+#pragma unroll
+        for (int s2 = 0; s2 < W::KS; ++s2) {
+            const uint4 own = __builtin_bit_cast(uint4, vf[s2]);
+            // lane g = 0 sends dims 4..7 of its group, lane g = 1 dims 0..3
+            const uint2 send = g == 0 ? make_uint2(own.z, own.w) : make_uint2(own.x, own.y);
+            const uint2 recv = make_uint2(__float_as_uint(other_half(__uint_as_float(send.x))),
+                                          __float_as_uint(other_half(__uint_as_float(send.y))));
+            const int m0 = 2 * s2, m1 = 2 * s2 + 1;
+            vr[m0 >> 2][m0 & 3] = g == 0 ? make_uint2(own.x, own.y) : recv;
+            vr[m1 >> 2][m1 & 3] = g == 0 ? recv : make_uint2(own.z, own.w);
+        }
+    };
     auto seed = [&](uint2 (&vr)[W::DB][4], float wt, bool has, bool add) {
 #pragma unroll
         for (int db = 0; db < W::DB; ++db) {
@@ -394,8 +408,28 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
             }
         }
     };
+    uint2 vraw[W::DB][4];
+    if (any_p) {
+        seed_layout(vpf, vraw);
+    } else {
+#pragma unroll
+        for (int db = 0; db < W::DB; ++db)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) vraw[db][i] = make_uint2(0, 0);
+    }
     seed(vraw, wp, has_p, false);
-    if constexpr (BIDIR) seed(vfraw, wf, has_f, true);
+    if constexpr (BIDIR) {
+        uint2 vfraw[W::DB][4];
+        if (any_f) {
+            seed_layout(vff, vfraw);
+        } else {
+#pragma unroll
+            for (int db = 0; db < W::DB; ++db)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) vfraw[db][i] = make_uint2(0, 0);
+        }
+        seed(vfraw, wf, has_f, true);
+    }
 #pragma unroll
     for (int hf = 0; hf < BPT; ++hf) tile_store<D>(st0[hf], tA, hf, tid);
     __syncthreads();
