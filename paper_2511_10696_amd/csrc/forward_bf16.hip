@@ -21,8 +21,9 @@
 // and A = V^T comes from the LDS transpose read (ds_read_b64_tr_b16) of the
 // row-major value tile, with the same permutation.
 //
-// Tiles are staged global -> registers -> LDS, the next tile while the two
-// blocks of the current one are consumed, row-major.  K rows have their
+// Tiles go from global memory straight into LDS (buffer loads with the LDS
+// destination, no staging registers), the next tile while the two blocks
+// of the current one are consumed, row-major.  K rows have their
 // 16-byte chunks XOR-swizzled (chunk ^ (r mod chunks-per-row)): the
 // fragment reads (16 lanes, 16 rows, one chunk each) hit 16 distinct groups
 // of 4 banks.  V rows are padded by 64 bytes at D = 128: the transpose reads
@@ -71,12 +72,12 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int WAVES = 4;
 constexpr int NT = 64 * WAVES;   // threads per work-group
 constexpr int BM = 32 * WAVES;   // queries per work-group
-constexpr int TK = 64;           // key rows per LDS tile
-constexpr int BPT = TK / 32;     // 32-key blocks per tile
+constexpr int TK = 64;           // key rows per LDS tile (two 32-key blocks)
 constexpr float kTau = 8.0f;     // lazy-max threshold, log2 units
 
 template <int D>
@@ -102,47 +103,70 @@ __device__ inline int k_swz(int row, int chunk, int cpr) { return chunk ^ (row &
 __device__ inline int v_swz(int row, int chunk) { return chunk ^ ((row & 3) << 1); }
 
 
-// Register staging of half a 64-row tile.  Chunk u of half hf for thread i
-// is tile chunk cid = i + NT*(hf*CH + u): physical chunk cid % CPR of tile
-// row cid / CPR, so consecutive threads read consecutive 16 bytes of a row
-// (the swizzle only permutes the chunks of a row among themselves).
-template <int D>
-struct Stage {
-    static constexpr int CH = TK * Tile<D>::CPR / NT / BPT;   // chunks per thread, tensor and part
-    uint4 k[CH];
-    uint4 v[CH];
-};
+// Fetch tile rows [row0, row0 + TK) (counted from the window start) into
+// LDS buffer tb with buffer loads that write LDS directly: 16 bytes per
+// lane, the 64 lanes of one instruction filling 1 KB of consecutive LDS,
+// each lane's source offset chosen so that the bytes land in the tile's
+// layout.  Instruction u fills bytes [1024u, 1024u + 1024) of the K or the V
+// buffer; wavefront w issues u = w, w + WAVES, ...  K: LDS chunk pc of row r
+// holds global chunk k_swz(r, pc).  V: D = 128 rows are padded to VROW and
+// the pad chunks take an out-of-range offset (written as zeros); D = 64 rows
+// hold global chunk v_swz(r, pc) at chunk pc.  Offsets past the rows the
+// descriptor covers read as zeros.
+constexpr int kOutOfRange = 1 << 30;   // past any tile range the descriptors describe
 
-// Load half hf of the tile whose first row is `row0` rows past the window
-// start, through buffer descriptors that begin at the window start and end at
-// the last row the query tile may use: rows beyond it read as zeros, so no
-// data of a row later than every query of the tile is ever used (a masked
-// weight is 0, but 0 times a non-finite value is not).  Offsets are 32-bit
-// and span at most k + BM rows; `rowb` is the row stride in bytes.
-template <int D>
-__device__ inline void tile_load(Stage<D> &st, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv, int rowb,
-                                 int row0, int hf, int tid) {
-    using T = Tile<D>;
-#pragma unroll
-    for (int u = 0; u < Stage<D>::CH; ++u) {
-        const int cid = tid + NT * (hf * Stage<D>::CH + u);
-        const int row = cid / T::CPR, pc = cid % T::CPR;
-        const int off = (row0 + row) * rowb + k_swz(row, pc, T::CPR) * 16;
-        const int offv = (row0 + row) * rowb + (T::VPAD ? pc : v_swz(row, pc)) * 16;
-        st.k[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, 0));
-        st.v[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, offv, 0, 0));
-    }
+// Raw buffer descriptor over nbytes from base (stride 0; word 3 is the gfx9
+// raw-buffer format: 32-bit data, range checked).
+__device__ inline u32x4 raw_rsrc(const void *base, int nbytes) {
+    const unsigned long long a = (unsigned long long)base;
+    u32x4 r;
+    r.x = __builtin_amdgcn_readfirstlane((unsigned)a);
+    r.y = __builtin_amdgcn_readfirstlane((unsigned)(a >> 32) & 0xffffu);
+    r.z = __builtin_amdgcn_readfirstlane((unsigned)nbytes);
+    r.w = 0x00020000u;
+    return r;
 }
 
-// Store half hf of a staged tile.
+// One 16-byte-per-lane buffer load into LDS at lds + 16 * lane.  Issued as
+// inline asm: the compiler then keeps no count of it (its own waits for
+// LDS reads after such a load would wait for every fetch in flight); the
+// kernel waits for it with an explicit counter before the barrier that
+// publishes the tile.
+__device__ inline void lds_fetch16(u32x4 rsrc, int voff, void *lds) {
+    const unsigned m0 = __builtin_amdgcn_readfirstlane(
+        (unsigned)(uintptr_t)(__attribute__((address_space(3))) void *)lds);
+    asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff), "s"(rsrc), "{m0}"(m0) : "memory");
+}
+
 template <int D>
-__device__ inline void tile_store(const Stage<D> &st, TileBuf<D> &tb, int hf, int tid) {
+struct Fetch {
+    static constexpr int KI = TK * Tile<D>::CPR / 64;   // instructions per K tile
+    static constexpr int VU = Tile<D>::VROW / 16;       // LDS chunks per V row
+    static constexpr int VI = TK * VU / 64;             // instructions per V tile
+};
+
+template <int D>
+__device__ inline void tile_fetch(TileBuf<D> &tb, u32x4 rk, u32x4 rv, int rowb, int row0, int w, int lane) {
+    using T = Tile<D>;
+    using F = Fetch<D>;
+    static_assert(F::KI % WAVES == 0 && TK * T::CPR % 64 == 0 && TK * F::VU % 64 == 0, "tile fetch shape");
 #pragma unroll
-    for (int u = 0; u < Stage<D>::CH; ++u) {
-        const int cid = tid + NT * (hf * Stage<D>::CH + u);   // = row * CPR + physical chunk
-        *reinterpret_cast<uint4 *>(tb.k + cid * 16) = st.k[u];
-        const int vo = Tile<D>::VPAD ? (cid / Tile<D>::CPR) * Tile<D>::VROW + (cid % Tile<D>::CPR) * 16 : cid * 16;
-        *reinterpret_cast<uint4 *>(tb.v + vo) = st.v[u];
+    for (int u0 = 0; u0 < F::KI; u0 += WAVES) {
+        const int u = u0 + w, pidx = 64 * u + lane;
+        const int row = pidx / T::CPR, pc = pidx % T::CPR;
+        const int off = (row0 + row) * rowb + k_swz(row, pc, T::CPR) * 16;
+        lds_fetch16(rk, off, tb.k + 1024 * u);
+    }
+#pragma unroll
+    for (int u0 = 0; u0 < F::VI; u0 += WAVES) {
+        const int u = u0 + w;
+        if (u < F::VI) {   // wave-uniform
+            const int pidx = 64 * u + lane;
+            const int row = pidx / F::VU, pc = pidx % F::VU;
+            const int off = T::VPAD ? (pc < T::CPR ? (row0 + row) * rowb + pc * 16 : kOutOfRange)
+                                    : (row0 + row) * rowb + v_swz(row, pc) * 16;
+            lds_fetch16(rv, off, tb.v + 1024 * u);
+        }
     }
 }
 
@@ -288,18 +312,11 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
     const int ntiles = (kend - kb0 + TK - 1) / TK;
     // ---- prologue: every load is issued before any is waited for ----------
     // (the query fragments, the gate logit, the partner key/value rows, then
-    // the first tile), so the prologue costs one memory round trip; loads
-    // complete in issue order, so the partner scoring starts while the first
-    // tile is still in flight.
-    // Buffer descriptors over rows [kb0, kend) of this head's keys and values
-    // (word 3 is the gfx9 raw-buffer format: 32-bit data, range checked).
+    // the first tile), so the prologue costs one memory round trip.
+    // Buffer descriptors over rows [kb0, kend) of this head's keys and values.
     const int rowb = (int)(2 * ksn);
-    const __amdgpu_buffer_rsrc_t rk =
-        __builtin_amdgcn_make_buffer_rsrc((void *)(kp + (int64_t)kb0 * ksn), (short)0, (kend - kb0) * rowb, 0x00020000);
-    const __amdgpu_buffer_rsrc_t rv =
-        __builtin_amdgcn_make_buffer_rsrc((void *)(vp + (int64_t)kb0 * ksn), (short)0, (kend - kb0) * rowb, 0x00020000);
-    Stage<D> st;
-    Stage<D> st0[BPT];
+    const u32x4 rk = raw_rsrc(kp + (int64_t)kb0 * ksn, (kend - kb0) * rowb);
+    const u32x4 rv = raw_rsrc(vp + (int64_t)kb0 * ksn, (kend - kb0) * rowb);
 
     // Loads use a clamped, always-readable row; lanes without a query or a
     // partner zero the data afterwards.
@@ -340,8 +357,7 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
             vff[s] = *reinterpret_cast<const bf16x8 *>(vp + frc * ksn + 16 * s + 8 * g);
         }
     }
-#pragma unroll
-    for (int hf = 0; hf < BPT; ++hf) tile_load<D>(st0[hf], rk, rv, rowb, 0, hf, tid);
+    if (ntiles > 0) tile_fetch<D>(tA, rk, rv, rowb, 0, w, lane);
 #pragma unroll
     for (int s = 0; s < W::KS; ++s) ws.qf[s] = t_ok ? qraw[s] : bf16x8{};
 
@@ -430,9 +446,6 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
         }
         seed(vfraw, wf, has_f, true);
     }
-#pragma unroll
-    for (int hf = 0; hf < BPT; ++hf) tile_store<D>(st0[hf], tA, hf, tid);
-    __syncthreads();
 
     // ---- window band -------------------------------------------------------
     // One 32-key block: rows [32 blk, 32 blk + 32) of the tile at kt / vt,
@@ -490,43 +503,28 @@ __global__ __launch_bounds__(NT, D == 64 ? 4 : 2) void forward_bf16_kernel(FwdPa
                 ws.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[cc][db], pb[cc], ws.o[db], 0, 0, 0);
         }
     };
-    // One 64-row tile; the next tile (if any) is loaded into registers and
-    // stored to the other buffer, which every wavefront finished reading
-    // before the last barrier.  D = 128 loads the whole next tile before the
-    // first block (two blocks of latency cover the loads); D = 64 loads half
-    // blk while block blk is consumed (its four wavefronts per SIMD leave no
-    // registers for a second half).
-    auto tile = [&](const TileBuf<D> &cur, int row0, TileBuf<D> &nxt, bool has_next) {
-        if constexpr (D == 128) {
-            if (has_next) {
-#pragma unroll
-                for (int hf = 0; hf < BPT; ++hf) tile_load<D>(st0[hf], rk, rv, rowb, row0 - kb0 + TK, hf, tid);
-            }
-#pragma unroll
-            for (int blk = 0; blk < BPT; ++blk) block(cur.k, cur.v, row0 + 32 * blk, blk);
-            if (has_next) {
-#pragma unroll
-                for (int hf = 0; hf < BPT; ++hf) tile_store<D>(st0[hf], nxt, hf, tid);
-            }
-        } else {
-#pragma unroll
-            for (int blk = 0; blk < BPT; ++blk) {
-                if (has_next) tile_load<D>(st, rk, rv, rowb, row0 - kb0 + TK, blk, tid);
-                block(cur.k, cur.v, row0 + 32 * blk, blk);
-                if (has_next) tile_store<D>(st, nxt, blk, tid);
-            }
-        }
+    // Tile m (keys kb0 + 64m ..) is in buffer m mod 2.  Before its blocks a
+    // wavefront waits for its own fetches of it (the only ones in flight)
+    // and the barrier makes every wavefront's share visible; then tile m + 1
+    // is fetched into the other buffer, which every wavefront finished
+    // reading (tile m - 1) before that barrier, and lands while tile m's two
+    // blocks are computed.  The fences around the barrier are LDS-scoped: a
+    // work-group fence would also wait for the fetch of the next tile.
+    auto tile = [&](const TileBuf<D> &cur, TileBuf<D> &ahead, int m) {
+        __builtin_amdgcn_s_waitcnt(0xF70);   // vmcnt(0): this wavefront's fetches of tile m
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+        if (m + 1 < ntiles) tile_fetch<D>(ahead, rk, rv, rowb, TK * (m + 1), w, lane);
+        block(cur.k, cur.v, kb0 + TK * m, 0);
+        block(cur.k, cur.v, kb0 + TK * m + 32, 1);
     };
-    // Double buffering, unrolled by two so that every store and every read
-    // names its buffer statically.
-    for (int it = 0; it < ntiles; it += 2) {
-        const int row0 = kb0 + TK * it;
-        tile(tA, row0, tB, it + 1 < ntiles);
-        if (it + 1 >= ntiles) break;
-        __syncthreads();
-        tile(tB, row0 + TK, tA, it + 2 < ntiles);
-        if (it + 2 >= ntiles) break;
-        __syncthreads();
+    // unrolled by two so that every fetch and every read names its buffer
+    // statically
+    for (int m = 0; m < ntiles; m += 2) {
+        tile(tA, tB, m);
+        if (m + 1 >= ntiles) break;
+        tile(tB, tA, m + 1);
     }
 
     // ---- normalise and store -----------------------------------------------
