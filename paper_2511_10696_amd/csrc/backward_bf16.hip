@@ -30,10 +30,14 @@
 // (window |j - t| <= k, band up to t0 + 127 + k) adds the second partner
 // t + pi the same way.
 //
-// LDS rows are padded (2D + 16 bytes): the row reads are free of bank
-// conflicts and the transpose reads of the key tile cost at most two ways.
-// Tiles are staged through range-checked buffer loads that zero-fill rows
-// past the query tile's last usable row.
+// Tiles go from global memory straight into LDS (buffer loads with the LDS
+// destination, range-checked so that rows past the query tile's last usable
+// row read as zeros), the next tile while the two blocks of the current one
+// are consumed.  The key tile is read both as rows and by transpose reads:
+// its rows are padded by 64 bytes and the low two bits of a row's 16-byte
+// chunk index are XORed with bits 2-3 of the row, which keeps both patterns
+// free of bank conflicts; the value tile, read as rows only, has rows padded
+// by 16 bytes.
 #include "kernels.h"
 #include "pi_common.h"
 
@@ -52,53 +56,53 @@ constexpr int WAVES = 4;
 constexpr int NT = 64 * WAVES;
 constexpr int BM = 32 * WAVES;
 constexpr int TK = 64;
-constexpr int BPT = TK / 32;
 
 template <int D>
 struct Tile {
-    static constexpr int CPR = D / 8;        // 16-byte chunks per row
-    static constexpr int ROW = 2 * D + 16;   // padded LDS row stride (bytes)
-    static constexpr int BYTES = TK * ROW;
-    static constexpr int KS = D / 16;        // k-steps of the score products
-    static constexpr int DB = D / 32;        // 32-dim output blocks
+    static constexpr int CPR = D / 8;         // 16-byte chunks per row
+    static constexpr int KROW = 2 * D + 64;   // key-tile LDS row stride (bytes)
+    static constexpr int VROW = 2 * D + 16;   // value-tile LDS row stride (bytes)
+    static constexpr int KS = D / 16;         // k-steps of the score products
+    static constexpr int DB = D / 32;         // 32-dim output blocks
 };
 
 template <int D>
 struct TileBuf {
-    alignas(16) unsigned char k[Tile<D>::BYTES];
-    alignas(16) unsigned char v[Tile<D>::BYTES];
+    alignas(16) unsigned char k[TK * Tile<D>::KROW];
+    alignas(16) unsigned char v[TK * Tile<D>::VROW];
 };
 
-template <int D>
-struct Stage {
-    static constexpr int CH = TK * Tile<D>::CPR / NT / BPT;
-    uint4 k[CH];
-    uint4 v[CH];
-};
+// Key-tile chunk swizzle: chunk pc of row r sits at chunk pc ^ chunk_x(r).
+__device__ inline int chunk_x(int row) { return (row >> 2) & 3; }
 
-// Half hf of the tile `row0` rows past the window start (descriptors begin
-// at the window start and end at its last usable row: later rows read 0).
+// Fetch tile rows [row0, row0 + TK) (counted from the window start) into
+// LDS buffer tb: instruction u of a tensor fills bytes [1024u, 1024u + 1024)
+// of its buffer, 16 bytes per lane, each lane's source chosen so that the
+// bytes land in the tile's layout (pad chunks take an out-of-range offset
+// and are written as zeros); wavefront w issues u = w, w + WAVES, ...
 template <int D>
-__device__ inline void tile_load(Stage<D> &st, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv, int rowb,
-                                 int row0, int hf, int tid) {
+__device__ inline void tile_fetch(TileBuf<D> &tb, u32x4 rk, u32x4 rv, int rowb, int row0, int w, int lane) {
+    using T = Tile<D>;
+    constexpr int KU = T::KROW / 16, VU = T::VROW / 16;   // LDS chunks per row
+    constexpr int KI = TK * KU / 64, VI = TK * VU / 64;   // instructions per tile
+    static_assert(TK * KU % 64 == 0 && TK * VU % 64 == 0, "tile fetch shape");
 #pragma unroll
-    for (int u = 0; u < Stage<D>::CH; ++u) {
-        const int cid = tid + NT * (hf * Stage<D>::CH + u);
-        const int row = cid / Tile<D>::CPR, pc = cid % Tile<D>::CPR;
-        const int off = row * rowb + pc * 16;
-        st.k[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, row0 * rowb, 0));
-        st.v[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, off, row0 * rowb, 0));
+    for (int u0 = 0; u0 < KI; u0 += WAVES) {
+        const int u = u0 + w;
+        if (u < KI) {   // wave-uniform
+            const int pidx = 64 * u + lane, row = pidx / KU, pc = pidx % KU;
+            const int off = pc < T::CPR ? (row0 + row) * rowb + (pc ^ chunk_x(row)) * 16 : kOutOfRange;
+            lds_fetch16(rk, off, tb.k + 1024 * u);
+        }
     }
-}
-
-template <int D>
-__device__ inline void tile_store(const Stage<D> &st, TileBuf<D> &tb, int hf, int tid) {
 #pragma unroll
-    for (int u = 0; u < Stage<D>::CH; ++u) {
-        const int cid = tid + NT * (hf * Stage<D>::CH + u);
-        const int row = cid / Tile<D>::CPR, pc = cid % Tile<D>::CPR;
-        *reinterpret_cast<uint4 *>(tb.k + row * Tile<D>::ROW + pc * 16) = st.k[u];
-        *reinterpret_cast<uint4 *>(tb.v + row * Tile<D>::ROW + pc * 16) = st.v[u];
+    for (int u0 = 0; u0 < VI; u0 += WAVES) {
+        const int u = u0 + w;
+        if (u < VI) {
+            const int pidx = 64 * u + lane, row = pidx / VU, pc = pidx % VU;
+            const int off = pc < T::CPR ? (row0 + row) * rowb + pc * 16 : kOutOfRange;
+            lds_fetch16(rv, off, tb.v + 1024 * u);
+        }
     }
 }
 
@@ -120,28 +124,41 @@ __device__ inline float dot_bf16x8(const bf16x8 &a, const bf16x8 &b, float acc) 
 }
 
 // Row fragments (A operand, row l%32, dims 16s + 8(l/32)) of 32-row block
-// `blk` of a tile array.
+// `blk` of the value tile ...
 template <int D>
-__device__ inline void read_rows(bf16x8 f[Tile<D>::KS], const unsigned char *tile, int blk, int c, int g) {
-    const unsigned char *base = tile + (32 * blk + c) * Tile<D>::ROW + 16 * g;
+__device__ inline void read_vrows(bf16x8 f[Tile<D>::KS], const unsigned char *tile, int blk, int c, int g) {
+    const unsigned char *base = tile + (32 * blk + c) * Tile<D>::VROW + 16 * g;
 #pragma unroll
     for (int s = 0; s < Tile<D>::KS; ++s) f[s] = *reinterpret_cast<const bf16x8 *>(base + 32 * s);
 }
 
+// ... and of the key tile: chunk (2s + g) ^ x = 2(s ^ (x >> 1)) + (g ^ (x & 1)),
+// x = chunk_x(row), so even and odd k-steps have one base each.
+template <int D>
+__device__ inline void read_krows(bf16x8 f[Tile<D>::KS], const unsigned char *tile, int blk, int c, int g) {
+    const int row = 32 * blk + c, x = chunk_x(row);
+    const int rb = row * Tile<D>::KROW + 16 * (g ^ (x & 1));
+    const int rbo[2] = {rb + 32 * (x >> 1), rb - 32 * (x >> 1)};
+#pragma unroll
+    for (int s = 0; s < Tile<D>::KS; ++s) f[s] = *reinterpret_cast<const bf16x8 *>(tile + rbo[s & 1] + 32 * s);
+}
+
 // Transposed fragments (A operand: dim 32db + l%32, keys 16cc + {4g..4g+3,
-// 8+4g..8+4g+3}) of 32-row block `blk` by LDS transpose reads.
+// 8+4g..8+4g+3}) of 32-row block `blk` of the key tile by LDS transpose
+// reads: rows 32 blk + 4g + r + 8hh + 16cc, whose chunk_x is g + 2hh.
 template <int D>
 __device__ inline void read_cols(bf16x8 f[2][Tile<D>::DB], const unsigned char *tile, int blk, int lane) {
     const int g = lane >> 5, G = lane >> 4, r = (lane >> 2) & 3, qd = lane & 3;
-    const unsigned char *base =
-        tile + (32 * blk + 4 * g + r) * Tile<D>::ROW + (2 * (G & 1) + (qd >> 1)) * 16 + (qd & 1) * 8;
+    const int jq = 2 * (G & 1) + (qd >> 1);
+    const int toff[2] = {(32 * blk + 4 * g + r) * Tile<D>::KROW + 16 * (jq ^ g) + (qd & 1) * 8,
+                         (32 * blk + 4 * g + r + 8) * Tile<D>::KROW + 16 * (jq ^ (g + 2)) + (qd & 1) * 8};
 #pragma unroll
     for (int cc = 0; cc < 2; ++cc) {
 #pragma unroll
         for (int db = 0; db < Tile<D>::DB; ++db) {
 #pragma unroll
             for (int hh = 0; hh < 2; ++hh) {
-                const unsigned char *src = base + (16 * cc + 8 * hh) * Tile<D>::ROW + 64 * db;
+                const unsigned char *src = tile + toff[hh] + 16 * cc * Tile<D>::KROW + 64 * db;
                 const bf16x4 y = __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)src));
                 f[cc][db][4 * hh + 0] = y[0];
                 f[cc][db][4 * hh + 1] = y[1];
@@ -190,14 +207,9 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
     const int kend = min(BIDIR ? (int)min((int64_t)t0 + BM + kw, (int64_t)NS) : min(t0 + BM, NQ), p.kvend);
     const int ntiles = (kend - kb0 + TK - 1) / TK;
     const int rowb = (int)(2 * ksn);
-    const __amdgpu_buffer_rsrc_t rk =
-        __builtin_amdgcn_make_buffer_rsrc((void *)(kp + (int64_t)kb0 * ksn), (short)0, (kend - kb0) * rowb, 0x00020000);
-    const __amdgpu_buffer_rsrc_t rv =
-        __builtin_amdgcn_make_buffer_rsrc((void *)(vp + (int64_t)kb0 * ksn), (short)0, (kend - kb0) * rowb, 0x00020000);
-    Stage<D> st;
-    Stage<D> st0[BPT];
-#pragma unroll
-    for (int hf = 0; hf < BPT; ++hf) tile_load<D>(st0[hf], rk, rv, rowb, 0, hf, tid);
+    const u32x4 rk = raw_rsrc(kp + (int64_t)kb0 * ksn, (kend - kb0) * rowb);
+    const u32x4 rv = raw_rsrc(vp + (int64_t)kb0 * ksn, (kend - kb0) * rowb);
+    if (ntiles > 0) tile_fetch<D>(tA, rk, rv, rowb, 0, w, lane);
 
     // Query and dL/dy rows as B operands (lanes without a query hold zeros).
     bf16x8 qf[KS], of[KS];
@@ -237,7 +249,7 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
 
     // ---- partners: scores and dP of the partner rows ------------------------
     // Partner row prow of this lane's query (has_p: it exists).
-    auto partner = [&](int prow, bool has_p) {
+    auto partner = [&](int prow, bool has_p) __attribute__((always_inline)) {
         if (__builtin_amdgcn_ballot_w64(has_p) == 0) return;
         const int prc = has_p ? prow : p.kvpos0;
         bf16x8 kpf[KS], vpf[KS];
@@ -299,34 +311,26 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
             }
         }
     };
-    // the first tile goes to LDS before the partners are scored, so that its
-    // staging registers are free while the partner rows are held
-#pragma unroll
-    for (int hf = 0; hf < BPT; ++hf) tile_store<D>(st0[hf], tA, hf, tid);
     partner(t - pi, partner_enabled(kw, pi) && t - pi >= 0 && t_ok);
     if constexpr (BIDIR) partner(t + pi, t_ok && partner_fwd_of(t, kw, pi, NS) >= 0);
-    __syncthreads();
 
     // ---- window band ---------------------------------------------------------
-    auto block = [&](const TileBuf<D> &tb, int j0, int blk) {
+    auto block = [&](const TileBuf<D> &tb, int j0, int blk) __attribute__((always_inline)) {
         const bool act = BIDIR ? j0 < kend && q0 < NQ && j0 - (q0 + 31) <= kw && j0 + 31 >= q0 - kw
                                : j0 < kend && q0 < NQ && j0 <= q0 + 31 && j0 + 31 >= q0 - kw;
         if (!act) return;
         const bool edge = BIDIR ? !(j0 + 31 - q0 <= kw && q0 + 31 - j0 <= kw) || q0 + 31 >= NQ || j0 + 31 >= NS
                                 : !(j0 + 31 <= q0 && j0 >= q0 + 31 - kw) || q0 + 31 >= NQ;
         bf16x8 f[KS];
-        read_rows<D>(f, tb.k, blk, c, g);
+        read_krows<D>(f, tb.k, blk, c, g);
         f32x16 sc = {};
 #pragma unroll
         for (int s = 0; s < KS; ++s) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[s], qf[s], sc, 0, 0, 0);
-        read_rows<D>(f, tb.v, blk, c, g);
+        read_vrows<D>(f, tb.v, blk, c, g);
         f32x16 dp = {};
 #pragma unroll
         for (int s = 0; s < KS; ++s) dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[s], of[s], dp, 0, 0, 0);
-        // K^T for dQ: read before the softmax so the reads land during it,
-        // except with the clamp, whose extra terms leave no registers for it
         bf16x8 kt[2][DB];
-        if constexpr (!CLAMP) read_cols<D>(kt, tb.k, blk, lane);
         float ds[16];
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
@@ -351,7 +355,7 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
             a_loc += cut ? 0.0f : pd;
             b_loc += cut ? 0.0f : wgt;
         }
-        if constexpr (CLAMP) read_cols<D>(kt, tb.k, blk, lane);
+        read_cols<D>(kt, tb.k, blk, lane);
         bf16x8 dsb[2];
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc)
@@ -363,22 +367,27 @@ __global__ __launch_bounds__(NT, 2) void backward_q_bf16_kernel(BwdParams bp, in
             for (int db = 0; db < DB; ++db)
                 dq[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt[cc][db], dsb[cc], dq[db], 0, 0, 0);
     };
-    auto tile = [&](const TileBuf<D> &cur, int row0, TileBuf<D> &nxt, bool has_next) {
-#pragma unroll
-        for (int blk = 0; blk < BPT; ++blk) {
-            if (has_next) tile_load<D>(st, rk, rv, rowb, row0 - kb0 + TK, blk, tid);
-            block(cur, row0 + 32 * blk, blk);
-            if (has_next) tile_store<D>(st, nxt, blk, tid);
-        }
+    // Tile m (keys kb0 + 64m ..) is in buffer m mod 2.  A wavefront waits
+    // for its own fetches of it (the only vector-memory operations in flight
+    // here), the barrier makes every wavefront's share visible, and tile
+    // m + 1 then goes into the other buffer (last read for tile m - 1,
+    // before that barrier).  LDS-scoped fences: a work-group fence would
+    // also wait for the fetch of the next tile.
+    auto tile = [&](const TileBuf<D> &cur, TileBuf<D> &ahead, int m) __attribute__((always_inline)) {
+        __builtin_amdgcn_s_waitcnt(0xF70);   // vmcnt(0)
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+        if (m + 1 < ntiles) tile_fetch<D>(ahead, rk, rv, rowb, TK * (m + 1), w, lane);
+        block(cur, kb0 + TK * m, 0);
+        block(cur, kb0 + TK * m + 32, 1);
     };
-    for (int it = 0; it < ntiles; it += 2) {
-        const int row0 = kb0 + TK * it;
-        tile(tA, row0, tB, it + 1 < ntiles);
-        if (it + 1 >= ntiles) break;
-        __syncthreads();
-        tile(tB, row0 + TK, tA, it + 2 < ntiles);
-        if (it + 2 >= ntiles) break;
-        __syncthreads();
+    // unrolled by two so that every fetch and every read names its buffer
+    // statically
+    for (int m = 0; m < ntiles; m += 2) {
+        tile(tA, tB, m);
+        if (m + 1 >= ntiles) break;
+        tile(tB, tA, m + 1);
     }
 
     // ---- store ---------------------------------------------------------------

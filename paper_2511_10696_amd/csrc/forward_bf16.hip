@@ -72,7 +72,6 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int WAVES = 4;
 constexpr int NT = 64 * WAVES;   // threads per work-group
@@ -113,31 +112,6 @@ __device__ inline int v_swz(int row, int chunk) { return chunk ^ ((row & 3) << 1
 // the pad chunks take an out-of-range offset (written as zeros); D = 64 rows
 // hold global chunk v_swz(r, pc) at chunk pc.  Offsets past the rows the
 // descriptor covers read as zeros.
-constexpr int kOutOfRange = 1 << 30;   // past any tile range the descriptors describe
-
-// Raw buffer descriptor over nbytes from base (stride 0; word 3 is the gfx9
-// raw-buffer format: 32-bit data, range checked).
-__device__ inline u32x4 raw_rsrc(const void *base, int nbytes) {
-    const unsigned long long a = (unsigned long long)base;
-    u32x4 r;
-    r.x = __builtin_amdgcn_readfirstlane((unsigned)a);
-    r.y = __builtin_amdgcn_readfirstlane((unsigned)(a >> 32) & 0xffffu);
-    r.z = __builtin_amdgcn_readfirstlane((unsigned)nbytes);
-    r.w = 0x00020000u;
-    return r;
-}
-
-// One 16-byte-per-lane buffer load into LDS at lds + 16 * lane.  Issued as
-// inline asm: the compiler then keeps no count of it (its own waits for
-// LDS reads after such a load would wait for every fetch in flight); the
-// kernel waits for it with an explicit counter before the barrier that
-// publishes the tile.
-__device__ inline void lds_fetch16(u32x4 rsrc, int voff, void *lds) {
-    const unsigned m0 = __builtin_amdgcn_readfirstlane(
-        (unsigned)(uintptr_t)(__attribute__((address_space(3))) void *)lds);
-    asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff), "s"(rsrc), "{m0}"(m0) : "memory");
-}
-
 template <int D>
 struct Fetch {
     static constexpr int KI = TK * Tile<D>::CPR / 64;   // instructions per K tile

@@ -1,6 +1,7 @@
 // pi_common.h -- working-set enumeration and fusion prior shared by every
 // kernel of the library and by pi_attn_index_set, so that the exported index
-// set is the one the attention kernels use.
+// set is the one the attention kernels use; the XCD-aware work-group order and
+// the direct global-to-LDS fetch the MFMA kernels share.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -103,6 +104,38 @@ __device__ inline int64_t xcd_remap(int64_t bid, int64_t n_logical) {
 inline int64_t xcd_grid(int64_t n_logical) {
     int64_t per = (n_logical + kNumXcd - 1) / kNumXcd;
     return per * kNumXcd;
+}
+
+// ---- direct global-to-LDS tile fetch ---------------------------------------
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kOutOfRange = 1 << 30;   // past any tile range the descriptors describe
+
+// Raw buffer descriptor over nbytes from base (stride 0; word 3 is the gfx9
+// raw-buffer format: 32-bit data, range checked).
+__device__ inline u32x4 raw_rsrc(const void *base, int nbytes) {
+    const unsigned long long a = (unsigned long long)base;
+    u32x4 r;
+    r.x = __builtin_amdgcn_readfirstlane((unsigned)a);
+    r.y = __builtin_amdgcn_readfirstlane((unsigned)(a >> 32) & 0xffffu);
+    r.z = __builtin_amdgcn_readfirstlane((unsigned)nbytes);
+    r.w = 0x00020000u;
+    return r;
+}
+
+// One 16-byte-per-lane buffer load into LDS at lds + 16 * lane.  Issued as
+// inline asm: the compiler then keeps no count of it (its own waits for
+// LDS reads after such a load would wait for every fetch in flight); the
+// kernel waits for it with an explicit counter before the barrier that
+// publishes the tile, and reads the buffer only after that barrier and an
+// LDS acquire fence.  No memory clobber: the volatile asm stays after the
+// barrier that frees its buffer (both have side effects), and a clobber
+// would force every object whose address the kernel takes into private
+// memory.
+__device__ inline void lds_fetch16(u32x4 rsrc, int voff, void *lds) {
+    const unsigned m0 = __builtin_amdgcn_readfirstlane(
+        (unsigned)(uintptr_t)(__attribute__((address_space(3))) void *)lds);
+    asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff), "s"(rsrc), "{m0}"(m0));
 }
 
 }  // namespace pi_attn
