@@ -407,18 +407,38 @@ __global__ __launch_bounds__(NT) void backward_kv_bf16_kernel(BwdParams bp, int 
     }
 
     // ---- store: lane (c, g) holds dims 32db + 8i + 4g + [0, 4) of key c ----
-    if (j_ok) {
-        const int64_t row = obase + j;
-        float *dst = (keyw ? bp.dk : bp.dv) + row * D;
+    // The accumulator goes out in whole rows: each wavefront writes half of
+    // its 32 rows' dims to a private LDS region (the tile buffers, free once
+    // every wavefront has left the loop), reads them back 16 bytes per lane
+    // along the rows and stores 256 contiguous bytes per row (128 at D = 64),
+    // instead of 16-byte pieces of 32 rows per instruction.
+    {
+        constexpr int HW = D / 2;              // dims per pass
+        constexpr int P = HW * 4 + 16;         // LDS row pitch (bytes), padded against bank conflicts
+        constexpr int LPR = HW / 4;            // lanes per row when reading back
+        constexpr int RPI = 64 / LPR;          // rows per read instruction
+        static_assert(4 * 32 * P <= (int)sizeof(QTile<D>), "store staging fits a tile buffer");
+        __syncthreads();
+        unsigned char *reg = reinterpret_cast<unsigned char *>(wv < PAIRS ? &tA : &tB) + (wv % PAIRS) * 32 * P;
+        float *dst = keyw ? bp.dk : bp.dv;
         const float f = keyw ? p.scale : 1.0f;
 #pragma unroll
-        for (int d = 0; d < DB; ++d) {
+        for (int hf = 0; hf < 2; ++hf) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                f32x4 a;
+            for (int d = 0; d < DB / 2; ++d) {
 #pragma unroll
-                for (int x = 0; x < 4; ++x) a[x] = acc[d][4 * i + x] * f;
-                *reinterpret_cast<f32x4 *>(dst + 32 * d + 8 * i + 4 * g) = a;
+                for (int i = 0; i < 4; ++i) {
+                    f32x4 a;
+#pragma unroll
+                    for (int x = 0; x < 4; ++x) a[x] = acc[hf * (DB / 2) + d][4 * i + x] * f;
+                    *reinterpret_cast<f32x4 *>(reg + c * P + (32 * d + 8 * i + 4 * g) * 4) = a;
+                }
+            }
+#pragma unroll
+            for (int v = 0; v < 32 / RPI; ++v) {
+                const int r = RPI * v + lane / LPR, ch = lane % LPR;
+                const f32x4 a = *reinterpret_cast<const f32x4 *>(reg + r * P + ch * 16);
+                if (kq0 + r < NK) *reinterpret_cast<f32x4 *>(dst + (obase + kq0 + r) * D + hf * HW + 4 * ch) = a;
             }
         }
     }
