@@ -4,23 +4,23 @@
 // A work-group of 8 wavefronts owns 128 keys [j0, j0 + 128) of one (b, h),
 // as 4 pairs: pair w (wavefronts w and w + 4) the 32 keys
 // kq0 = j0 + 32w + [0, 32).  The queries that hold these keys in their
-// working set stream through LDS in 64-row tiles of Q and dL/dy, with the
-// per-query lse, row term r_t = <dL/dy_t, y_t> and prior bias: first the
-// window band, queries [j0, j0 + 127 + k] (key j is in W_t iff
-// j <= t <= j + k, Sec. 3.2 eq. Nr), then the partner run
-// [j0 + pi, j0 + pi + 128) (key j is the partner of query j + pi when
-// pi > k, Sec. 3.4 eq. Npi), in which pair w meets its partners on the
-// diagonal of block w.  The bidirectional mode streams the band
-// [j0 - k, j0 + 127 + k] (|t - j| <= k) and a second partner run
-// [j0 - pi, j0 - pi + 128) (key j is the partner t + pi of query j - pi);
-// rows of a run outside [0, N) are zero and masked.
+// window stream through LDS in 64-row tiles of Q and dL/dy, with the
+// per-query lse, row term r_t = <dL/dy_t, y_t> and prior bias: the band
+// of queries [j0, j0 + 127 + k] (key j is in W_t iff j <= t <= j + k,
+// Sec. 3.2 eq. Nr; bidirectionally [j0 - k, j0 + 127 + k], |t - j| <= k);
+// rows outside [0, N) are zero and masked.  After the band, the queries
+// whose partner is one of these keys (Sec. 3.4 eq. Npi, pi > k), the run
+// [j0 + pi, j0 + pi + 128) of queries t = j + pi (bidirectionally also
+// [j0 - pi, j0 - pi + 128), t = j - pi), are staged into the two tile
+// buffers: each key meets exactly one query of a run, row 32w + c for key
+// kq0 + c, and each lane forms that entry with per-lane dot products.
 //
 // The two wavefronts of a pair split each 32-query block between them, on
 // v_mfma_f32_32x32x16_bf16 with lane l holding key l%32 and queries
 // 8i + 4(l/32) + j at slot 4i + j:
 //   value wavefront (K^T in registers, dV^T accumulator)
 //     S = Q K^T (A = Q rows from LDS), alpha^ = exp(delta - lse_t),
-//     alpha^ to LDS for its partner, then dV^T += dO^T alpha^
+//     alpha^ to LDS for the pair's key wavefront, then dV^T += dO^T alpha^
 //   key wavefront (V^T in registers, dK^T accumulator)
 //     dP = dO V^T, then with alpha^ from LDS dS = alpha^ (dP - r_t)
 //     (Sec. 3.5 eq. jac; 0 where the clamp saturates), dK^T += Q^T dS
@@ -95,6 +95,24 @@ struct Stage {
 // the k-step (two bases, even and odd steps) and in the dimension block.
 __device__ inline int chunk_x(int row) { return (row >> 2) & 3; }
 
+// The value held by the other half of the wavefront (lane l ^ 32).
+__device__ inline float other_half(float x) {
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(__lane_id() < 32 ? p[1] : p[0]);
+}
+
+// acc + <a, b> over eight bf16 pairs (packed products, fp32 sums).
+__device__ inline float dot_bf16x8(const bf16x8 &a, const bf16x8 &b, float acc) {
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 0, 1), __builtin_shufflevector(b, b, 0, 1),
+                                          acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 2, 3), __builtin_shufflevector(b, b, 2, 3),
+                                          acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 4, 5), __builtin_shufflevector(b, b, 4, 5),
+                                          acc, false);
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 6, 7), __builtin_shufflevector(b, b, 6, 7),
+                                           acc, false);
+}
+
 template <int D, bool CLAMP, bool BIDIR>
 __global__ __launch_bounds__(NT) void backward_kv_bf16_kernel(BwdParams bp, int n_kt, int64_t n_logical) {
     using T = Tile<D>;
@@ -147,37 +165,23 @@ __global__ __launch_bounds__(NT) void backward_kv_bf16_kernel(BwdParams bp, int 
 #pragma unroll
     for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
 
-    // Query streams (kind 0 band, 1 the run of queries whose partner t - pi
-    // is one of these keys, 2 (bidirectional) the run whose partner t + pi
-    // is): tiles [0, nband), [nband, nband + npar), then the rest.  Query
-    // rows [lo, hi) of a stream; rows outside [0, N) are zero and masked.
+    // The window band streams through LDS: query rows [band_lo, band_hi) in
+    // 64-row tiles (rows outside the held [QS, QE) are zero and masked).
+    // The partner runs, queries [par_lo, par_hi) whose partner t - pi is
+    // one of these keys and (bidirectional) [par2_lo, par2_hi) whose
+    // partner t + pi is, are handled after the band.
     const int band_lo = BIDIR ? window_lo(j0, kw) & ~31 : j0;
     const int band_hi = BIDIR ? (int)min((int64_t)j0 + BK + kw, (int64_t)QE) : min(QE, j0 + BK + kw);
-    const int nband = band_hi > band_lo ? (band_hi - band_lo + TQ - 1) / TQ : 0;
+    const int ntiles = band_hi > band_lo ? (band_hi - band_lo + TQ - 1) / TQ : 0;
     const bool has_par = partner_enabled(kw, pi) && (int64_t)j0 + pi < QE;
     const int par_lo = j0 + pi;
     const int par_hi = has_par ? min(QE, j0 + pi + BK) : par_lo;
-    const int npar = has_par ? (par_hi - par_lo + TQ - 1) / TQ : 0;
     const bool has_par2 = BIDIR && partner_enabled(kw, pi) && j0 + BK > pi;
     const int par2_lo = j0 - pi;   // may be negative
     const int par2_hi = has_par2 ? min(QE, j0 + BK - pi) : par2_lo;
-    const int npar2 = has_par2 ? (par2_hi - par2_lo + TQ - 1) / TQ : 0;
-    const int ntiles = nband + npar + npar2;
 
-    // Stage tile m of the combined stream: 64 query rows starting at q0m.
-    // Arithmetic with 0/1 weights rather than choices between variables: a
-    // choice between two memory locations (the captured values) compiles to a
-    // load through a chosen address, which keeps them in private memory.
-    auto in_par = [=](int m) { return m >= nband ? 1 : 0; };
-    auto in_par2 = [=](int m) { return BIDIR && m >= nband + npar ? 1 : 0; };
-    auto tile_kind = [=](int m) { return in_par(m) + in_par2(m); };
-    auto tile_start = [=](int m) {
-        const int s0 = band_lo + TQ * m, s1 = par_lo + TQ * (m - nband), s2 = par2_lo + TQ * (m - nband - npar);
-        return s0 + in_par(m) * (s1 - s0) + in_par2(m) * (s2 - s1);
-    };
-    auto tile_end = [=](int m) { return band_hi + in_par(m) * (par_hi - band_hi) + in_par2(m) * (par2_hi - par_hi); };
-    auto load = [&](Stage<D> &st, int m) {
-        const int q0m = tile_start(m), lim = tile_end(m);
+    // Stage 64 query rows starting at q0m (held [max(q0m, QS), lim)).
+    auto load_rows = [&](Stage<D> &st, int q0m, int lim, bool band) __attribute__((always_inline)) {
         const int tfirst = min(max(q0m, QS), QE - 1);   // an always-held row
 #pragma unroll
         for (int u = 0; u < T::CH; ++u) {
@@ -200,8 +204,11 @@ __global__ __launch_bounds__(NT) void backward_kv_bf16_kernel(BwdParams bp, int 
             st.gl = p.gate[b * p.gsb + h * p.gsh + (tc - QS) * p.gsn];
             st.lse = bp.lse[rbase + tc];
             st.r = bp.rowterm[rbase + tc];
-            st.band = m < nband;
+            st.band = band;
         }
+    };
+    auto load = [&](Stage<D> &st, int m) __attribute__((always_inline)) {
+        load_rows(st, band_lo + TQ * m, band_hi, true);
     };
     auto store = [&](const Stage<D> &st, QTile<D> &tb) {
 #pragma unroll
@@ -224,22 +231,20 @@ __global__ __launch_bounds__(NT) void backward_kv_bf16_kernel(BwdParams bp, int 
 
     // Whether pair w meets the 32-query block starting at t0b, and whether
     // the block needs masking.
-    auto active = [&](int t0b, int blk, int kind, int lim) {
-        if (kind != 0) return blk == (w & 1) && t0b == (BIDIR && kind == 2 ? kq0 - pi : kq0 + pi);
-        if constexpr (BIDIR) return t0b < lim && kq0 < NK && t0b - (kq0 + 31) <= kw && t0b + 31 >= kq0 - kw;
-        return t0b < lim && kq0 < NK && t0b <= kq0 + 31 + kw && t0b + 31 >= kq0;
+    auto active = [&](int t0b) {
+        if constexpr (BIDIR) return t0b < band_hi && kq0 < NK && t0b - (kq0 + 31) <= kw && t0b + 31 >= kq0 - kw;
+        return t0b < band_hi && kq0 < NK && t0b <= kq0 + 31 + kw && t0b + 31 >= kq0;
     };
-    auto edge_block = [&](int t0b, int kind) {
-        const bool partner = kind != 0;
-        return BIDIR ? partner || !(t0b + 31 - kq0 <= kw && kq0 + 31 - t0b <= kw) || t0b + 31 >= QE ||
-                           kq0 + 31 >= NK || t0b < QS
-                     : partner || !(t0b >= kq0 + 31 && t0b + 31 <= kq0 + kw) || t0b + 31 >= QE || kq0 + 31 >= NK;
+    auto edge_block = [&](int t0b) {
+        return BIDIR ? !(t0b + 31 - kq0 <= kw && kq0 + 31 - t0b <= kw) || t0b + 31 >= QE || kq0 + 31 >= NK ||
+                           t0b < QS
+                     : !(t0b >= kq0 + 31 && t0b + 31 <= kq0 + kw) || t0b + 31 >= QE || kq0 + 31 >= NK;
     };
 
     // First phase of a block (rows 32 blk.. of tile tb, first query t0b):
-    // the value wavefront forms alpha^ (to pb for dV, to LDS for its
-    // partner), the key wavefront dP (to dp).
-    auto phase1 = [&](const QTile<D> &tb, int t0b, int blk, int kind, bool edge, int par, bf16x8 (&pb)[2],
+    // the value wavefront forms alpha^ (to pb for dV, to LDS for the pair's
+    // key wavefront), the key wavefront dP (to dp).
+    auto phase1 = [&](const QTile<D> &tb, int t0b, int blk, bool edge, int par, bf16x8 (&pb)[2],
                       f32x16 &dp) {
         // rows of this block (A operands: query l%32, dims 16s + 8g): chunk
         // (2s + g) ^ x = 2(s ^ (x >> 1)) + (g ^ (x & 1)), x = chunk_x(row)
@@ -283,22 +288,15 @@ __global__ __launch_bounds__(NT) void backward_kv_bf16_kernel(BwdParams bp, int 
         }
         // Edge blocks: the working-set entries of this lane's key j among the
         // block's queries are one run of rows, the window [j, j + k] (|t - j|
-        // <= k bidirectionally) or the single partner query of this stream,
-        // cut to the held rows [QS, QE) and to the block; bit r of keep marks
+        // <= k bidirectionally), cut to the held rows [QS, QE) and to the
+        // block; bit r of keep marks
         // row 4g + r of the block (this lane's rows 4g + 8i + jj at bit
         // 8i + jj), and alpha^ of the other entries is cleared.  The empty
         // asm keeps this a branch that interior blocks skip.
         if (edge) {
             asm volatile("" ::: "memory");
-            int lo, hi;
-            if (kind == 0) {
-                lo = BIDIR ? j - kw : j;
-                hi = j + kw;
-            } else {
-                lo = hi = j + ((BIDIR && kind == 2) ? -pi : pi);
-            }
-            lo = max(lo, max(QS, t0b));
-            hi = min(hi, min(QE - 1, t0b + 31));
+            const int lo = max(BIDIR ? j - kw : j, max(QS, t0b));
+            const int hi = min(j + kw, min(QE - 1, t0b + 31));
             const int n = hi - lo + 1;
             uint32_t keep = !j_ok || n <= 0 ? 0u : n >= 32 ? ~0u : ((1u << n) - 1u) << (lo - t0b);
             keep >>= 4 * g;
@@ -378,14 +376,14 @@ __global__ __launch_bounds__(NT) void backward_kv_bf16_kernel(BwdParams bp, int 
     // tile's second block, finished before this tile's first barrier).
     Stage<D> st;
     auto tile = [&](const QTile<D> &cur, QTile<D> &nxt, int m) {
-        const int t0 = tile_start(m), kind = tile_kind(m), lim = tile_end(m);
+        const int t0 = band_lo + TQ * m;
         bf16x8 pb[2];
         f32x16 dp;
-        const bool a0 = active(t0, 0, kind, lim), a1 = active(t0 + 32, 1, kind, lim);
-        if (a0) phase1(cur, t0, 0, kind, edge_block(t0, kind), 0, pb, dp);
+        const bool a0 = active(t0), a1 = active(t0 + 32);
+        if (a0) phase1(cur, t0, 0, edge_block(t0), 0, pb, dp);
         __syncthreads();
         if (a0) phase2(cur, 0, 0, pb, dp);
-        if (a1) phase1(cur, t0 + 32, 1, kind, edge_block(t0 + 32, kind), 1, pb, dp);
+        if (a1) phase1(cur, t0 + 32, 1, edge_block(t0 + 32), 1, pb, dp);
         if (m + 1 < ntiles) {
             store(st, nxt);
             if (m + 2 < ntiles) load(st, m + 2);
@@ -405,6 +403,73 @@ __global__ __launch_bounds__(NT) void backward_kv_bf16_kernel(BwdParams bp, int 
             tile(tB, tA, m + 1);
         }
     }
+
+    // ---- partners (Sec. 3.4, eq. Npi) ---------------------------------------
+    // The queries whose partner is one of this work-group's keys form one run
+    // of 128 rows (t = j + pi; bidirectionally also t = j - pi), row 32w + c
+    // the partner of key kq0 + c.  The run is staged into the two tile
+    // buffers after the band; each lane then forms its one entry by a dot
+    // product of its half of the query (dL/dy) row with its half of k_j
+    // (v_j), plus the other half's: the value wavefront adds alpha^ dO_t to
+    // dV and hands alpha^ over through LDS, the key wavefront adds
+    // alpha^ (dP - r_t) q_t to dK.
+    auto partner_run = [&](int lo, int hi) __attribute__((always_inline)) {
+        __syncthreads();   // every wavefront is done with the tile buffers
+        load_rows(st, lo, hi, false);
+        store(st, tA);
+        load_rows(st, lo + TQ, hi, false);
+        store(st, tB);
+        __syncthreads();
+        const QTile<D> &tb = w < 2 ? tA : tB;
+        const int row = 32 * (w & 1) + c, t = lo + 32 * w + c;
+        const bool has = j_ok && t >= QS && t < hi;
+        const int xr = chunk_x(row);
+        const int rb = row * T::ROW + 16 * (g ^ (xr & 1));
+        const int rbo[2] = {rb + 32 * (xr >> 1), rb - 32 * (xr >> 1)};   // even, odd k-steps
+        const unsigned char *src = keyw ? tb.o : tb.q;
+        float part = 0.0f;
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+            part = dot_bf16x8(*reinterpret_cast<const bf16x8 *>(src + rbo[s & 1] + 32 * s), kvf[s], part);
+        const float d = part + other_half(part);
+        // the other operand row in the accumulator layout: dims 32db + 8i + 4g + [0, 4)
+        auto add_row = [&](const unsigned char *rows, float wgt) __attribute__((always_inline)) {
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const uint2 raw = *reinterpret_cast<const uint2 *>(
+                        rows + row * T::ROW + ((4 * db + i) ^ xr) * 16 + 8 * g);
+                    acc[db][4 * i + 0] += wgt * __uint_as_float(raw.x << 16);
+                    acc[db][4 * i + 1] += wgt * __uint_as_float(raw.x & 0xffff0000u);
+                    acc[db][4 * i + 2] += wgt * __uint_as_float(raw.y << 16);
+                    acc[db][4 * i + 3] += wgt * __uint_as_float(raw.y & 0xffff0000u);
+                }
+            }
+        };
+        if (!keyw) {
+            float pr;
+            bool cut = false;
+            if constexpr (CLAMP) {
+                const float dl = fminf(fmaxf(d * p.scale + tb.bias[row], -p.clamp), p.clamp);
+                cut = fabsf(dl) >= p.clamp;
+                pr = __builtin_amdgcn_exp2f(dl * kLog2e - tb.lse2[row]);
+            } else {
+                pr = __builtin_amdgcn_exp2f(__builtin_fmaf(d, c2, tb.bias[row]));
+            }
+            pr = has ? pr : 0.0f;
+            pbuf.v[0][w][0][lane][0] = cut ? -pr : pr;
+            add_row(tb.o, pr);
+        }
+        __syncthreads();   // alpha^ handed over
+        if (keyw) {
+            const float hv = pbuf.v[0][w][0][lane][0];
+            const float dsv = CLAMP && hv < 0.0f ? 0.0f : hv * (d - tb.r[row]);
+            add_row(tb.q, dsv);
+        }
+    };
+    if (has_par) partner_run(par_lo, par_hi);
+    if (has_par2) partner_run(par2_lo, par2_hi);
 
     // ---- store: lane (c, g) holds dims 32db + 8i + 4g + [0, 4) of key c ----
     // The accumulator goes out in whole rows: each wavefront writes half of
