@@ -4,7 +4,8 @@ gates; with and without the logit clamp; k on both sides of the
 small-window threshold; pi below, at and above k), the backward (bf16) and
 the index set, each against the oracle at its bar; random sequence shards
 (boundaries on or off the 128-query tile grid) through the shard calls; and
-random decode steps (per-sequence lengths from 0 to cap - 1).  The cases
+random decode steps (per-sequence lengths from 0 to cap - 1), and longer
+banded backward problems with partners outside the window.  The cases
 are drawn once from fixed seeds, so every run checks the same ones."""
 import numpy as np
 import pytest
@@ -58,6 +59,30 @@ def test_forward_sweep(device, c, dtype):
 def test_backward_sweep(device, c):
     if c["clamp"]:
         pytest.skip("the clamp's gradient cut is a discontinuity; clamp cases are placed by hand elsewhere")
+    cfg = W.ForwardConfig("custom", c["B"], c["H"], c["N"], c["D"], c["k"], c["pi"], torch.bfloat16)
+    q, k, v, gate = W.forward_inputs(cfg, c["seed"], device, per_query_gate=c["pq"])
+    check_backward(q, k, v, gate, c["k"], c["pi"], c["seed"], causal=c["causal"], per_head_sum=False)
+
+
+def draw_partner_cases(n, seed):
+    """Banded (k > 16) problems whose partners lie outside the window (pi > k),
+    with sequences long enough that whole partner runs of 128 queries occur."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for _ in range(n):
+        k = int(rng.choice([17, 24, 31, 40, 64, 100, 150, 300]))
+        pi = max(k + 1, int(rng.choice([k + 1, k + 5, 2 * k + 3, 97, 300, 700])))
+        cases.append(dict(B=int(rng.integers(1, 3)), H=int(rng.integers(1, 3)), N=int(rng.integers(40, 1600)),
+                          D=int(rng.choice([64, 128])), k=k, pi=pi, causal=bool(rng.integers(0, 2)),
+                          pq=bool(rng.integers(0, 2)), clamp=0.0, seed=int(rng.integers(0, 1 << 30))))
+    return cases
+
+
+PARTNER_CASES = draw_partner_cases(12, 20261203)
+
+
+@pytest.mark.parametrize("c", PARTNER_CASES, ids=ident)
+def test_backward_partner_sweep(device, c):
     cfg = W.ForwardConfig("custom", c["B"], c["H"], c["N"], c["D"], c["k"], c["pi"], torch.bfloat16)
     q, k, v, gate = W.forward_inputs(cfg, c["seed"], device, per_query_gate=c["pq"])
     check_backward(q, k, v, gate, c["k"], c["pi"], c["seed"], causal=c["causal"], per_head_sum=False)
